@@ -1,0 +1,78 @@
+"""Brute-force per-token mixer in pure Python, for tiny shapes only.
+
+TEST INFRASTRUCTURE ONLY: it exists to pin the numpy oracle (``oracle.mixer``) by an
+independent implementation. It is written with scalar loops and the ``math`` module,
+shares no code with the oracle or with the GPU path, and rounds nothing (exact float64
+arithmetic up to summation order).
+
+It walks one sequence token by token through the full-width (unsharded) mixer in the
+op order of Section II-B / Fig. 1, with the readings listed in ``oracle.mixer``: packed
+[x | z] and [delta | B | C], a causal K-tap convolution with bias and SiLU,
+Delta = softplus(dt_proj(delta) + b_dt), h <- exp(Delta*A) h + Delta*B*u,
+y = C.h + D*u, gate y*SiLU(z), output projection.
+"""
+from __future__ import annotations
+
+import math
+from typing import List, Optional, Sequence
+
+
+def _silu(v: float) -> float:
+    return v / (1.0 + math.exp(-v))
+
+
+def _softplus(v: float) -> float:
+    return v if v > 20.0 else math.log1p(math.exp(v))
+
+
+def _row(m, i) -> List[float]:
+    return [float(v) for v in m[i]]
+
+
+def mixer_sequence(w, x_rows: Sequence[Sequence[float]], conv_hist: Optional[Sequence[Sequence[float]]] = None,
+                   h0: Optional[Sequence[Sequence[float]]] = None):
+    """Run one sequence through the full-width layer.
+
+    w: dict of full-width weights (W_in [2E,dm], conv_w [E,K], conv_b [E], W_x [R+2N,E],
+    W_dt [E,R], b_dt [E], A_log [E,N], D [E], W_out [dm,E]).
+    x_rows: L rows of d_model values. conv_hist: [E][K-1] (oldest first) or None.
+    h0: [E][N] or None. Returns (y rows [L][dm], new conv_hist [E][K-1], h [E][N]).
+    """
+    E = len(w["conv_b"])
+    K = len(w["conv_w"][0])
+    N = len(w["A_log"][0])
+    R = len(w["W_dt"][0])
+    dm = len(w["W_out"])
+    hist = [[0.0] * (K - 1) for _ in range(E)] if conv_hist is None else [list(map(float, r)) for r in conv_hist]
+    h = [[0.0] * N for _ in range(E)] if h0 is None else [list(map(float, r)) for r in h0]
+    A = [[-math.exp(float(w["A_log"][c][n])) for n in range(N)] for c in range(E)]
+    ys = []
+    for x in x_rows:
+        # input projection: channel c of the SSM path uses row c, gate row E + c
+        xs = [sum(float(w["W_in"][c][k]) * float(x[k]) for k in range(dm)) for c in range(E)]
+        zs = [sum(float(w["W_in"][E + c][k]) * float(x[k]) for k in range(dm)) for c in range(E)]
+        # causal convolution over the window [hist..., current], tap K-1 on the current token
+        u = []
+        for c in range(E):
+            window = hist[c] + [xs[c]]
+            acc = float(w["conv_b"][c])
+            for j in range(K):
+                acc += float(w["conv_w"][c][j]) * window[j]
+            u.append(_silu(acc))
+            hist[c] = window[1:]
+        # packed token fields
+        W = R + 2 * N
+        dbl = [sum(float(w["W_x"][r][c]) * u[c] for c in range(E)) for r in range(W)]
+        delta_lr, Bt, Ct = dbl[:R], dbl[R:R + N], dbl[R + N:]
+        y_inner = []
+        for c in range(E):
+            dtc = sum(float(w["W_dt"][c][r]) * delta_lr[r] for r in range(R))
+            D_step = _softplus(dtc + float(w["b_dt"][c]))
+            acc = 0.0
+            for n in range(N):
+                h[c][n] = math.exp(D_step * A[c][n]) * h[c][n] + D_step * Bt[n] * u[c]
+                acc += Ct[n] * h[c][n]
+            acc += float(w["D"][c]) * u[c]
+            y_inner.append(acc * _silu(zs[c]))
+        ys.append([sum(float(w["W_out"][m][c]) * y_inner[c] for c in range(E)) for m in range(dm)])
+    return ys, hist, h
