@@ -1,0 +1,228 @@
+/*
+ * ssm_shard.h - C ABI of the selective-SSM (Mamba-1) mixer on one tensor-parallel
+ * channel shard, for AMD Instinct MI355X (gfx950).
+ *
+ * Source: "Scaling State-Space Models on Multiple GPUs with Tensor Parallelism".
+ *   - Section II-B / Fig. 1: the mixer's op order (in_proj, split into SSM and gate
+ *     paths, short channel-separable convolution, projection to packed Delta/B/C,
+ *     discretisation with per-channel A, state update with D skip, gate, out_proj).
+ *   - Section IV-A: the SSM cache = final recurrent state + last K-1 convolution
+ *     inputs per sequence, sharded by channel, written by prefill and read and
+ *     advanced by decode without rescanning the prompt.
+ *   - Section IV-B: channel-wise splitting; each rank owns a contiguous channel range;
+ *     exactly two reductions per block: after x_proj and at the residual boundary.
+ *   - Section IV-C: the packed [delta | B | C] parameters are unpacked by column
+ *     range; Delta is sharded with channels, B and C are complete on every rank after
+ *     the first reduction, A and D are per channel and local.
+ *
+ * Conventions (all entry points):
+ *   - Every tensor argument is DEVICE memory owned by the caller, row-major with the
+ *     last dimension contiguous, 16-byte aligned. The library never allocates; the
+ *     caller provides a workspace of at least the size the *_workspace_bytes query
+ *     returns. Inputs are never modified; cache pools are updated in place.
+ *   - "act" tensors hold the activation dtype of the descriptor (SSM_BF16 or SSM_F32).
+ *   - Calls are asynchronous on the given HIP stream (0 = the null stream).
+ *   - Return value: SSM_OK (0) or a negative SSM_E_* code. All argument checks happen
+ *     on the host before anything is enqueued; a failed check enqueues nothing.
+ *     ssm_last_error() gives a message for the calling thread's last failure.
+ *   - Per-sequence metadata (cu_seqlens, cache_slot, has_initial_state) is DEVICE
+ *     int32 memory so that calls can be enqueued without host round trips. Kernels
+ *     never index out of range with it: an out-of-range slot or a non-monotone
+ *     cu_seqlens entry makes the affected work a no-op and sets a bit in the
+ *     workspace status word (SSM_STATUS_*), read with ssm_shard_take_status().
+ *     ssm_shard_check_meta_host() validates host copies completely (including
+ *     duplicate slots, which the kernels cannot detect; duplicates in one call race).
+ *   - Cache layout: conv_pool [num_slots][E][K-1] act dtype, oldest input first;
+ *     ssm_pool [num_slots][E][N] float32. Slots not named in a call stay bit-identical.
+ */
+#ifndef SSM_SHARD_H
+#define SSM_SHARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSM_SHARD_ABI_VERSION 1
+
+/* Return codes. */
+#define SSM_OK 0
+#define SSM_E_INVAL (-1)     /* bad descriptor, shape, dtype or null pointer      */
+#define SSM_E_ALIGN (-2)     /* pointer or leading dimension not aligned          */
+#define SSM_E_WORKSPACE (-3) /* workspace smaller than the size query returned    */
+#define SSM_E_SLOT (-4)      /* cache slot out of range or duplicated (host check)*/
+#define SSM_E_SEQLENS (-5)   /* cu_seqlens not 0 = c0 <= c1 <= ... = T (host check)*/
+#define SSM_E_HIP (-6)       /* a HIP runtime call failed                          */
+
+/* Bits of the workspace status word, set by kernels that met bad device metadata. */
+#define SSM_STATUS_BAD_SLOT 1
+#define SSM_STATUS_BAD_SEQLENS 2
+
+/* Storage dtype of activations and act-typed weights. */
+typedef enum ssm_dtype { SSM_F32 = 0, SSM_BF16 = 1 } ssm_dtype_t;
+
+/* Shape of one layer and of the shard this rank owns (Section IV-B). The shard owns
+ * channels [shard_index * d_inner_shard, (shard_index + 1) * d_inner_shard).
+ * Requirements: d_inner_shard * shard_count == d_inner_total; d_state == 16;
+ * d_conv in [1, 4]; d_model, d_inner_shard and dt_rank multiples of 16. */
+typedef struct ssm_shard_desc {
+    int32_t d_model;        /* residual width                                   */
+    int32_t d_inner_total;  /* E_tot, intermediate channels of the whole layer  */
+    int32_t d_inner_shard;  /* E, channels of this shard                        */
+    int32_t d_state;        /* N, states per channel                            */
+    int32_t dt_rank;        /* R, width of the low-rank step-size input         */
+    int32_t d_conv;         /* K, convolution taps                              */
+    int32_t shard_index;    /* this rank                                        */
+    int32_t shard_count;    /* P, channel-split degree                          */
+    int32_t act_dtype;      /* ssm_dtype_t                                      */
+} ssm_shard_desc_t;
+
+/* One shard's weights (device pointers), already sliced to the shard's channels.
+ *   in_proj_w  [2E][d_model] act: rows 0..E-1 feed the SSM path, rows E..2E-1 the gate
+ *   conv_w     [E][K] act, conv_b [E] act (tap K-1 multiplies the current token)
+ *   x_proj_w   [R+2N][E] act: output columns are [delta | B | C]
+ *   dt_proj_w  [E][R] act, dt_proj_b [E] float32
+ *   A_log      [E][N] float32 (A = -exp(A_log)), D [E] float32
+ *   out_proj_w [d_model][E] act */
+typedef struct ssm_shard_weights {
+    const void* in_proj_w;
+    const void* conv_w;
+    const void* conv_b;
+    const void* x_proj_w;
+    const void* dt_proj_w;
+    const void* out_proj_w;
+    const float* dt_proj_b;
+    const float* A_log;
+    const float* D;
+} ssm_shard_weights_t;
+
+/* Packed variable-length batch (device int32 arrays).
+ *   cu_seqlens [nseq+1]: sequence i occupies packed tokens [cu_seqlens[i], cu_seqlens[i+1])
+ *   cache_slot [nseq]: pool slot of sequence i
+ *   has_initial_state [nseq]: 1 = continue from the slot's cached conv history and
+ *     state (a chunk of a longer prompt), 0 = start from zeros. */
+typedef struct ssm_seq_meta {
+    const int32_t* cu_seqlens;
+    const int32_t* cache_slot;
+    const int32_t* has_initial_state;
+    int32_t nseq;
+} ssm_seq_meta_t;
+
+/* ---------------------------------------------------------------- housekeeping */
+int ssm_shard_abi_version(void);
+/* Message for the calling thread's most recent failure ("" if none). */
+const char* ssm_last_error(void);
+/* Checks a descriptor; SSM_OK or SSM_E_INVAL. */
+int ssm_shard_check_desc(const ssm_shard_desc_t* desc);
+/* Host-side check of HOST copies of the metadata: cu_seqlens[0] == 0, non-decreasing,
+ * cu_seqlens[nseq] == T; every slot in [0, num_slots) and no slot repeated;
+ * has_initial_state entries 0 or 1. Returns SSM_OK, SSM_E_SEQLENS, SSM_E_SLOT or SSM_E_INVAL. */
+int ssm_shard_check_meta_host(const int32_t* cu_seqlens, const int32_t* cache_slot,
+                              const int32_t* has_initial_state, int32_t nseq, int64_t T,
+                              int32_t num_slots);
+
+/* Workspace sizes. A prefill workspace serves every call with T <= max_tokens and
+ * nseq <= max_seqs; a decode workspace serves batches up to max_batch. */
+int ssm_shard_prefill_workspace_bytes(const ssm_shard_desc_t* desc, int64_t max_tokens,
+                                      int32_t max_seqs, size_t* bytes);
+int ssm_shard_decode_workspace_bytes(const ssm_shard_desc_t* desc, int32_t max_batch, size_t* bytes);
+/* Zero the workspace status word (call once after allocating a workspace). */
+int ssm_shard_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+/* Synchronise the stream, read the status word into *status and clear it. */
+int ssm_shard_take_status(void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------ prefill
+ * ssm_shard_prefill: the whole shard over a packed batch of T tokens.
+ *   x [T][d_model] act -> y_partial [T][d_model] act, this shard's out_proj partial sum
+ *   (the second reduction, at the residual boundary, is the caller's).
+ * Writes conv_pool[slot] and ssm_pool[slot] of every sequence in meta.
+ * The first reduction (x_proj sum over ranks) is taken as the identity: exact when
+ * shard_count == 1; with several shards use the two stages below. */
+int ssm_shard_prefill(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                      const void* x, int64_t T, const ssm_seq_meta_t* meta,
+                      void* conv_pool, float* ssm_pool, int32_t num_slots,
+                      void* y_partial, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stage 1: in_proj, causal conv1d + SiLU (writes conv_pool), x_proj.
+ *   x_dbl_partial [T][R+2N] float32 out: this shard's partial x_proj output.
+ * Keeps xz and u in ws for stage 2 (pass the same ws, T and meta to stage 2). */
+int ssm_shard_prefill_stage1(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                             const void* x, int64_t T, const ssm_seq_meta_t* meta,
+                             void* conv_pool, int32_t num_slots, float* x_dbl_partial,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+/* Stage 2: from the x_proj output summed over all shards (x_dbl [T][R+2N] float32):
+ * dt_proj, selective scan with D skip and gate (writes ssm_pool), out_proj. */
+int ssm_shard_prefill_stage2(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                             const float* x_dbl, int64_t T, const ssm_seq_meta_t* meta,
+                             float* ssm_pool, int32_t num_slots, void* y_partial,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------- decode
+ * One token for each of `batch` sequences, advancing their cached history and state
+ * in place (Section IV-A). cache_slot [batch] device int32, distinct.
+ *   x_t [batch][d_model] act -> y_partial [batch][d_model] act. */
+int ssm_shard_decode_step(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                          const void* x_t, int32_t batch, const int32_t* cache_slot,
+                          void* conv_pool, float* ssm_pool, int32_t num_slots,
+                          void* y_partial, void* ws, size_t ws_bytes, hipStream_t stream);
+int ssm_shard_decode_stage1(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                            const void* x_t, int32_t batch, const int32_t* cache_slot,
+                            void* conv_pool, int32_t num_slots, float* x_dbl_partial,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+int ssm_shard_decode_stage2(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                            const float* x_dbl, int32_t batch, const int32_t* cache_slot,
+                            float* ssm_pool, int32_t num_slots, void* y_partial,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ utilities
+ * Channel splitter (Section IV-B): copy this shard's slices of full-width weights
+ * (full: same fields at full width, E_tot channels) into caller-allocated shard
+ * buffers (out: fields point to writable device memory of the shard shapes).
+ * in_proj's x rows and z rows are sliced separately; x_proj and out_proj by column. */
+int ssm_shard_slice_weights(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* full,
+                            const ssm_shard_weights_t* out, hipStream_t stream);
+/* dst[i] += src[i] for i < n (float32): the x_proj exchange when all shards run on one GPU. */
+int ssm_reduce_add_f32(float* dst, const float* src, int64_t n, hipStream_t stream);
+
+/* ------------------------------------------------------- stage operators
+ * The kernels the entry points above are built from, exposed for kernel-level checks.
+ *
+ * C[M][N] = A[M][K] * B[N][K]^T, float32 accumulation. a_dtype, b_dtype, c_dtype are
+ * ssm_dtype_t. With b_dtype == SSM_BF16 the product runs on bf16 matrix cores and a
+ * float32 A is rounded to bf16 (ties to even) as it is loaded; with b_dtype == SSM_F32
+ * both operands must be float32. K, lda, ldb multiples of 8; ldc a multiple of 4. */
+int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t a_dtype,
+                const void* B, int64_t ldb, int32_t b_dtype, void* C, int64_t ldc, int32_t c_dtype,
+                hipStream_t stream);
+/* Causal depthwise conv1d + SiLU over a packed batch: reads the SSM half of
+ * xz [T][2E] (columns 0..E-1), writes u [T][E] act and the new conv history. */
+int ssm_conv1d_silu(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, const void* xz,
+                    int64_t T, const ssm_seq_meta_t* meta, void* conv_pool, int32_t num_slots,
+                    void* u, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Selective scan: Delta = softplus(dt + dt_proj_b), h <- exp(Delta*A) h + Delta*B*u,
+ * y = C.h + D*u, g = y * SiLU(z). u, dt [T][E] act; z = columns E..2E-1 of xz [T][2E];
+ * B, C = columns R..R+N-1 and R+N..R+2N-1 of x_dbl [T][R+2N] float32.
+ * Writes g [T][E] act and ssm_pool[slot] of every sequence. */
+int ssm_selective_scan(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                       const void* u, const void* dt, const void* xz, const float* x_dbl,
+                       int64_t T, const ssm_seq_meta_t* meta, float* ssm_pool, int32_t num_slots,
+                       void* g, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Decode: shift each sequence's cached window by the new token (column c of xz) and
+ * convolve: u [batch][E]; conv_pool updated in place. */
+int ssm_decode_conv(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, const void* xz,
+                    int32_t batch, const int32_t* cache_slot, void* conv_pool, int32_t num_slots,
+                    void* u, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Decode: one recurrence step per sequence on ssm_pool[slot] in place, with D skip and
+ * gate; same operand layout as ssm_selective_scan with T = batch. */
+int ssm_decode_ssm(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, const void* u,
+                   const void* dt, const void* xz, const float* x_dbl, int32_t batch,
+                   const int32_t* cache_slot, float* ssm_pool, int32_t num_slots, void* g,
+                   void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SSM_SHARD_H */

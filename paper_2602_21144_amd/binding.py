@@ -1,0 +1,304 @@
+"""ctypes binding of ``libssm_shard.so`` (declared in include/ssm_shard.h).
+
+Argument marshalling only: torch tensors supply device memory and the current HIP
+stream; every step of the mixer runs in the library's gfx950 kernels. There is no
+fallback: if the library is missing, loading it raises.
+
+Function names follow the C ABI; tensors replace pointer + size arguments.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from .synth import LayerShape
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libssm_shard.so")
+
+SSM_F32, SSM_BF16 = 0, 1
+SSM_OK = 0
+ERRORS = {-1: "SSM_E_INVAL", -2: "SSM_E_ALIGN", -3: "SSM_E_WORKSPACE", -4: "SSM_E_SLOT",
+          -5: "SSM_E_SEQLENS", -6: "SSM_E_HIP"}
+SSM_STATUS_BAD_SLOT, SSM_STATUS_BAD_SEQLENS = 1, 2
+
+
+class SsmError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "d_model", "d_inner_total", "d_inner_shard", "d_state", "dt_rank", "d_conv",
+        "shard_index", "shard_count", "act_dtype")]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "in_proj_w", "conv_w", "conv_b", "x_proj_w", "dt_proj_w", "out_proj_w",
+        "dt_proj_b", "A_log", "D")]
+
+
+class SeqMetaC(ctypes.Structure):
+    _fields_ = [("cu_seqlens", ctypes.c_void_p), ("cache_slot", ctypes.c_void_p),
+                ("has_initial_state", ctypes.c_void_p), ("nseq", ctypes.c_int32)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+_P, _I32, _I64, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+_SIGS = {
+    "ssm_shard_abi_version": ([], _I32),
+    "ssm_last_error": ([], ctypes.c_char_p),
+    "ssm_shard_check_desc": ([_P], _I32),
+    "ssm_shard_check_meta_host": ([_P, _P, _P, _I32, _I64, _I32], _I32),
+    "ssm_shard_prefill_workspace_bytes": ([_P, _I64, _I32, _P], _I32),
+    "ssm_shard_decode_workspace_bytes": ([_P, _I32, _P], _I32),
+    "ssm_shard_workspace_init": ([_P, _SZ, _P], _I32),
+    "ssm_shard_take_status": ([_P, _SZ, _P, _P], _I32),
+    "ssm_shard_prefill": ([_P, _P, _P, _I64, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_prefill_stage1": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_prefill_stage2": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_decode_step": ([_P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_decode_stage1": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_decode_stage2": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_slice_weights": ([_P, _P, _P, _P], _I32),
+    "ssm_reduce_add_f32": ([_P, _P, _I64, _P], _I32),
+    "ssm_gemm_nt": ([_I64, _I64, _I64, _P, _I64, _I32, _P, _I64, _I32, _P, _I64, _I32, _P], _I32),
+    "ssm_conv1d_silu": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_selective_scan": ([_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_decode_conv": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_decode_ssm": ([_P, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2602_21144_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes, f.restype = args, res
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != SSM_OK:
+        raise SsmError(rc, lib().ssm_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensor expected")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor expected")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def torch_act(act: str):
+    return torch.bfloat16 if act == "bf16" else torch.float32
+
+
+def make_desc(shape: LayerShape, shard_index: int = 0) -> Desc:
+    d = Desc(shape.d_model, shape.d_inner, shape.d_shard, shape.d_state, shape.dt_rank, shape.d_conv,
+             shard_index, shape.shard_count, SSM_BF16 if shape.act == "bf16" else SSM_F32)
+    _check(lib().ssm_shard_check_desc(ctypes.byref(d)))
+    return d
+
+
+_WKEYS = {"in_proj_w": "W_in", "conv_w": "conv_w", "conv_b": "conv_b", "x_proj_w": "W_x", "dt_proj_w": "W_dt",
+          "out_proj_w": "W_out", "dt_proj_b": "b_dt", "A_log": "A_log", "D": "D"}
+_F32_KEYS = ("b_dt", "A_log", "D")
+
+
+def upload_weights(host: Dict[str, np.ndarray], act: str, device="cuda") -> Dict[str, torch.Tensor]:
+    """Copy host weights (float32 arrays, act-typed ones already representable) to the device."""
+    out = {}
+    for k in _WKEYS.values():
+        dt = torch.float32 if k in _F32_KEYS else torch_act(act)
+        out[k] = torch.from_numpy(np.ascontiguousarray(host[k], np.float32)).to(device=device, dtype=dt)
+    return out
+
+
+def weights_struct(dev: Dict[str, torch.Tensor]) -> Weights:
+    return Weights(*[_ptr(dev[_WKEYS[f]]) for f, _ in Weights._fields_])
+
+
+def empty_shard_weights(shape: LayerShape, device="cuda") -> Dict[str, torch.Tensor]:
+    E, dm, N, R, K = shape.d_shard, shape.d_model, shape.d_state, shape.dt_rank, shape.d_conv
+    a = torch_act(shape.act)
+    f = torch.float32
+    shapes = {"W_in": ((2 * E, dm), a), "conv_w": ((E, K), a), "conv_b": ((E,), a), "W_x": ((R + 2 * N, E), a),
+              "W_dt": ((E, R), a), "W_out": ((dm, E), a), "b_dt": ((E,), f), "A_log": ((E, N), f), "D": ((E,), f)}
+    return {k: torch.empty(s, dtype=t, device=device) for k, (s, t) in shapes.items()}
+
+
+def ssm_shard_slice_weights(desc: Desc, full: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor], stream=None):
+    fw, ow = weights_struct(full), weights_struct(out)
+    _check(lib().ssm_shard_slice_weights(ctypes.byref(desc), ctypes.byref(fw), ctypes.byref(ow), _stream(stream)))
+
+
+class SeqMeta:
+    """Device-resident packed-batch metadata (int32), validated from its host copy."""
+
+    def __init__(self, cu_seqlens, cache_slot, has_initial_state, num_slots: int, device="cuda"):
+        cu = np.ascontiguousarray(cu_seqlens, np.int32)
+        sl = np.ascontiguousarray(cache_slot, np.int32)
+        hi = np.ascontiguousarray(has_initial_state, np.int32)
+        self.nseq = int(sl.shape[0])
+        self.T = int(cu[-1]) if cu.size else 0
+        _check(lib().ssm_shard_check_meta_host(cu.ctypes.data, sl.ctypes.data, hi.ctypes.data, self.nseq,
+                                               self.T, int(num_slots)))
+        self.host = (cu, sl, hi)
+        n = max(self.nseq, 1)
+        self.cu = torch.zeros(n + 1, dtype=torch.int32, device=device)
+        self.slot = torch.zeros(n, dtype=torch.int32, device=device)
+        self.has_init = torch.zeros(n, dtype=torch.int32, device=device)
+        if self.nseq:
+            self.cu.copy_(torch.from_numpy(cu))
+            self.slot.copy_(torch.from_numpy(sl))
+            self.has_init.copy_(torch.from_numpy(hi))
+        self.c = SeqMetaC(self.cu.data_ptr(), self.slot.data_ptr(), self.has_init.data_ptr(), self.nseq)
+
+
+def prefill_workspace_bytes(desc: Desc, max_tokens: int, max_seqs: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_shard_prefill_workspace_bytes(ctypes.byref(desc), max_tokens, max_seqs, ctypes.byref(n)))
+    return n.value
+
+
+def decode_workspace_bytes(desc: Desc, max_batch: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_shard_decode_workspace_bytes(ctypes.byref(desc), max_batch, ctypes.byref(n)))
+    return n.value
+
+
+def workspace(nbytes: int, device="cuda", stream=None) -> torch.Tensor:
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    _check(lib().ssm_shard_workspace_init(_ptr(ws), ws.numel(), _stream(stream)))
+    return ws
+
+
+def take_status(ws: torch.Tensor, stream=None) -> int:
+    v = ctypes.c_int32()
+    _check(lib().ssm_shard_take_status(_ptr(ws), ws.numel(), ctypes.byref(v), _stream(stream)))
+    return v.value
+
+
+def _w(weights):
+    return weights if isinstance(weights, Weights) else weights_struct(weights)
+
+
+def ssm_shard_prefill(desc, weights, x, meta: SeqMeta, conv_pool, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_prefill(ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c),
+                                   _ptr(conv_pool), _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _ptr(ws),
+                                   ws.numel(), _stream(stream)))
+
+
+def ssm_shard_prefill_stage1(desc, weights, x, meta: SeqMeta, conv_pool, x_dbl_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_prefill_stage1(ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c),
+                                          _ptr(conv_pool), conv_pool.shape[0], _ptr(x_dbl_partial), _ptr(ws),
+                                          ws.numel(), _stream(stream)))
+
+
+def ssm_shard_prefill_stage2(desc, weights, x_dbl, meta: SeqMeta, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_prefill_stage2(ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), meta.T,
+                                          ctypes.byref(meta.c), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(y_partial),
+                                          _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_shard_decode_step(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_decode_step(ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0],
+                                       _ptr(cache_slot), _ptr(conv_pool), _ptr(ssm_pool), conv_pool.shape[0],
+                                       _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_decode_stage1(ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0],
+                                         _ptr(cache_slot), _ptr(conv_pool), conv_pool.shape[0], _ptr(x_dbl_partial),
+                                         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_shard_decode_stage2(desc, weights, x_dbl, cache_slot, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_shard_decode_stage2(ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), x_dbl.shape[0],
+                                         _ptr(cache_slot), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(y_partial),
+                                         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_reduce_add_f32(dst, src, stream=None):
+    assert dst.dtype == torch.float32 and src.dtype == torch.float32 and dst.numel() == src.numel()
+    _check(lib().ssm_reduce_add_f32(_ptr(dst), _ptr(src), dst.numel(), _stream(stream)))
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SSM_F32
+    if t.dtype == torch.bfloat16:
+        return SSM_BF16
+    raise ValueError(t.dtype)
+
+
+def ssm_gemm_nt(A, B, C, stream=None):
+    """C[M][N] = A[M][K] B[N][K]^T on the library's GEMM kernels (row strides from the tensors)."""
+    M, K = A.shape
+    N = B.shape[0]
+    assert B.shape[1] == K and C.shape == (M, N)
+    for t in (A, B, C):
+        assert t.stride(1) == 1
+    _check(lib().ssm_gemm_nt(M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0), _dt(A),
+                             ctypes.c_void_p(B.data_ptr()), B.stride(0), _dt(B), ctypes.c_void_p(C.data_ptr()),
+                             C.stride(0), _dt(C), _stream(stream)))
+
+
+def ssm_conv1d_silu(desc, weights, xz, meta: SeqMeta, conv_pool, u, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_conv1d_silu(ctypes.byref(desc), ctypes.byref(w), _ptr(xz), meta.T, ctypes.byref(meta.c),
+                                 _ptr(conv_pool), conv_pool.shape[0], _ptr(u), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_selective_scan(desc, weights, u, dt, xz, x_dbl, meta: SeqMeta, ssm_pool, g, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_selective_scan(ctypes.byref(desc), ctypes.byref(w), _ptr(u), _ptr(dt), _ptr(xz), _ptr(x_dbl),
+                                    meta.T, ctypes.byref(meta.c), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(g),
+                                    _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_decode_conv(desc, weights, xz, cache_slot, conv_pool, u, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_decode_conv(ctypes.byref(desc), ctypes.byref(w), _ptr(xz), xz.shape[0], _ptr(cache_slot),
+                                 _ptr(conv_pool), conv_pool.shape[0], _ptr(u), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def ssm_decode_ssm(desc, weights, u, dt, xz, x_dbl, cache_slot, ssm_pool, g, ws, stream=None):
+    w = _w(weights)
+    _check(lib().ssm_decode_ssm(ctypes.byref(desc), ctypes.byref(w), _ptr(u), _ptr(dt), _ptr(xz), _ptr(x_dbl),
+                                u.shape[0], _ptr(cache_slot), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(g), _ptr(ws),
+                                ws.numel(), _stream(stream)))
+
+
+def scan_scratch_workspace_bytes(desc: Desc, T: int, nseq: int) -> int:
+    """Workspace large enough for ssm_selective_scan at (T, nseq) (header + scan scratch)."""
+    return prefill_workspace_bytes(desc, T, nseq)

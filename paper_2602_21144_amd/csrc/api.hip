@@ -1,0 +1,541 @@
+// C ABI of the mixer shard: argument checks (host only, before anything is enqueued),
+// workspace layout and the order of kernels for prefill and decode.
+//
+// Prefill (Section II-B order; Section IV-B reductions):
+//   stage 1: in_proj GEMM -> xz; conv1d+SiLU -> u (and the conv history); x_proj GEMM -> x_dbl
+//   [first reduction over shards: the caller's]
+//   stage 2: dt_proj GEMM -> dt; selective scan -> g (and the final states); out_proj GEMM -> y
+// Decode: the same with one token per sequence and the single-step kernels.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace ssm;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(SSM_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define SSM_TRY_HIP(expr, what)                          \
+    do {                                                 \
+        hipError_t e_ = (expr);                          \
+        if (e_ != hipSuccess) return hip_fail(e_, what); \
+    } while (0)
+
+#define SSM_TRY(expr)            \
+    do {                         \
+        int r_ = (expr);         \
+        if (r_ != SSM_OK) return r_; \
+    } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t act_bytes(const ssm_shard_desc_t* d) { return d->act_dtype == SSM_BF16 ? 2 : 4; }
+
+int check_desc(const ssm_shard_desc_t* d) {
+    if (!d) return fail(SSM_E_INVAL, "desc is null");
+    if (d->act_dtype != SSM_F32 && d->act_dtype != SSM_BF16) return fail(SSM_E_INVAL, "act_dtype %d", d->act_dtype);
+    if (d->d_model <= 0 || d->d_model % 16) return fail(SSM_E_INVAL, "d_model %d must be a positive multiple of 16", d->d_model);
+    if (d->d_inner_shard <= 0 || d->d_inner_shard % 64)
+        return fail(SSM_E_INVAL, "d_inner_shard %d must be a positive multiple of 64", d->d_inner_shard);
+    if (d->shard_count <= 0 || d->shard_index < 0 || d->shard_index >= d->shard_count)
+        return fail(SSM_E_INVAL, "shard %d of %d", d->shard_index, d->shard_count);
+    if ((int64_t)d->d_inner_shard * d->shard_count != d->d_inner_total)
+        return fail(SSM_E_INVAL, "d_inner_shard %d * shard_count %d != d_inner_total %d", d->d_inner_shard,
+                    d->shard_count, d->d_inner_total);
+    if (d->d_state != kN) return fail(SSM_E_INVAL, "d_state %d: the kernels are built for %d", d->d_state, kN);
+    if (d->dt_rank <= 0 || d->dt_rank % 16) return fail(SSM_E_INVAL, "dt_rank %d must be a positive multiple of 16", d->dt_rank);
+    if (d->d_conv < 1 || d->d_conv > kMaxConv) return fail(SSM_E_INVAL, "d_conv %d not in [1, %d]", d->d_conv, kMaxConv);
+    return SSM_OK;
+}
+
+int check_weights(const ssm_shard_weights_t* w) {
+    if (!w) return fail(SSM_E_INVAL, "weights is null");
+    const void* ps[] = {w->in_proj_w, w->conv_w, w->conv_b, w->x_proj_w, w->dt_proj_w,
+                        w->out_proj_w, w->dt_proj_b, w->A_log, w->D};
+    const char* names[] = {"in_proj_w", "conv_w", "conv_b", "x_proj_w", "dt_proj_w",
+                           "out_proj_w", "dt_proj_b", "A_log", "D"};
+    for (int i = 0; i < 9; ++i) {
+        if (!ps[i]) return fail(SSM_E_INVAL, "weights.%s is null", names[i]);
+        if (!aligned16(ps[i])) return fail(SSM_E_ALIGN, "weights.%s is not 16-byte aligned", names[i]);
+    }
+    return SSM_OK;
+}
+
+int check_ptr(const void* p, const char* name) {
+    if (!p) return fail(SSM_E_INVAL, "%s is null", name);
+    if (!aligned16(p)) return fail(SSM_E_ALIGN, "%s is not 16-byte aligned", name);
+    return SSM_OK;
+}
+
+int check_meta(const ssm_seq_meta_t* m, int64_t T) {
+    if (!m) return fail(SSM_E_INVAL, "meta is null");
+    if (m->nseq < 0) return fail(SSM_E_INVAL, "nseq %d", m->nseq);
+    if (m->nseq == 0 && T != 0) return fail(SSM_E_SEQLENS, "T = %lld tokens but no sequences", (long long)T);
+    if (m->nseq > 0 && (!m->cu_seqlens || !m->cache_slot || !m->has_initial_state))
+        return fail(SSM_E_INVAL, "meta arrays must be non-null");
+    return SSM_OK;
+}
+
+// ------------------------------------------------------------------ workspaces
+struct PrefillWs {
+    int32_t* status;
+    char *xz, *u, *dt, *g;
+    float* xdbl;
+    char* scan;
+    size_t total;
+};
+
+PrefillWs prefill_layout(const ssm_shard_desc_t* d, int64_t T, int nseq, void* base) {
+    const size_t s = act_bytes(d);
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state;
+    PrefillWs L{};
+    char* b = (char*)base;
+    size_t off = kWsHeader;
+    auto take = [&](size_t bytes) { char* p = b ? b + off : nullptr; off += align256(bytes); return p; };
+    L.status = (int32_t*)b;
+    L.xz = take((size_t)T * 2 * E * s);
+    L.u = take((size_t)T * E * s);
+    L.xdbl = (float*)take((size_t)T * W * 4);
+    L.dt = take((size_t)T * E * s);
+    L.g = take((size_t)T * E * s);
+    L.scan = take(scan_scratch_bytes(T, (int)E, nseq));
+    L.total = off;
+    return L;
+}
+
+struct DecodeWs {
+    int32_t* status;
+    char *xz, *u, *dt, *g;
+    float* xdbl;
+    size_t total;
+};
+
+DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
+    const size_t s = act_bytes(d);
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state;
+    DecodeWs L{};
+    char* b = (char*)base;
+    size_t off = kWsHeader;
+    auto take = [&](size_t bytes) { char* p = b ? b + off : nullptr; off += align256(bytes); return p; };
+    L.status = (int32_t*)b;
+    L.xz = take((size_t)B * 2 * E * s);
+    L.u = take((size_t)B * E * s);
+    L.xdbl = (float*)take((size_t)B * W * 4);
+    L.dt = take((size_t)B * E * s);
+    L.g = take((size_t)B * E * s);
+    L.total = off;
+    return L;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+    if (!ws) return fail(SSM_E_INVAL, "workspace is null");
+    if (!aligned16(ws)) return fail(SSM_E_ALIGN, "workspace is not 16-byte aligned");
+    if (have < need) return fail(SSM_E_WORKSPACE, "workspace %zu bytes < %zu needed", have, need);
+    return SSM_OK;
+}
+
+int gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int adt, const void* B, int64_t ldb, int bdt,
+         void* C, int64_t ldc, int cdt, hipStream_t s, const char* what) {
+    SSM_TRY_HIP(launch_gemm_nt(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s), what);
+    return SSM_OK;
+}
+
+ConvArgs conv_args(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int64_t T,
+                   const int32_t* cu, const int32_t* slot, const int32_t* hi, int nseq, void* conv_pool, int S,
+                   void* u, int32_t* status) {
+    ConvArgs a{};
+    a.xz = xz; a.ld_xz = 2 * (int64_t)d->d_inner_shard;
+    a.w = w->conv_w; a.b = w->conv_b; a.u = u; a.conv_pool = conv_pool;
+    a.cu = cu; a.slot = slot; a.has_init = hi; a.status = status;
+    a.T = T; a.E = d->d_inner_shard; a.K = d->d_conv; a.nseq = nseq; a.S = S;
+    return a;
+}
+
+ScanArgs scan_args(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* u, const void* dt,
+                   const void* xz, const float* xdbl, int64_t T, const int32_t* cu, const int32_t* slot,
+                   const int32_t* hi, int nseq, float* pool, int S, void* g, int32_t* status, void* scratch) {
+    ScanArgs a{};
+    const int64_t E = d->d_inner_shard;
+    a.u = u; a.dt = dt;
+    a.z = (const char*)xz + E * act_bytes(d); a.ld_z = 2 * E;
+    a.xdbl = xdbl; a.ld_xdbl = d->dt_rank + 2 * d->d_state; a.R = d->dt_rank;
+    a.b_dt = w->dt_proj_b; a.A_log = w->A_log; a.D = w->D;
+    a.g = g; a.pool = pool; a.cu = cu; a.slot = slot; a.has_init = hi; a.status = status;
+    a.h_local = (float*)scratch;
+    a.T = T; a.E = (int)E; a.nseq = nseq; a.S = S;
+    a.win = scan_window_len(T, (int)E);
+    return a;
+}
+
+int common_checks(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, int64_t T, int32_t S) {
+    SSM_TRY(check_desc(d));
+    SSM_TRY(check_weights(w));
+    if (T < 0 || T > INT32_MAX) return fail(SSM_E_INVAL, "token count %lld", (long long)T);
+    if (S <= 0) return fail(SSM_E_INVAL, "num_slots %d", S);
+    return SSM_OK;
+}
+
+// stage bodies (arguments already checked)
+int prefill1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int64_t T,
+             const ssm_seq_meta_t* m, void* conv_pool, int32_t S, float* xdbl, const PrefillWs& L, hipStream_t s) {
+    const int adt = d->act_dtype;
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
+    SSM_TRY(gemm(T, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "in_proj"));
+    ConvArgs ca = conv_args(d, w, L.xz, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq, conv_pool,
+                            S, L.u, L.status);
+    SSM_TRY_HIP(launch_conv_prefill(ca, adt == SSM_BF16, s), "conv1d");
+    SSM_TRY_HIP(launch_conv_state_update(ca, adt == SSM_BF16, s), "conv history");
+    SSM_TRY(gemm(T, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "x_proj"));
+    return SSM_OK;
+}
+
+int prefill2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float* xdbl, int64_t T,
+             const ssm_seq_meta_t* m, float* ssm_pool, int32_t S, void* y, const PrefillWs& L, hipStream_t s) {
+    const int adt = d->act_dtype;
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
+    SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "dt_proj"));
+    ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, T, m->cu_seqlens, m->cache_slot, m->has_initial_state,
+                            m->nseq, ssm_pool, S, L.g, L.status, L.scan);
+    SSM_TRY_HIP(launch_scan_prefill(sa, adt == SSM_BF16, s), "selective scan");
+    SSM_TRY(gemm(T, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "out_proj"));
+    return SSM_OK;
+}
+
+int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int32_t B, const int32_t* slot,
+            void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
+    const int adt = d->act_dtype;
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
+    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "in_proj"));
+    ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
+    SSM_TRY_HIP(launch_conv_decode(ca, adt == SSM_BF16, s), "decode conv");
+    SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "x_proj"));
+    return SSM_OK;
+}
+
+int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float* xdbl, int32_t B,
+            const int32_t* slot, float* ssm_pool, int32_t S, void* y, const DecodeWs& L, hipStream_t s) {
+    const int adt = d->act_dtype;
+    const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
+    SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "dt_proj"));
+    ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, B, nullptr, slot, nullptr, B, ssm_pool, S, L.g, L.status,
+                            nullptr);
+    SSM_TRY_HIP(launch_decode_ssm(sa, adt == SSM_BF16, s), "decode state update");
+    SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "out_proj"));
+    return SSM_OK;
+}
+
+int prefill_checks(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, int64_t T, const ssm_seq_meta_t* m,
+                   int32_t S, void* ws, size_t ws_bytes, PrefillWs* L) {
+    SSM_TRY(common_checks(d, w, T, S));
+    SSM_TRY(check_meta(m, T));
+    *L = prefill_layout(d, T, m->nseq, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L->total));
+    *L = prefill_layout(d, T, m->nseq, ws);
+    return SSM_OK;
+}
+
+int decode_checks(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, int32_t B, const int32_t* slot, int32_t S,
+                  void* ws, size_t ws_bytes, DecodeWs* L) {
+    SSM_TRY(common_checks(d, w, B, S));
+    if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
+    if (B > 0 && !slot) return fail(SSM_E_INVAL, "cache_slot is null");
+    *L = decode_layout(d, B, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L->total));
+    *L = decode_layout(d, B, ws);
+    return SSM_OK;
+}
+
+}  // namespace
+
+// ======================================================================= C ABI
+extern "C" {
+
+int ssm_shard_abi_version(void) { return SSM_SHARD_ABI_VERSION; }
+
+const char* ssm_last_error(void) { return g_err.c_str(); }
+
+int ssm_shard_check_desc(const ssm_shard_desc_t* desc) { return check_desc(desc); }
+
+int ssm_shard_check_meta_host(const int32_t* cu, const int32_t* slot, const int32_t* hi, int32_t nseq, int64_t T,
+                              int32_t num_slots) {
+    if (nseq < 0) return fail(SSM_E_INVAL, "nseq %d", nseq);
+    if (nseq == 0) return T == 0 ? SSM_OK : fail(SSM_E_SEQLENS, "T = %lld tokens but no sequences", (long long)T);
+    if (!cu || !slot || !hi) return fail(SSM_E_INVAL, "metadata arrays must be non-null");
+    if (cu[0] != 0) return fail(SSM_E_SEQLENS, "cu_seqlens[0] = %d, expected 0", cu[0]);
+    for (int i = 0; i < nseq; ++i)
+        if (cu[i + 1] < cu[i]) return fail(SSM_E_SEQLENS, "cu_seqlens decreases at %d", i + 1);
+    if ((int64_t)cu[nseq] != T) return fail(SSM_E_SEQLENS, "cu_seqlens[nseq] = %d, expected T = %lld", cu[nseq], (long long)T);
+    if (num_slots <= 0) return fail(SSM_E_INVAL, "num_slots %d", num_slots);
+    std::vector<char> seen((size_t)num_slots, 0);
+    for (int i = 0; i < nseq; ++i) {
+        if (slot[i] < 0 || slot[i] >= num_slots) return fail(SSM_E_SLOT, "cache_slot[%d] = %d not in [0, %d)", i, slot[i], num_slots);
+        if (seen[(size_t)slot[i]]) return fail(SSM_E_SLOT, "cache_slot %d used twice", slot[i]);
+        seen[(size_t)slot[i]] = 1;
+        if (hi[i] != 0 && hi[i] != 1) return fail(SSM_E_INVAL, "has_initial_state[%d] = %d", i, hi[i]);
+    }
+    return SSM_OK;
+}
+
+int ssm_shard_prefill_workspace_bytes(const ssm_shard_desc_t* desc, int64_t max_tokens, int32_t max_seqs, size_t* bytes) {
+    SSM_TRY(check_desc(desc));
+    if (!bytes || max_tokens < 0 || max_tokens > INT32_MAX || max_seqs < 0) return fail(SSM_E_INVAL, "bad size query");
+    *bytes = prefill_layout(desc, max_tokens, max_seqs, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm_shard_decode_workspace_bytes(const ssm_shard_desc_t* desc, int32_t max_batch, size_t* bytes) {
+    SSM_TRY(check_desc(desc));
+    if (!bytes || max_batch < 0) return fail(SSM_E_INVAL, "bad size query");
+    *bytes = decode_layout(desc, max_batch, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm_shard_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
+    SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    SSM_TRY_HIP(launch_fill_zero(ws, kWsHeader, stream), "workspace init");
+    return SSM_OK;
+}
+
+int ssm_shard_take_status(void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream) {
+    SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    if (!status) return fail(SSM_E_INVAL, "status is null");
+    SSM_TRY_HIP(hipStreamSynchronize(stream), "sync");
+    SSM_TRY_HIP(hipMemcpy(status, ws, sizeof(int32_t), hipMemcpyDeviceToHost), "read status");
+    SSM_TRY_HIP(launch_fill_zero(ws, kWsHeader, stream), "clear status");
+    SSM_TRY_HIP(hipStreamSynchronize(stream), "sync");
+    return SSM_OK;
+}
+
+int ssm_shard_prefill_stage1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int64_t T,
+                             const ssm_seq_meta_t* m, void* conv_pool, int32_t S, float* xdbl, void* ws,
+                             size_t ws_bytes, hipStream_t s) {
+    PrefillWs L;
+    SSM_TRY(prefill_checks(d, w, T, m, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (T > 0) {
+        SSM_TRY(check_ptr(x, "x"));
+        SSM_TRY(check_ptr(xdbl, "x_dbl_partial"));
+    }
+    return prefill1(d, w, x, T, m, conv_pool, S, xdbl, L, s);
+}
+
+int ssm_shard_prefill_stage2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float* xdbl, int64_t T,
+                             const ssm_seq_meta_t* m, float* ssm_pool, int32_t S, void* y, void* ws, size_t ws_bytes,
+                             hipStream_t s) {
+    PrefillWs L;
+    SSM_TRY(prefill_checks(d, w, T, m, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    if (T > 0) {
+        SSM_TRY(check_ptr(xdbl, "x_dbl"));
+        SSM_TRY(check_ptr(y, "y_partial"));
+    }
+    return prefill2(d, w, xdbl, T, m, ssm_pool, S, y, L, s);
+}
+
+int ssm_shard_prefill(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int64_t T,
+                      const ssm_seq_meta_t* m, void* conv_pool, float* ssm_pool, int32_t S, void* y, void* ws,
+                      size_t ws_bytes, hipStream_t s) {
+    PrefillWs L;
+    SSM_TRY(prefill_checks(d, w, T, m, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    if (T > 0) {
+        SSM_TRY(check_ptr(x, "x"));
+        SSM_TRY(check_ptr(y, "y_partial"));
+    }
+    SSM_TRY(prefill1(d, w, x, T, m, conv_pool, S, L.xdbl, L, s));
+    return prefill2(d, w, L.xdbl, T, m, ssm_pool, S, y, L, s);
+}
+
+int ssm_shard_decode_stage1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int32_t B,
+                            const int32_t* slot, void* conv_pool, int32_t S, float* xdbl, void* ws, size_t ws_bytes,
+                            hipStream_t s) {
+    DecodeWs L;
+    SSM_TRY(decode_checks(d, w, B, slot, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (B > 0) {
+        SSM_TRY(check_ptr(x, "x_t"));
+        SSM_TRY(check_ptr(xdbl, "x_dbl_partial"));
+    }
+    return decode1(d, w, x, B, slot, conv_pool, S, xdbl, L, s);
+}
+
+int ssm_shard_decode_stage2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float* xdbl, int32_t B,
+                            const int32_t* slot, float* ssm_pool, int32_t S, void* y, void* ws, size_t ws_bytes,
+                            hipStream_t s) {
+    DecodeWs L;
+    SSM_TRY(decode_checks(d, w, B, slot, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    if (B > 0) {
+        SSM_TRY(check_ptr(xdbl, "x_dbl"));
+        SSM_TRY(check_ptr(y, "y_partial"));
+    }
+    return decode2(d, w, xdbl, B, slot, ssm_pool, S, y, L, s);
+}
+
+int ssm_shard_decode_step(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int32_t B,
+                          const int32_t* slot, void* conv_pool, float* ssm_pool, int32_t S, void* y, void* ws,
+                          size_t ws_bytes, hipStream_t s) {
+    DecodeWs L;
+    SSM_TRY(decode_checks(d, w, B, slot, S, ws, ws_bytes, &L));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    if (B > 0) {
+        SSM_TRY(check_ptr(x, "x_t"));
+        SSM_TRY(check_ptr(y, "y_partial"));
+    }
+    SSM_TRY(decode1(d, w, x, B, slot, conv_pool, S, L.xdbl, L, s));
+    return decode2(d, w, L.xdbl, B, slot, ssm_pool, S, y, L, s);
+}
+
+int ssm_shard_slice_weights(const ssm_shard_desc_t* d, const ssm_shard_weights_t* full, const ssm_shard_weights_t* out,
+                            hipStream_t s) {
+    SSM_TRY(check_desc(d));
+    SSM_TRY(check_weights(full));
+    SSM_TRY(check_weights(out));
+    const size_t a = act_bytes(d);
+    const int64_t E = d->d_inner_shard, Et = d->d_inner_total, c0 = (int64_t)d->shard_index * E;
+    const int64_t dm = d->d_model, K = d->d_conv, R = d->dt_rank, N = d->d_state, W = R + 2 * N;
+    auto cp = [&](const void* src, int64_t ld_src, void* dst, int64_t ld_dst, int64_t rows, int64_t row_bytes,
+                  const char* what) -> int {
+        SSM_TRY_HIP(launch_copy_rows(dst, ld_dst, src, ld_src, rows, row_bytes, s), what);
+        return SSM_OK;
+    };
+    const char* fin = (const char*)full->in_proj_w;
+    SSM_TRY(cp(fin + c0 * dm * a, dm * a, (void*)out->in_proj_w, dm * a, E, dm * a, "slice in_proj x rows"));
+    SSM_TRY(cp(fin + (Et + c0) * dm * a, dm * a, (char*)out->in_proj_w + E * dm * a, dm * a, E, dm * a,
+               "slice in_proj z rows"));
+    SSM_TRY(cp((const char*)full->conv_w + c0 * K * a, E * K * a, (void*)out->conv_w, E * K * a, 1, E * K * a, "slice conv_w"));
+    SSM_TRY(cp((const char*)full->conv_b + c0 * a, E * a, (void*)out->conv_b, E * a, 1, E * a, "slice conv_b"));
+    SSM_TRY(cp((const char*)full->x_proj_w + c0 * a, Et * a, (void*)out->x_proj_w, E * a, W, E * a, "slice x_proj"));
+    SSM_TRY(cp((const char*)full->dt_proj_w + c0 * R * a, E * R * a, (void*)out->dt_proj_w, E * R * a, 1, E * R * a,
+               "slice dt_proj"));
+    SSM_TRY(cp((const char*)full->out_proj_w + c0 * a, Et * a, (void*)out->out_proj_w, E * a, dm, E * a, "slice out_proj"));
+    SSM_TRY(cp((const char*)full->dt_proj_b + c0 * 4, E * 4, (void*)out->dt_proj_b, E * 4, 1, E * 4, "slice dt_proj_b"));
+    SSM_TRY(cp((const char*)full->A_log + c0 * N * 4, E * N * 4, (void*)out->A_log, E * N * 4, 1, E * N * 4, "slice A_log"));
+    SSM_TRY(cp((const char*)full->D + c0 * 4, E * 4, (void*)out->D, E * 4, 1, E * 4, "slice D"));
+    return SSM_OK;
+}
+
+int ssm_reduce_add_f32(float* dst, const float* src, int64_t n, hipStream_t s) {
+    if (n < 0) return fail(SSM_E_INVAL, "n %lld", (long long)n);
+    if (n == 0) return SSM_OK;
+    SSM_TRY(check_ptr(dst, "dst"));
+    SSM_TRY(check_ptr(src, "src"));
+    SSM_TRY_HIP(launch_reduce_add(dst, src, n, s), "reduce_add");
+    return SSM_OK;
+}
+
+int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t adt, const void* B, int64_t ldb,
+                int32_t bdt, void* C, int64_t ldc, int32_t cdt, hipStream_t s) {
+    if (M < 0 || N < 0 || K < 0 || M > INT32_MAX || N > INT32_MAX || K > INT32_MAX)
+        return fail(SSM_E_INVAL, "gemm size %lld x %lld x %lld", (long long)M, (long long)N, (long long)K);
+    for (int32_t dt : {adt, bdt, cdt})
+        if (dt != SSM_F32 && dt != SSM_BF16) return fail(SSM_E_INVAL, "dtype %d", dt);
+    if (bdt == SSM_F32 && (adt != SSM_F32 || cdt != SSM_F32))
+        return fail(SSM_E_INVAL, "float32 B needs float32 A and C");
+    if (M == 0 || N == 0) return SSM_OK;
+    if (K % 8 || lda % 8 || ldb % 8 || ldc % 4) return fail(SSM_E_ALIGN, "K, lda, ldb must be multiples of 8, ldc of 4");
+    if (lda < K || ldb < K || ldc < N) return fail(SSM_E_INVAL, "leading dimension smaller than the row");
+    SSM_TRY(check_ptr(A, "A"));
+    SSM_TRY(check_ptr(B, "B"));
+    SSM_TRY(check_ptr(C, "C"));
+    return gemm(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, "gemm");
+}
+
+int ssm_conv1d_silu(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int64_t T,
+                    const ssm_seq_meta_t* m, void* conv_pool, int32_t S, void* u, void* ws, size_t ws_bytes,
+                    hipStream_t s) {
+    SSM_TRY(common_checks(d, w, T, S));
+    SSM_TRY(check_meta(m, T));
+    SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (T > 0) {
+        SSM_TRY(check_ptr(xz, "xz"));
+        SSM_TRY(check_ptr(u, "u"));
+    }
+    ConvArgs ca = conv_args(d, w, xz, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq, conv_pool, S, u,
+                            (int32_t*)ws);
+    SSM_TRY_HIP(launch_conv_prefill(ca, d->act_dtype == SSM_BF16, s), "conv1d");
+    SSM_TRY_HIP(launch_conv_state_update(ca, d->act_dtype == SSM_BF16, s), "conv history");
+    return SSM_OK;
+}
+
+int ssm_selective_scan(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* u, const void* dt,
+                       const void* xz, const float* xdbl, int64_t T, const ssm_seq_meta_t* m, float* pool, int32_t S,
+                       void* g, void* ws, size_t ws_bytes, hipStream_t s) {
+    SSM_TRY(common_checks(d, w, T, S));
+    SSM_TRY(check_meta(m, T));
+    const size_t need = kWsHeader + scan_scratch_bytes(T, d->d_inner_shard, m->nseq);
+    SSM_TRY(check_ws(ws, ws_bytes, need));
+    SSM_TRY(check_ptr(pool, "ssm_pool"));
+    if (T > 0) {
+        SSM_TRY(check_ptr(u, "u"));
+        SSM_TRY(check_ptr(dt, "dt"));
+        SSM_TRY(check_ptr(xz, "xz"));
+        SSM_TRY(check_ptr(xdbl, "x_dbl"));
+        SSM_TRY(check_ptr(g, "g"));
+    }
+    ScanArgs sa = scan_args(d, w, u, dt, xz, xdbl, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq,
+                            pool, S, g, (int32_t*)ws, (char*)ws + kWsHeader);
+    SSM_TRY_HIP(launch_scan_prefill(sa, d->act_dtype == SSM_BF16, s), "selective scan");
+    return SSM_OK;
+}
+
+int ssm_decode_conv(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int32_t B,
+                    const int32_t* slot, void* conv_pool, int32_t S, void* u, void* ws, size_t ws_bytes,
+                    hipStream_t s) {
+    SSM_TRY(common_checks(d, w, B, S));
+    SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
+    if (B > 0) {
+        if (!slot) return fail(SSM_E_INVAL, "cache_slot is null");
+        SSM_TRY(check_ptr(xz, "xz"));
+        SSM_TRY(check_ptr(u, "u"));
+    }
+    ConvArgs ca = conv_args(d, w, xz, B, nullptr, slot, nullptr, B, conv_pool, S, u, (int32_t*)ws);
+    SSM_TRY_HIP(launch_conv_decode(ca, d->act_dtype == SSM_BF16, s), "decode conv");
+    return SSM_OK;
+}
+
+int ssm_decode_ssm(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* u, const void* dt,
+                   const void* xz, const float* xdbl, int32_t B, const int32_t* slot, float* pool, int32_t S, void* g,
+                   void* ws, size_t ws_bytes, hipStream_t s) {
+    SSM_TRY(common_checks(d, w, B, S));
+    SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
+    SSM_TRY(check_ptr(pool, "ssm_pool"));
+    if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
+    if (B > 0) {
+        if (!slot) return fail(SSM_E_INVAL, "cache_slot is null");
+        SSM_TRY(check_ptr(u, "u"));
+        SSM_TRY(check_ptr(dt, "dt"));
+        SSM_TRY(check_ptr(xz, "xz"));
+        SSM_TRY(check_ptr(xdbl, "x_dbl"));
+        SSM_TRY(check_ptr(g, "g"));
+    }
+    ScanArgs sa = scan_args(d, w, u, dt, xz, xdbl, B, nullptr, slot, nullptr, B, pool, S, g, (int32_t*)ws, nullptr);
+    SSM_TRY_HIP(launch_decode_ssm(sa, d->act_dtype == SSM_BF16, s), "decode state update");
+    return SSM_OK;
+}
+
+}  // extern "C"

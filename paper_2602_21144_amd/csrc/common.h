@@ -1,0 +1,89 @@
+// Internal declarations shared by the gfx950 kernels and the C-ABI layer.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ssm_shard.h"
+
+namespace ssm {
+
+using bf16 = __bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kN = 16;          // states per channel the kernels are built for
+constexpr int kMaxConv = 4;     // largest convolution width
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Activation element <-> float. bf16 stores round to nearest even (hardware cvt on gfx950).
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+
+// exp2 / log2 on the transcendental unit (v_exp_f32 / v_log_f32).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// softplus(v) = log(1 + e^v), v itself above 20. log1p is formed as
+// log(1+w) * w / ((1+w) - 1), which keeps full relative accuracy for small w.
+__device__ __forceinline__ float softplus_f(float v) {
+    float w = fast_exp2(v * kLog2e);
+    float p = 1.0f + w;
+    float l = (p == 1.0f) ? w : fast_log2(p) * kLn2 * (w / (p - 1.0f));
+    return v > 20.0f ? v : l;
+}
+// SiLU(v) = v / (1 + e^-v)
+__device__ __forceinline__ float silu_f(float v) { return v * fast_rcp(1.0f + fast_exp2(-v * kLog2e)); }
+
+// Workspace header: status word at offset 0; regions start 256-byte aligned.
+constexpr size_t kWsHeader = 256;
+__host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// ---------------------------------------------------------------- launchers
+// GEMM: C[M][N] = A[M][K] * B[N][K]^T. Returns hipError_t of the launch.
+hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt,
+                          const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
+                          hipStream_t s);
+
+struct ConvArgs {
+    const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1
+    const void* w; const void* b;      // [E][K], [E]
+    void* u;                           // [T][E]
+    void* conv_pool;                   // [S][E][K-1]
+    const int32_t* cu; const int32_t* slot; const int32_t* has_init;
+    int32_t* status;
+    int64_t T; int E, K, nseq, S;
+};
+hipError_t launch_conv_prefill(const ConvArgs& a, bool bf16_act, hipStream_t s);
+hipError_t launch_conv_state_update(const ConvArgs& a, bool bf16_act, hipStream_t s);
+hipError_t launch_conv_decode(const ConvArgs& a, bool bf16_act, hipStream_t s);
+
+struct ScanArgs {
+    const void* u; const void* dt; const void* z; int64_t ld_z;   // z: stride 2E
+    const float* xdbl; int64_t ld_xdbl; int R;                     // B at R, C at R+N
+    const float* b_dt; const float* A_log; const float* D;
+    void* g;                                                       // [T][E]
+    float* pool;                                                   // [S][E][N]
+    const int32_t* cu; const int32_t* slot; const int32_t* has_init;
+    int32_t* status;
+    // scan scratch (prefill only)
+    float* h_local; float* sum_delta; float* h_in; float* h0_seq;
+    int64_t T; int E, nseq, S, win;                                // win: tokens per window
+};
+int scan_window_len(int64_t T, int E);
+size_t scan_scratch_bytes(int64_t max_T, int E, int max_seqs);
+hipError_t launch_scan_prefill(const ScanArgs& a, bool bf16_act, hipStream_t s);
+hipError_t launch_decode_ssm(const ScanArgs& a, bool bf16_act, hipStream_t s);
+
+hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);  // bytes: multiple of 4
+hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_t s);
+hipError_t launch_copy_rows(void* dst, int64_t ld_dst, const void* src, int64_t ld_src,
+                            int64_t rows, int64_t row_bytes, hipStream_t s);
+
+}  // namespace ssm

@@ -1,0 +1,295 @@
+// Dense projections of the mixer (in_proj, x_proj, dt_proj, out_proj) as
+// C[M][N] = A[M][K] * B[N][K]^T on gfx950 matrix cores.
+//
+// Both operands are K-contiguous (activations [tokens][features], weights
+// [out_features][in_features]), which is the natural operand layout of MFMA: every
+// lane loads 8 consecutive k of one row. bf16 path: v_mfma_f32_32x32x16_bf16 with
+// fp32 accumulation; fp32 path: v_mfma_f32_16x16x4_f32.
+#include "common.h"
+
+namespace ssm {
+namespace {
+
+constexpr int kBK = 64;  // k per LDS stage (bf16): 128 bytes per row = 8 chunks of 16 B
+
+// Row r of an LDS tile stores its 8 chunks permuted by an XOR with (r>>1)&7, so the
+// 16 lanes that read one chunk column from 16 consecutive rows hit distinct banks.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+// Map the linear workgroup id to an output tile. Workgroups are dispatched round robin
+// over the 8 XCDs; regroup so each XCD gets a contiguous run of tiles, and order the
+// tiles in groups of 8 tile-rows so that a run shares A panels and B panels in its L2.
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
+    int nwg = gridDim.x;
+    int bid = blockIdx.x;
+    if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+    constexpr int G = 8;
+    int per_group = G * tiles_n;
+    int grp = bid / per_group;
+    int first = grp * G;
+    int gm = min(tiles_m - first, G);
+    int r = bid - grp * per_group;
+    tm = first + r % gm;
+    tn = r / gm;
+}
+
+__device__ __forceinline__ bf16x8 cvt8(float4 a, float4 b) {
+    bf16x8 o;
+    o[0] = (bf16)a.x; o[1] = (bf16)a.y; o[2] = (bf16)a.z; o[3] = (bf16)a.w;
+    o[4] = (bf16)b.x; o[5] = (bf16)b.y; o[6] = (bf16)b.z; o[7] = (bf16)b.w;
+    return o;
+}
+
+template <int BM, int BN, int WM, int WN, bool A_F32, bool C_F32>
+__global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
+                                                    const void* __restrict__ Ap, int64_t lda,
+                                                    const bf16* __restrict__ B, int64_t ldb,
+                                                    void* __restrict__ Cp, int64_t ldc,
+                                                    int tiles_m, int tiles_n) {
+    static_assert(WM * WN == 4, "four waves");
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+    constexpr int AC = BM * 8 / 256;  // 16-byte chunks per thread per stage
+    constexpr int BC = BN * 8 / 256;
+    static_assert(AC >= 1 && BC >= 1, "tile too small for 256 threads");
+
+    __shared__ __attribute__((aligned(16))) bf16 As[2][BM * kBK];
+    __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * kBK];
+
+    int tm, tn;
+    tile_of(tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    bf16x8 ra[AC], rb[BC];
+
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < AC; ++i) {
+            const int q = tid + 256 * i, row = q >> 3, ck = q & 7;
+            const int gm = m0 + row, gk = k0 + ck * 8;
+            if (gm < M && gk < K) {
+                if constexpr (A_F32) {
+                    const float* p = (const float*)Ap + (int64_t)gm * lda + gk;
+                    ra[i] = cvt8(*(const float4*)p, *(const float4*)(p + 4));
+                } else {
+                    ra[i] = *(const bf16x8*)((const bf16*)Ap + (int64_t)gm * lda + gk);
+                }
+            } else {
+                ra[i] = bf16x8{};
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < BC; ++i) {
+            const int q = tid + 256 * i, row = q >> 3, ck = q & 7;
+            const int gn = n0 + row, gk = k0 + ck * 8;
+            rb[i] = (gn < N && gk < K) ? *(const bf16x8*)(B + (int64_t)gn * ldb + gk) : bf16x8{};
+        }
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < AC; ++i) {
+            const int q = tid + 256 * i, row = q >> 3, ck = q & 7;
+            *(bf16x8*)&As[buf][row * kBK + swz(row, ck) * 8] = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < BC; ++i) {
+            const int q = tid + 256 * i, row = q >> 3, ck = q & 7;
+            *(bf16x8*)&Bs[buf][row * kBK + swz(row, ck) * 8] = rb[i];
+        }
+    };
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+
+    const int nk = (K + kBK - 1) / kBK;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        if (kt + 1 < nk) gload((kt + 1) * kBK);
+#pragma unroll
+        for (int s = 0; s < kBK / 16; ++s) {
+            const int c = s * 2 + (lane >> 5);
+            bf16x8 af[TM], bfg[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int row = wm * WTM + i * 32 + (lane & 31);
+                af[i] = *(const bf16x8*)&As[cur][row * kBK + swz(row, c) * 8];
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int row = wn * WTN + j * 32 + (lane & 31);
+                bfg[j] = *(const bf16x8*)&Bs[cur][row * kBK + swz(row, c) * 8];
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfg[j], af[i], acc[i][j], 0, 0, 0);
+        }
+        if (kt + 1 < nk) lstore(cur ^ 1);
+        __syncthreads();
+    }
+
+    // Operands were swapped (B rows first), so lane l holds output row (l & 31) and
+    // four consecutive output columns per group of four accumulators.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WTM + i * 32 + (lane & 31);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = n0 + wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+                const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
+                const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+                if constexpr (C_F32) {
+                    float* p = (float*)Cp + (int64_t)m * ldc + n;
+                    if (n + 3 < N) {
+                        *(float4*)p = make_float4(v0, v1, v2, v3);
+                    } else {
+                        if (n < N) p[0] = v0;
+                        if (n + 1 < N) p[1] = v1;
+                        if (n + 2 < N) p[2] = v2;
+                    }
+                } else {
+                    bf16* p = (bf16*)Cp + (int64_t)m * ldc + n;
+                    if (n + 3 < N) {
+                        bf16x4 o;
+                        o[0] = (bf16)v0; o[1] = (bf16)v1; o[2] = (bf16)v2; o[3] = (bf16)v3;
+                        *(bf16x4*)p = o;
+                    } else {
+                        if (n < N) p[0] = (bf16)v0;
+                        if (n + 1 < N) p[1] = (bf16)v1;
+                        if (n + 2 < N) p[2] = (bf16)v2;
+                    }
+                }
+            }
+        }
+    }
+}
+
+// fp32 operands on v_mfma_f32_16x16x4_f32: 64x64 tiles, k 16 per stage, four waves of 32x32.
+constexpr int kFBK = 16;
+constexpr int kFPad = kFBK + 1;
+
+__global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const float* __restrict__ A,
+                                                   int64_t lda, const float* __restrict__ B, int64_t ldb,
+                                                   float* __restrict__ C, int64_t ldc, int tiles_m, int tiles_n) {
+    __shared__ float As[2][64 * kFPad];
+    __shared__ float Bs[2][64 * kFPad];
+    int tm, tn;
+    tile_of(tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * 64, n0 = tn * 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = tid >> 2, lck = tid & 3;  // one float4 of A and of B per thread
+    float4 ra, rb;
+    auto gload = [&](int k0) {
+        const int gk = k0 + lck * 4;
+        const int gm = m0 + lrow, gn = n0 + lrow;
+        ra = (gm < M && gk < K) ? *(const float4*)(A + (int64_t)gm * lda + gk) : make_float4(0, 0, 0, 0);
+        rb = (gn < N && gk < K) ? *(const float4*)(B + (int64_t)gn * ldb + gk) : make_float4(0, 0, 0, 0);
+    };
+    auto lstore = [&](int buf) {
+        float* a = &As[buf][lrow * kFPad + lck * 4];
+        float* b = &Bs[buf][lrow * kFPad + lck * 4];
+        a[0] = ra.x; a[1] = ra.y; a[2] = ra.z; a[3] = ra.w;
+        b[0] = rb.x; b[1] = rb.y; b[2] = rb.z; b[3] = rb.w;
+    };
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{};
+    const int nk = (K + kFBK - 1) / kFBK;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        if (kt + 1 < nk) gload((kt + 1) * kFBK);
+#pragma unroll
+        for (int s = 0; s < kFBK / 4; ++s) {
+            float af[2], bfv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) af[i] = As[cur][(wm * 32 + i * 16 + (lane & 15)) * kFPad + s * 4 + (lane >> 4)];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bfv[j] = Bs[cur][(wn * 32 + j * 16 + (lane & 15)) * kFPad + s * 4 + (lane >> 4)];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(bfv[j], af[i], acc[i][j], 0, 0, 0);
+        }
+        if (kt + 1 < nk) lstore(cur ^ 1);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int m = m0 + wm * 32 + i * 16 + (lane & 15);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = n0 + wn * 32 + j * 16 + 4 * (lane >> 4);
+            float* p = C + (int64_t)m * ldc + n;
+            if (n + 3 < N) {
+                *(float4*)p = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (n + v < N) p[v] = acc[i][j][v];
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int WN, bool AF, bool CF>
+hipError_t run_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+                    void* C, int64_t ldc, hipStream_t s) {
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, AF, CF>), dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N,
+                       (int)K, A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
+    return hipGetLastError();
+}
+
+template <bool AF, bool CF>
+hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+                         void* C, int64_t ldc, hipStream_t s) {
+    // Tile by output size: large outputs use 256x256 (each wave 128x128, the most
+    // MFMA work per LDS byte); small token counts use narrow tiles to spread the
+    // weight read over more workgroups.
+    if (M <= 32) return run_bf16<32, 128, 1, 4, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (M <= 64) return run_bf16<64, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+    if (big_tiles >= 512) return run_bf16<256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return run_bf16<128, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt, const void* B,
+                          int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s) {
+    if (M == 0 || N == 0) return hipSuccess;
+    if (b_dt == SSM_F32) {
+        const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
+        hipLaunchKernelGGL(gemm_f32_nt, dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, lda,
+                           (const float*)B, ldb, (float*)C, ldc, tm, tn);
+        return hipGetLastError();
+    }
+    const bool af = a_dt == SSM_F32, cf = c_dt == SSM_F32;
+    if (af && cf) return dispatch_bf16<true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (af) return dispatch_bf16<true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (cf) return dispatch_bf16<false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return dispatch_bf16<false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+}
+
+}  // namespace ssm

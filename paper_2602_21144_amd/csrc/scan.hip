@@ -1,0 +1,333 @@
+// Selective scan of the SSM path (Section II-B; Section IV-C: Delta sharded with the
+// channels, B and C complete on every rank, A and D local) and the recurrent half of
+// the SSM cache (Section IV-A).
+//
+// Per channel c and state n:  Delta_t = softplus(dt_t + b_dt)
+//                             h_t = exp(Delta_t * A) * h_{t-1} + Delta_t * B_t * u_t
+//                             y_t = sum_n C_t[n] h_t[n] + D u_t ;  g_t = y_t * SiLU(z_t)
+//
+// Layout on gfx950: one lane per channel, its 16 fp32 states in VGPRs; B_t and C_t are
+// the same for every channel of a token, so a wave reads them with scalar loads. The
+// packed token range is cut into windows of `win` tokens so that there are enough
+// waves for the 1024 SIMDs: pass A computes, for each window whose last sequence runs
+// on into the next window, that piece's end state from a zero start (and its sum of
+// Delta); pass B links windows in order per (channel, state) -- the state entering
+// window j+1 is exp(A * sum Delta_j) * (state entering j) + local end state of j; pass C
+// runs the full recurrence from the linked state and writes g and the final states.
+// Initial states of continuing sequences are copied out of the pool in pass A, so pass
+// C (which writes final states into the pool) never reads a slot another pass writes.
+#include "common.h"
+
+namespace ssm {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kMinWin = 32, kMaxWin = 2048;
+constexpr int kTargetWaves = 3072;
+
+// flags per window, written by pass A
+constexpr int kFlagContIn = 1;    // first token continues a sequence begun earlier
+constexpr int kFlagCarryOut = 2;  // last sequence continues past the window end
+constexpr int kFlagLastCont = 4;  // last piece starts at the window start as a continuation
+
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ int seq_of(const int32_t* cu, int nseq, int64_t t) {
+    int lo = 0, hi = nseq;
+    while (hi - lo > 1) {
+        int mid = (lo + hi) >> 1;
+        if (cu[mid] <= t) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+int64_t target_windows(int E) { return std::max<int64_t>(1, ((int64_t)kTargetWaves * kWave + E - 1) / E); }
+
+template <typename T>
+__device__ __forceinline__ void load_tok(const ScanArgs& a, int64_t t, int c, float& u, float& dt) {
+    u = to_f32(((const T*)a.u)[t * a.E + c]);
+    dt = to_f32(((const T*)a.dt)[t * a.E + c]);
+}
+
+// ---------------------------------------------------------------- pass A
+template <typename T>
+__global__ __launch_bounds__(kWave) void scan_local_kernel(ScanArgs a, int nwin, int32_t* wflags) {
+    const int cblocks = a.E / kWave;
+    const int j = blockIdx.x / cblocks;
+    const int c = (blockIdx.x % cblocks) * kWave + threadIdx.x;
+    const int64_t w0 = (int64_t)j * a.win, w1 = min(w0 + a.win, a.T);
+    const int s_first = uni(seq_of(a.cu, a.nseq, w0));
+    const int s_last = uni(seq_of(a.cu, a.nseq, w1 - 1));
+    const int64_t b_first = uni(a.cu[s_first]);
+    const int64_t b_last = uni(a.cu[s_last]), e_last = uni(a.cu[s_last + 1]);
+    const bool carry_out = w1 < a.T && e_last > w1;
+    const bool last_cont = b_last < w0;
+    if (blockIdx.x % cblocks == 0 && threadIdx.x == 0)
+        wflags[j] = (b_first < w0 ? kFlagContIn : 0) | (carry_out ? kFlagCarryOut : 0) | (last_cont ? kFlagLastCont : 0);
+
+    // copy the initial state of every non-empty sequence that starts in this window
+    for (int s = s_first; s <= s_last; ++s) {
+        const int64_t b = uni(a.cu[s]), e = uni(a.cu[s + 1]);
+        if (b < w0 || e <= b || !a.has_init[s]) continue;
+        const int slot = uni(a.slot[s]);
+        if (slot < 0 || slot >= a.S) {
+            if (threadIdx.x == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+            continue;
+        }
+        const float4* src = (const float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
+        float4* dst = (float4*)(a.h0_seq + ((int64_t)s * a.E + c) * kN);
+#pragma unroll
+        for (int q = 0; q < kN / 4; ++q) dst[q] = src[q];
+    }
+    if (!carry_out) return;
+
+    float A2[kN], h[kN];
+#pragma unroll
+    for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
+    const float bdt = a.b_dt[c];
+    int64_t t = last_cont ? w0 : b_last;
+    if (!last_cont && a.has_init[s_last]) {
+        const int slot = uni(a.slot[s_last]);
+        const bool ok = slot >= 0 && slot < a.S;
+#pragma unroll
+        for (int n = 0; n < kN; ++n) h[n] = ok ? a.pool[((int64_t)slot * a.E + c) * kN + n] : 0.0f;
+    } else {
+#pragma unroll
+        for (int n = 0; n < kN; ++n) h[n] = 0.0f;
+    }
+    float sum_delta = 0.0f;
+    for (; t < w1; ++t) {
+        float u, dt;
+        load_tok<T>(a, t, c, u, dt);
+        const float* Bt = a.xdbl + t * a.ld_xdbl + a.R;
+        const float delta = softplus_f(dt + bdt);
+        const float du = delta * u;
+        sum_delta += delta;
+#pragma unroll
+        for (int n = 0; n < kN; ++n) h[n] = fast_exp2(delta * A2[n]) * h[n] + du * Bt[n];
+    }
+    float4* hl = (float4*)(a.h_local + ((int64_t)j * a.E + c) * kN);
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) hl[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
+    a.sum_delta[(int64_t)j * a.E + c] = sum_delta;
+}
+
+// ---------------------------------------------------------------- pass B
+// One lane per (channel, state): walk the windows in order carrying the state across
+// window boundaries of continuing sequences. Also clears the state of empty sequences
+// that start fresh (their final state is the zero initial state).
+__global__ __launch_bounds__(256) void scan_link_kernel(ScanArgs a, int nwin, const int32_t* wflags) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= (int64_t)a.E * kN) return;
+    const int c = (int)(gid / kN), n = (int)(gid % kN);
+    const float A2 = -__expf(a.A_log[c * kN + n]) * kLog2e;
+    float carry = 0.0f;
+    for (int j = 0; j < nwin; ++j) {
+        const int f = wflags[j];
+        if (f & kFlagContIn) a.h_in[((int64_t)j * a.E + c) * kN + n] = carry;
+        if (f & kFlagCarryOut) {
+            const float hl = a.h_local[((int64_t)j * a.E + c) * kN + n];
+            carry = (f & kFlagLastCont) ? fast_exp2(a.sum_delta[(int64_t)j * a.E + c] * A2) * carry + hl : hl;
+        }
+    }
+    for (int s = 0; s < a.nseq; ++s) {
+        if (a.cu[s + 1] != a.cu[s] || a.has_init[s]) continue;
+        const int slot = a.slot[s];
+        if (slot < 0 || slot >= a.S) continue;
+        a.pool[((int64_t)slot * a.E + c) * kN + n] = 0.0f;
+    }
+}
+
+// ---------------------------------------------------------------- pass C
+template <typename T>
+__global__ __launch_bounds__(kWave) void scan_main_kernel(ScanArgs a) {
+    const int cblocks = a.E / kWave;
+    const int j = blockIdx.x / cblocks;
+    const int c = (blockIdx.x % cblocks) * kWave + threadIdx.x;
+    const int64_t w0 = (int64_t)j * a.win, w1 = min(w0 + a.win, a.T);
+    float A2[kN], h[kN];
+#pragma unroll
+    for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
+    const float bdt = a.b_dt[c], Dc = a.D[c];
+    int s = uni(seq_of(a.cu, a.nseq, w0));
+    int64_t sb = uni(a.cu[s]);
+    if (sb < w0) {
+        const float4* src = (const float4*)(a.h_in + ((int64_t)j * a.E + c) * kN);
+#pragma unroll
+        for (int q = 0; q < kN / 4; ++q) {
+            float4 v = src[q];
+            h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+        }
+    }
+    int64_t t = w0;
+    bool first = true;
+    while (t < w1) {
+        const int64_t se = uni(a.cu[s + 1]);
+        if (se <= t) {  // empty sequence or inconsistent cu_seqlens
+            if (se < t || s + 1 >= a.nseq) {
+                if (threadIdx.x == 0) atomicOr(a.status, SSM_STATUS_BAD_SEQLENS);
+                break;
+            }
+            ++s;
+            first = false;
+            continue;
+        }
+        if (!first || sb >= w0) {
+            // a sequence starting here: zeros, or the initial state copied in pass A
+            if (a.has_init[s]) {
+                const float4* src = (const float4*)(a.h0_seq + ((int64_t)s * a.E + c) * kN);
+#pragma unroll
+                for (int q = 0; q < kN / 4; ++q) {
+                    float4 v = src[q];
+                    h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+                }
+            } else {
+#pragma unroll
+                for (int n = 0; n < kN; ++n) h[n] = 0.0f;
+            }
+        }
+        first = false;
+        const int64_t te = min(se, w1);
+        for (; t < te; ++t) {
+            float u, dt;
+            load_tok<T>(a, t, c, u, dt);
+            const float z = to_f32(((const T*)a.z)[t * a.ld_z + c]);
+            const float* Bt = a.xdbl + t * a.ld_xdbl + a.R;
+            const float delta = softplus_f(dt + bdt);
+            const float du = delta * u;
+            float y = 0.0f;
+#pragma unroll
+            for (int n = 0; n < kN; ++n) {
+                h[n] = fast_exp2(delta * A2[n]) * h[n] + du * Bt[n];
+                y += Bt[kN + n] * h[n];
+            }
+            y += Dc * u;
+            ((T*)a.g)[t * a.E + c] = from_f32<T>(y * silu_f(z));
+        }
+        if (se <= w1) {  // the sequence ends in this window: store its final state
+            const int slot = uni(a.slot[s]);
+            if (slot >= 0 && slot < a.S) {
+                float4* dst = (float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
+#pragma unroll
+                for (int q = 0; q < kN / 4; ++q) dst[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
+            } else if (threadIdx.x == 0) {
+                atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+            }
+            if (s + 1 >= a.nseq) break;
+            ++s;
+            sb = uni(a.cu[s]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------- decode
+// One lane per (sequence, channel): one recurrence step on the cached state, in place.
+template <typename T>
+__global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= (int64_t)a.nseq * a.E) return;
+    const int b = (int)(gid / a.E), c = (int)(gid % a.E);
+    const int slot = a.slot[b];
+    if (slot < 0 || slot >= a.S) {
+        atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+        ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(0.0f);
+        return;
+    }
+    float4* hp = (float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
+    float h[kN];
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) {
+        float4 v = hp[q];
+        h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+    }
+    const float u = to_f32(((const T*)a.u)[(int64_t)b * a.E + c]);
+    const float dt = to_f32(((const T*)a.dt)[(int64_t)b * a.E + c]);
+    const float z = to_f32(((const T*)a.z)[(int64_t)b * a.ld_z + c]);
+    const float* Bt = a.xdbl + (int64_t)b * a.ld_xdbl + a.R;
+    const float delta = softplus_f(dt + a.b_dt[c]);
+    const float du = delta * u;
+    float y = 0.0f;
+#pragma unroll
+    for (int n = 0; n < kN; ++n) {
+        const float A2 = -__expf(a.A_log[c * kN + n]) * kLog2e;
+        h[n] = fast_exp2(delta * A2) * h[n] + du * Bt[n];
+        y += Bt[kN + n] * h[n];
+    }
+    y += a.D[c] * u;
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) hp[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
+    ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(y * silu_f(z));
+}
+
+}  // namespace
+
+int scan_window_len(int64_t T, int E) {
+    const int64_t tw = target_windows(E);
+    int64_t want = (T + tw - 1) / tw;
+    int64_t w = kMinWin;
+    while (w < want && w < kMaxWin) w <<= 1;
+    return (int)w;
+}
+
+static int64_t max_windows(int64_t max_T, int E) {
+    return std::max<int64_t>(target_windows(E), (max_T + kMaxWin - 1) / kMaxWin) + 1;
+}
+
+// Scratch regions of the windowed scan, in order: local end states [nwin][E][N],
+// sums of Delta [nwin][E], linked entry states [nwin][E][N], copied initial states
+// [nseq][E][N], window flags [nwin].
+static size_t scan_layout(char* base, int64_t T, int E, int nseq, int nwin, ScanArgs* a, int32_t** wflags) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) { char* p = base ? base + off : nullptr; off += align256(bytes); return p; };
+    char* hl = take((size_t)nwin * E * kN * 4);
+    char* sd = take((size_t)nwin * E * 4);
+    char* hi = take((size_t)nwin * E * kN * 4);
+    char* h0 = take((size_t)std::max(nseq, 1) * E * kN * 4);
+    char* wf = take((size_t)std::max(nwin, 1) * 4);
+    if (a) {
+        a->h_local = (float*)hl; a->sum_delta = (float*)sd; a->h_in = (float*)hi; a->h0_seq = (float*)h0;
+    }
+    if (wflags) *wflags = (int32_t*)wf;
+    (void)T;
+    return off;
+}
+
+static int num_windows(int64_t T, int win) { return T > 0 ? (int)((T + win - 1) / win) : 0; }
+
+size_t scan_scratch_bytes(int64_t max_T, int E, int max_seqs) {
+    // the window count is largest at the largest T (windows grow with T)
+    const int nwin = std::max<int>((int)max_windows(max_T, E), num_windows(max_T, scan_window_len(max_T, E)));
+    return scan_layout(nullptr, max_T, E, max_seqs, nwin, nullptr, nullptr);
+}
+
+hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
+    ScanArgs a = a0;
+    if (a.nseq <= 0) return hipSuccess;
+    const int nwin = num_windows(a.T, a.win);
+    int32_t* wflags = nullptr;
+    scan_layout((char*)a0.h_local, a.T, a.E, a.nseq, nwin, &a, &wflags);
+    const int cblocks = a.E / kWave;
+    if (nwin > 0) {
+        if (bf) hipLaunchKernelGGL(scan_local_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
+        else hipLaunchKernelGGL(scan_local_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
+    }
+    const int64_t lanes = (int64_t)a.E * kN;
+    hipLaunchKernelGGL(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
+                       (const int32_t*)wflags);
+    if (nwin > 0) {
+        if (bf) hipLaunchKernelGGL(scan_main_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
+        else hipLaunchKernelGGL(scan_main_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
+    const int64_t lanes = (int64_t)a.nseq * a.E;
+    if (lanes <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
+    if (bf) hipLaunchKernelGGL(decode_ssm_kernel<bf16>, grid, block, 0, s, a);
+    else hipLaunchKernelGGL(decode_ssm_kernel<float>, grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace ssm

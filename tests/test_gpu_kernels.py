@@ -1,0 +1,294 @@
+"""Kernel-level parity on the GPU: each stage operator of the C ABI against the oracle's
+stage function on the same seeded inputs (drawn on the host, never computed on the GPU).
+"""
+import numpy as np
+import pytest
+
+from mixer_cases import TOL, assert_close, f64, poison_like
+from oracle import mixer as om
+from paper_2602_21144_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2602_21144_amd import binding
+    binding.lib()
+    return binding
+
+
+def _rnd_host(rng, shape, act, scale=1.0):
+    a = (rng.normal(size=shape) * scale).astype(np.float32)
+    return synth.round_bf16_f32(a) if act == "bf16" else a
+
+
+def _dev(a, dt):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to("cuda", dt)
+
+
+# ----------------------------------------------------------------------- GEMM
+GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (33, 200, 160), (64, 96, 224), (100, 300, 256), (257, 513, 64),
+               (1000, 520, 768), (2048, 2048, 512), (300, 5120, 2560)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("kind", ["bf16_bf16", "bf16_f32", "f32a_bf16", "f32"])
+def test_gemm_nt(B, M, N, K, kind):
+    rng = np.random.default_rng(M * 7 + N * 3 + K)
+    a_act = "f32" if kind in ("f32a_bf16", "f32") else "bf16"
+    b_act = "f32" if kind == "f32" else "bf16"
+    A = _rnd_host(rng, (M, K), a_act)
+    Bm = _rnd_host(rng, (N, K), b_act, 1.0 / np.sqrt(K))
+    c_dt = torch.float32 if kind in ("bf16_f32", "f32") else torch.bfloat16
+    # ragged N: the output row stride is padded to a multiple of 4 and C is a view
+    Cpad = torch.full((M, (N + 3) // 4 * 4), float("nan"), dtype=c_dt, device="cuda")
+    C = Cpad[:, :N]
+    B.ssm_gemm_nt(_dev(A, torch.float32 if a_act == "f32" else torch.bfloat16),
+                  _dev(Bm, torch.float32 if b_act == "f32" else torch.bfloat16), C)
+    torch.cuda.synchronize()
+    A64 = A.astype(np.float64)
+    if kind == "f32a_bf16":      # A is rounded to bf16 as it is loaded (dt_proj's input)
+        A64 = om.round_bf16(A64)
+    ref = A64 @ Bm.astype(np.float64).T
+    if c_dt == torch.bfloat16:
+        ref = om.round_bf16(ref)
+    got = C.to(torch.float64).cpu().numpy()
+    tol = 1e-5 if c_dt == torch.float32 else 8e-3
+    assert_close(got, ref, tol, f"gemm {kind} {M}x{N}x{K}")
+
+
+def test_gemm_strided_operands(B):
+    """dt_proj reads the first R columns of x_dbl (row stride R+2N) as its A operand."""
+    rng = np.random.default_rng(5)
+    T, R, N, E = 77, 48, 16, 192
+    xdbl = rng.normal(size=(T, R + 2 * N)).astype(np.float32)
+    W = synth.round_bf16_f32((rng.normal(size=(E, R)) / np.sqrt(R)).astype(np.float32))
+    xd = _dev(xdbl, torch.float32)
+    C = torch.empty(T, E, dtype=torch.bfloat16, device="cuda")
+    B.ssm_gemm_nt(xd[:, :R], _dev(W, torch.bfloat16), C)
+    torch.cuda.synchronize()
+    ref = om.round_bf16(om.round_bf16(xdbl.astype(np.float64)[:, :R]) @ W.astype(np.float64).T)
+    assert_close(C.to(torch.float64).cpu().numpy(), ref, 8e-3, "strided dt_proj")
+
+
+# ------------------------------------------------------------------ conv1d
+def _meta_case(rng, lens, S, init_frac=0.5):
+    nseq = len(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    slots = rng.permutation(S)[:nseq].astype(np.int32)
+    hi = (rng.random(nseq) < init_frac).astype(np.int32)
+    return cu, slots, hi
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [4, 3, 2])
+def test_conv1d_silu_prefill(B, act, K):
+    rng = np.random.default_rng(11 + K)
+    shape = synth.LayerShape(64, 128, 16, 16, K, 1, act)
+    E = shape.d_shard
+    lens = [5, 1, 0, 40, 2, 17, 1, 3]
+    S = len(lens) + 4
+    cu, slots, hi = _meta_case(rng, lens, S)
+    hi[0], hi[1], hi[4] = 1, 1, 1      # short continuing pieces (fewer than K-1 tokens)
+    T = int(cu[-1])
+    xz = _rnd_host(rng, (T, 2 * E), act)
+    w = f64(synth.make_general_layer(shape, 3))
+    pool0 = _rnd_host(rng, (S, E, K - 1), act)
+    dt_act = torch.float32 if act == "f32" else torch.bfloat16
+    dw = B.upload_weights(synth.make_general_layer(shape, 3), act)
+    d = B.make_desc(shape)
+    meta = B.SeqMeta(cu, slots, hi, S)
+    pool = _dev(pool0, dt_act)
+    untouched = [s for s in range(S) if s not in set(slots.tolist())]
+    for s in untouched:
+        poison_like(pool[s])
+    u = torch.full((T, E), float("nan"), dtype=dt_act, device="cuda")
+    ws = B.workspace(4096)
+    B.ssm_conv1d_silu(d, dw, _dev(xz, dt_act), meta, pool, u, ws)
+    assert B.take_status(ws) == 0
+    got_u = u.to(torch.float64).cpu().numpy()
+    got_pool = pool.to(torch.float64).cpu().numpy()
+    for i in range(len(lens)):
+        a, b = cu[i], cu[i + 1]
+        s = slots[i]
+        ref_u, ref_st = om.conv1d_silu(w, xz[a:b, :E].astype(np.float64),
+                                       pool0[s].astype(np.float64) if hi[i] else None, act)
+        if b > a:
+            assert_close(got_u[a:b], ref_u, TOL[act], f"u of sequence {i}")
+        # the new history is a copy of inputs: bit-exact
+        assert np.array_equal(got_pool[s], ref_st), f"history of sequence {i}"
+    raw = pool.view(torch.int16 if act == "bf16" else torch.int32).cpu().numpy()
+    for s in untouched:
+        assert np.all(raw[s] == (0x7FC1 if act == "bf16" else 0x7FC0DEAD)), f"slot {s} was touched"
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_conv_decode(B, act):
+    rng = np.random.default_rng(21)
+    shape = synth.LayerShape(64, 192, 16, 16, 4, 1, act)
+    E, K = shape.d_shard, 4
+    S, Bd = 12, 5
+    slots = np.array([3, 0, 11, 7, 5], np.int32)
+    xz = _rnd_host(rng, (Bd, 2 * E), act)
+    pool0 = _rnd_host(rng, (S, E, K - 1), act)
+    hw = synth.make_general_layer(shape, 4)
+    w = f64(hw)
+    dt_act = torch.float32 if act == "f32" else torch.bfloat16
+    d = B.make_desc(shape)
+    pool = _dev(pool0, dt_act)
+    u = torch.empty(Bd, E, dtype=dt_act, device="cuda")
+    ws = B.workspace(4096)
+    sl = torch.from_numpy(slots).cuda()
+    B.ssm_decode_conv(d, B.upload_weights(hw, act), _dev(xz, dt_act), sl, pool, u, ws)
+    assert B.take_status(ws) == 0
+    gu = u.to(torch.float64).cpu().numpy()
+    gp = pool.to(torch.float64).cpu().numpy()
+    for i in range(Bd):
+        s = slots[i]
+        win = np.concatenate([pool0[s].astype(np.float64), xz[i, :E, None].astype(np.float64)], axis=1)
+        ref = om.rnd(om.silu(w["conv_b"] + np.sum(w["conv_w"] * win, axis=1)), act)
+        assert_close(gu[i], ref, TOL[act], f"decode u {i}")
+        assert np.array_equal(gp[s], win[:, 1:]), "shifted window"
+    for s in set(range(S)) - set(slots.tolist()):
+        assert np.array_equal(gp[s], pool0[s].astype(np.float64))
+
+
+# -------------------------------------------------------------------- scan
+def _scan_inputs(rng, T, E, R, act, stress=False):
+    N = 16
+    u = _rnd_host(rng, (T, E), act)
+    dt = _rnd_host(rng, (T, E), act, 0.7)
+    xz = _rnd_host(rng, (T, 2 * E), act)
+    xdbl = rng.normal(size=(T, R + 2 * N)).astype(np.float32)
+    return u, dt, xz, xdbl
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("lens", [[70, 1, 0, 33, 100, 31, 65], [300], [1, 2, 3, 31, 32, 33, 64, 65, 0, 5]])
+def test_selective_scan(B, act, lens):
+    rng = np.random.default_rng(sum(lens) + len(lens))
+    shape = synth.LayerShape(64, 128, 16, 16, 4, 1, act)
+    E, N, R = shape.d_shard, 16, 16
+    S = len(lens) + 3
+    cu, slots, hi = _meta_case(rng, lens, S)
+    T = int(cu[-1])
+    u, dt, xz, xdbl = _scan_inputs(rng, T, E, R, act)
+    hw = synth.make_general_layer(shape, 8)
+    w = f64(hw)
+    pool0 = rng.normal(size=(S, E, N)).astype(np.float32)
+    dt_act = torch.float32 if act == "f32" else torch.bfloat16
+    d = B.make_desc(shape)
+    meta = B.SeqMeta(cu, slots, hi, S)
+    pool = torch.from_numpy(pool0).cuda()
+    untouched = [s for s in range(S) if s not in set(slots.tolist())]
+    for s in untouched:
+        poison_like(pool[s])
+    g = torch.full((max(T, 1), E), float("nan"), dtype=dt_act, device="cuda")
+    ws = B.workspace(B.scan_scratch_workspace_bytes(d, T, len(lens)))
+    B.ssm_selective_scan(d, B.upload_weights(hw, act), _dev(u, dt_act), _dev(dt, dt_act), _dev(xz, dt_act),
+                         torch.from_numpy(xdbl).cuda(), meta, pool, g, ws)
+    assert B.take_status(ws) == 0
+    gg = g.to(torch.float64).cpu().numpy()
+    gp = pool.to(torch.float64).cpu().numpy()
+    Bm, Cm = xdbl[:, R:R + N].astype(np.float64), xdbl[:, R + N:].astype(np.float64)
+    for i in range(len(lens)):
+        a, b = cu[i], cu[i + 1]
+        s = slots[i]
+        h0 = pool0[s].astype(np.float64) if hi[i] else np.zeros((E, N))
+        ref_g, ref_h = om.selective_scan(w, u[a:b].astype(np.float64), dt[a:b].astype(np.float64),
+                                         xz[a:b, E:].astype(np.float64), Bm[a:b], Cm[a:b], h0, act)
+        if b > a:
+            assert_close(gg[a:b], ref_g, TOL[act], f"g of sequence {i} (len {b - a})")
+        assert_close(gp[s], ref_h, 2e-5 if act == "f32" else 1e-4, f"state of sequence {i} (len {b - a})")
+    raw = pool.view(torch.int32).cpu().numpy()
+    for s in untouched:
+        assert np.all(raw[s] == 0x7FC0DEAD), f"slot {s} was touched"
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_selective_scan_long_sequence_many_windows(B, act):
+    """One long sequence crossing ~100 windows: exercises the window-to-window state links."""
+    rng = np.random.default_rng(99)
+    shape = synth.LayerShape(64, 64, 16, 16, 4, 1, act)
+    E, N, R = 64, 16, 16
+    T = 3333
+    u, dt, xz, xdbl = _scan_inputs(rng, T, E, R, act)
+    dt = (dt - 2.0).astype(np.float32)        # small steps: long memory across windows
+    if act == "bf16":
+        dt = synth.round_bf16_f32(dt)
+    hw = synth.make_general_layer(shape, 9)
+    w = f64(hw)
+    dt_act = torch.float32 if act == "f32" else torch.bfloat16
+    d = B.make_desc(shape)
+    meta = B.SeqMeta([0, T], [1], [1], 2)
+    pool0 = rng.normal(size=(2, E, N)).astype(np.float32)
+    pool = torch.from_numpy(pool0).cuda()
+    g = torch.empty(T, E, dtype=dt_act, device="cuda")
+    ws = B.workspace(B.scan_scratch_workspace_bytes(d, T, 1))
+    B.ssm_selective_scan(d, B.upload_weights(hw, act), _dev(u, dt_act), _dev(dt, dt_act), _dev(xz, dt_act),
+                         torch.from_numpy(xdbl).cuda(), meta, pool, g, ws)
+    assert B.take_status(ws) == 0
+    ref_g, ref_h = om.selective_scan(w, u.astype(np.float64), dt.astype(np.float64), xz[:, E:].astype(np.float64),
+                                     xdbl[:, R:R + N].astype(np.float64), xdbl[:, R + N:].astype(np.float64),
+                                     pool0[1].astype(np.float64), act)
+    assert_close(g.to(torch.float64).cpu().numpy(), ref_g, TOL[act], "g")
+    assert_close(pool[1].to(torch.float64).cpu().numpy(), ref_h, 2e-5 if act == "f32" else 1e-4, "state")
+    assert np.array_equal(pool[0].cpu().numpy(), pool0[0])
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_decode_ssm(B, act):
+    rng = np.random.default_rng(31)
+    shape = synth.LayerShape(64, 128, 16, 16, 4, 1, act)
+    E, N, R = 128, 16, 16
+    S, Bd = 9, 4
+    slots = np.array([8, 2, 0, 5], np.int32)
+    u, dt, xz, xdbl = _scan_inputs(rng, Bd, E, R, act)
+    hw = synth.make_general_layer(shape, 12)
+    w = f64(hw)
+    pool0 = rng.normal(size=(S, E, N)).astype(np.float32)
+    dt_act = torch.float32 if act == "f32" else torch.bfloat16
+    d = B.make_desc(shape)
+    pool = torch.from_numpy(pool0).cuda()
+    g = torch.empty(Bd, E, dtype=dt_act, device="cuda")
+    ws = B.workspace(4096)
+    B.ssm_decode_ssm(d, B.upload_weights(hw, act), _dev(u, dt_act), _dev(dt, dt_act), _dev(xz, dt_act),
+                     torch.from_numpy(xdbl).cuda(), torch.from_numpy(slots).cuda(), pool, g, ws)
+    assert B.take_status(ws) == 0
+    gg = g.to(torch.float64).cpu().numpy()
+    gp = pool.cpu().numpy().astype(np.float64)
+    for i in range(Bd):
+        s = slots[i]
+        ref_g, ref_h = om.selective_scan(w, u[i:i + 1].astype(np.float64), dt[i:i + 1].astype(np.float64),
+                                         xz[i:i + 1, E:].astype(np.float64), xdbl[i:i + 1, R:R + N].astype(np.float64),
+                                         xdbl[i:i + 1, R + N:].astype(np.float64), pool0[s].astype(np.float64), act)
+        assert_close(gg[i], ref_g[0], TOL[act], f"g {i}")
+        assert_close(gp[s], ref_h, 1e-5, f"state {i}")
+    for s in set(range(S)) - set(slots.tolist()):
+        assert np.array_equal(gp[s], pool0[s].astype(np.float64))
+
+
+def test_bad_device_slot_is_reported_not_followed(B):
+    """A slot outside the pool in device metadata: the kernels skip it and flag the status."""
+    shape = synth.LayerShape(64, 64, 16, 16, 4, 1, "f32")
+    d = B.make_desc(shape)
+    hw = synth.make_general_layer(shape, 1)
+    S = 3
+    pool = torch.zeros(S, 64, 16, device="cuda")
+    slots = torch.tensor([1, 7], dtype=torch.int32, device="cuda")
+    u = torch.randn(2, 64, device="cuda")
+    xz = torch.randn(2, 128, device="cuda")
+    xdbl = torch.randn(2, 48, device="cuda")
+    g = torch.empty(2, 64, device="cuda")
+    ws = B.workspace(4096)
+    B.ssm_decode_ssm(d, B.upload_weights(hw, "f32"), u, u, xz, xdbl, slots, pool, g, ws)
+    st = B.take_status(ws)
+    assert st & B.SSM_STATUS_BAD_SLOT
+    assert torch.count_nonzero(pool[0]) == 0 and torch.count_nonzero(pool[2]) == 0
+    assert torch.count_nonzero(pool[1]) > 0
+    assert B.take_status(ws) == 0   # cleared by the read

@@ -1,0 +1,182 @@
+"""End-to-end parity of the C ABI (prefill stages, exchange, decode) against the oracle at
+sizes the oracle finishes in seconds: several GEMM tiles, ragged tails, packed sequences
+of mixed lengths with continuing and fresh states, all shards of a channel split.
+"""
+import numpy as np
+import pytest
+
+from mixer_cases import TOL, GpuLayer, assert_close, f64, host
+from oracle import mixer as om
+from paper_2602_21144_amd import synth
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _case(act, P, init, seed=0, dm=64, E_tot=256, R=16):
+    shape = synth.LayerShape(dm, E_tot, 16, R, 4, P, act)
+    if init == "general":
+        full = synth.make_general_layer(shape, seed)
+    else:
+        full = synth.make_layer(shape, seed, stress=(init == "stress"))
+    return shape, full
+
+
+def _pools_host(rng, shape, S, act):
+    E, N, K = shape.d_inner, shape.d_state, shape.d_conv
+    cp = rng.normal(size=(S, E, K - 1)).astype(np.float32)
+    if act == "bf16":
+        cp = synth.round_bf16_f32(cp)
+    sp = (rng.normal(size=(S, E, N)) * 0.5).astype(np.float32)
+    return cp, sp
+
+
+def _slice(a, r, E):
+    return a[:, r * E:(r + 1) * E]
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("P", [1, 2])
+@pytest.mark.parametrize("init", ["baseline", "stress", "general"])
+def test_prefill_then_decode(act, P, init):
+    shape, full = _case(act, P, init, seed=3)
+    E = shape.d_shard
+    rng = np.random.default_rng(17)
+    lens = [37, 1, 0, 130, 2, 64, 3]
+    S = 11
+    nseq = len(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    slots = rng.permutation(S)[:nseq].astype(np.int32)
+    hi = np.array([1, 0, 1, 0, 1, 1, 0], np.int32)
+    T = int(cu[-1])
+    x = synth.make_tokens(rng, T, shape.d_model, act)
+    cp0, sp0 = _pools_host(rng, shape, S, act)
+
+    g = GpuLayer(shape, full)
+    from paper_2602_21144_amd import binding as B
+    meta = B.SeqMeta(cu, slots, hi, S)
+    conv, ssm = g.new_pools(S)
+    for r in range(P):
+        conv[r].copy_(g.to_dev(_slice(cp0, r, E)))
+        ssm[r].copy_(torch.from_numpy(np.ascontiguousarray(_slice(sp0, r, E))).cuda())
+    ys = g.prefill(x, meta, conv, ssm)
+    for r in range(P):
+        assert B.take_status(g.last_ws[r]) == 0
+
+    w64 = f64(full)
+    shards = [om.shard_weights(w64, r, P) for r in range(P)]
+    cps = [_slice(cp0, r, E).astype(np.float64) for r in range(P)]
+    sps = [_slice(sp0, r, E).astype(np.float64) for r in range(P)]
+    s1, s2, _ = om.tp_prefill(shards, x.astype(np.float64), cu, slots, hi, cps, sps, act)
+    tol = TOL[act]
+    for r in range(P):
+        assert_close(host(ys[r]), s2[r]["y"], tol, f"y_partial shard {r}")
+        assert_close(host(ssm[r]), s2[r]["ssm_pool"], 1e-4 if act == "bf16" else 2e-5, f"ssm_pool shard {r}")
+        assert_close(host(conv[r]), s1[r]["conv_pool"], tol, f"conv_pool shard {r}")
+    if P > 1:
+        assert_close(sum(host(ys[r]) for r in range(P)), sum(s2[r]["y"] for r in range(P)), tol, "sum of partials")
+
+    # decode: 4 steps over the non-empty sequences
+    dec = [i for i in range(nseq) if lens[i] > 0]
+    dslots = slots[dec]
+    sl_dev = torch.from_numpy(dslots).cuda()
+    cps = [s["conv_pool"] for s in s1]
+    sps = [s["ssm_pool"] for s in s2]
+    for step in range(4):
+        xt = synth.make_tokens(rng, len(dec), shape.d_model, act)
+        yd = g.decode(xt, sl_dev, conv, ssm)
+        d1, d2, _ = om.tp_decode_step(shards, xt.astype(np.float64), dslots, cps, sps, act)
+        cps = [d["conv_pool"] for d in d1]
+        sps = [d["ssm_pool"] for d in d2]
+        for r in range(P):
+            assert_close(host(yd[r]), d2[r]["y"], tol, f"decode step {step} shard {r}")
+    for r in range(P):
+        assert_close(host(ssm[r]), sps[r], 1e-4 if act == "bf16" else 2e-5, f"ssm_pool after decode, shard {r}")
+        assert_close(host(conv[r]), cps[r], tol, f"conv_pool after decode, shard {r}")
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_shards_sum_to_full_width_on_gpu(act):
+    """Section IV-B: concatenated shard states and summed partial outputs equal the
+    unsplit layer (all run on the GPU; checked against each other and the oracle)."""
+    shape4, full = _case(act, 4, "stress", seed=5, E_tot=256)
+    shape1 = synth.LayerShape(shape4.d_model, shape4.d_inner, 16, shape4.dt_rank, 4, 1, act)
+    rng = np.random.default_rng(3)
+    lens = [90, 45]
+    cu = np.array([0, 90, 135], np.int32)
+    slots = np.array([1, 0], np.int32)
+    hi = np.zeros(2, np.int32)
+    x = synth.make_tokens(rng, 135, shape4.d_model, act)
+    from paper_2602_21144_amd import binding as B
+    g4, g1 = GpuLayer(shape4, full), GpuLayer(shape1, full)
+    meta = B.SeqMeta(cu, slots, hi, 2)
+    c4, s4 = g4.new_pools(2)
+    c1, s1 = g1.new_pools(2)
+    y4 = g4.prefill(x, meta, c4, s4)
+    y1 = g1.prefill(x, meta, c1, s1)
+    ysum = sum(host(y4[r]) for r in range(4))
+    assert_close(ysum, host(y1[0]), TOL[act], "sum of 4 shard partials vs full width")
+    assert_close(np.concatenate([host(s4[r]) for r in range(4)], axis=1), host(s1[0]),
+                 1e-4 if act == "bf16" else 2e-5, "states")
+    ref = om.prefill(f64(full), x.astype(np.float64), cu, slots, hi, np.zeros((2, 256, 3)), np.zeros((2, 256, 16)), act)
+    assert_close(host(y1[0]), ref["y"], TOL[act], "full width vs oracle")
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_chunked_prefill_equals_whole_on_gpu(act):
+    """Prefill in pieces with the cache carried between calls (pieces shorter than the
+    convolution history included) gives the whole-prompt result (Section IV-A)."""
+    shape, full = _case(act, 1, "stress", seed=8, E_tot=128)
+    rng = np.random.default_rng(8)
+    L = 200
+    x = synth.make_tokens(rng, L, shape.d_model, act)
+    from paper_2602_21144_amd import binding as B
+    g = GpuLayer(shape, full)
+    cw, sw = g.new_pools(1)
+    yw = host(g.prefill(x, B.SeqMeta([0, L], [0], [0], 1), cw, sw)[0])
+    cc, sc = g.new_pools(1)
+    parts = [0, 1, 3, 70, 71, 150, 200]
+    yc = []
+    for a, b in zip(parts[:-1], parts[1:]):
+        yc.append(host(g.prefill(x[a:b], B.SeqMeta([0, b - a], [0], [1 if a > 0 else 0], 1), cc, sc)[0]))
+    assert_close(np.concatenate(yc), yw, TOL[act], "chunked y")
+    assert_close(host(sc[0]), host(sw[0]), 1e-4 if act == "bf16" else 2e-5, "state")
+    assert torch.equal(cc[0], cw[0])
+
+
+def test_prefill_is_deterministic():
+    shape, full = _case("bf16", 2, "baseline", seed=4)
+    rng = np.random.default_rng(4)
+    cu = np.array([0, 500, 777], np.int32)
+    x = synth.make_tokens(rng, 777, shape.d_model, "bf16")
+    from paper_2602_21144_amd import binding as B
+    g = GpuLayer(shape, full)
+    meta = B.SeqMeta(cu, [0, 1], [0, 0], 2)
+    outs = []
+    for _ in range(2):
+        c, s = g.new_pools(2)
+        y = g.prefill(x, meta, c, s)
+        outs.append((y[0].clone(), s[0].clone(), c[0].clone()))
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a.view(torch.uint8) if a.dtype != torch.float32 else a, b.view(torch.uint8) if b.dtype != torch.float32 else b)
+
+
+def test_empty_batch_and_empty_sequences():
+    shape, full = _case("bf16", 1, "baseline", seed=6, E_tot=128)
+    from paper_2602_21144_amd import binding as B
+    g = GpuLayer(shape, full)
+    c, s = g.new_pools(4, poison=True)
+    # all-empty batch: fresh empty sequences end with zero cache; continuing ones keep it
+    meta = B.SeqMeta([0, 0, 0], [2, 3], [0, 1], 4)
+    before3 = (c[0][3].clone(), s[0][3].clone())
+    g.prefill(np.zeros((0, shape.d_model), np.float32), meta, c, s)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(s[0][2]) == 0 and torch.count_nonzero(c[0][2].float()) == 0
+    assert torch.equal(c[0][3].view(torch.int16), before3[0].view(torch.int16))
+    assert torch.equal(s[0][3].view(torch.int32), before3[1].view(torch.int32))
