@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of the selective-SSM mixer shard on one MI355X.
+
+Workload: a Mamba-2.8B-shaped layer (d_model 2560, d_inner 5120 split over 2 ranks, so
+this GPU runs the 2560-channel shard 0; N 16, dt_rank 160, conv 4), bf16 activations
+and weights with fp32 scan state; 8 prompts of 2048 tokens prefilled, then 128 decode
+steps over the 8 sequences. One step = that prefill plus the 128 decode steps.
+
+Per shard, the work of one step is: stage 1 (in_proj, conv1d+SiLU, x_proj), the sum of
+the x_proj partials over ranks (here: shard 1's partial, computed outside the timed
+region because it is the other GPU's work, added by the library's reduce kernel), and
+stage 2 (dt_proj, selective scan, out_proj); the same for every decode step.
+
+Prints one JSON line: prefill tokens/s (value), decode us/step, ms per step, a roofline
+entry for the kernel that takes the most time in a step (its duration measured with HIP
+events on the launch stream during the timed region), a per-kernel breakdown from one
+extra profiled step, and the CPU oracle timed on a bounded sample on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "selective-scan prefill tokens/s + decode µs/step per shard; % HBM/MFMA peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic(name, sh, T, Bd, nseq):
+    """(roof, amount per launch, unit) of a kernel role: flops for the dense in/out
+    projections in prefill, else bytes each operand must move once (s = act bytes)."""
+    s = 2 if sh.act == "bf16" else 4
+    E, dm, N, R, K, W = sh.d_shard, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv, sh.w_dbl
+    M = T if name.startswith("prefill") else Bd
+    table = {
+        "prefill.in_proj": ("mfma", 2.0 * T * 2 * E * dm),
+        "prefill.out_proj": ("mfma", 2.0 * T * dm * E),
+        "prefill.x_proj": ("hbm", T * E * s + W * E * s + T * W * 4),
+        "prefill.dt_proj": ("hbm", T * R * 4 + E * R * s + T * E * s),
+        "prefill.conv1d": ("hbm", 2 * T * E * s + E * (K + 1) * s),
+        "prefill.conv_history": ("hbm", 2 * nseq * E * (K - 1) * s),
+        "prefill.scan_main": ("hbm", 4 * T * E * s + T * 2 * N * 4 + nseq * E * N * 4 + E * (N + 2) * 4),
+        "decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
+        "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
+        "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
+        "decode.dt_proj": ("hbm", E * R * s + M * R * 4 + M * E * s),
+        "decode.state_update": ("hbm", 2 * M * E * N * 4 + 4 * M * E * s + M * 2 * N * 4 + E * (N + 2) * 4),
+        "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s),
+    }
+    if name in table:
+        roof, amt = table[name]
+        return roof, float(amt), ("TFLOP/s" if roof == "mfma" else "GB/s")
+    if name == "exchange.reduce_add":
+        return "hbm", None, "GB/s"
+    return "hbm", None, "GB/s"
+
+
+def achieved(roof, amount, avg_ms):
+    if amount is None or avg_ms <= 0:
+        return None
+    per_s = amount / (avg_ms * 1e-3)
+    return per_s / 1e12 if roof == "mfma" else per_s / 1e9
+
+
+def run(args):
+    import numpy as np
+    import torch
+
+    from paper_2602_21144_amd import binding as B
+    from paper_2602_21144_amd import synth
+
+    cfg = synth.CONFIGS["mamba2.8b_tp2"]
+    sh = cfg["shape"]
+    Bsz, L, steps_dec = cfg["batch"], cfg["prefill_len"], cfg["decode_steps"]
+    T = Bsz * L
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    B.lib()
+
+    log("drawing seeded inputs")
+    full = synth.make_layer(sh, cfg["seed"])
+    rng = full["_rng"]
+    x_host = synth.make_tokens(rng, T, sh.d_model, sh.act)
+    xdec_host = np.stack([synth.make_tokens(rng, Bsz, sh.d_model, sh.act) for _ in range(steps_dec)])
+    S = Bsz + 16
+    slots = synth.make_slots(rng, Bsz)
+
+    log("uploading and slicing weights")
+    full_dev = B.upload_weights(full, sh.act, dev)
+    desc = [B.make_desc(sh, r) for r in range(sh.shard_count)]
+    wdev = []
+    for r in range(sh.shard_count):
+        out = B.empty_shard_weights(sh, dev)
+        B.ssm_shard_slice_weights(desc[r], full_dev, out)
+        wdev.append(out)
+    del full_dev
+    wst = [B.weights_struct(w) for w in wdev]
+    act = B.torch_act(sh.act)
+    x = torch.from_numpy(x_host).to(dev, act)
+    xdec = torch.from_numpy(xdec_host).to(dev, act)
+    cu = np.arange(0, T + 1, L, dtype=np.int32)
+    meta = B.SeqMeta(cu, slots, np.zeros(Bsz, np.int32), S, dev)
+    slots_dev = torch.from_numpy(slots).to(dev)
+    E, N, K, W = sh.d_shard, sh.d_state, sh.d_conv, sh.w_dbl
+    conv = [torch.zeros(S, E, K - 1, dtype=act, device=dev) for _ in range(sh.shard_count)]
+    ssm = [torch.zeros(S, E, N, dtype=torch.float32, device=dev) for _ in range(sh.shard_count)]
+    wsp = [B.workspace(B.prefill_workspace_bytes(desc[r], T, Bsz), dev) for r in range(sh.shard_count)]
+    wsd = [B.workspace(B.decode_workspace_bytes(desc[r], Bsz), dev) for r in range(sh.shard_count)]
+    p0 = torch.empty(T, W, dtype=torch.float32, device=dev)
+    q0 = torch.empty(Bsz, W, dtype=torch.float32, device=dev)
+    y = torch.empty(T, sh.d_model, dtype=act, device=dev)
+    yd = torch.empty(Bsz, sh.d_model, dtype=act, device=dev)
+
+    log("x_proj partials of the other shard (the other GPU's work, outside the timed region)")
+    p1_pref = torch.zeros(T, W, dtype=torch.float32, device=dev)
+    p1_dec = torch.zeros(steps_dec, Bsz, W, dtype=torch.float32, device=dev)
+    pr = torch.empty(T, W, dtype=torch.float32, device=dev)
+    qr = torch.empty(Bsz, W, dtype=torch.float32, device=dev)
+    for r in range(1, sh.shard_count):
+        B.ssm_shard_prefill_stage1(desc[r], wst[r], x, meta, conv[r], pr, wsp[r])
+        B.ssm_reduce_add_f32(p1_pref, pr)
+        for k in range(steps_dec):
+            B.ssm_shard_decode_stage1(desc[r], wst[r], xdec[k], slots_dev, conv[r], qr, wsd[r])
+            B.ssm_reduce_add_f32(p1_dec[k], qr)
+    torch.cuda.synchronize()
+
+    def prefill():
+        B.ssm_shard_prefill_stage1(desc[0], wst[0], x, meta, conv[0], p0, wsp[0])
+        B.ssm_reduce_add_f32(p0, p1_pref)
+        B.ssm_shard_prefill_stage2(desc[0], wst[0], p0, meta, ssm[0], y, wsp[0])
+
+    def decode(k):
+        B.ssm_shard_decode_stage1(desc[0], wst[0], xdec[k], slots_dev, conv[0], q0, wsd[0])
+        B.ssm_reduce_add_f32(q0, p1_dec[k])
+        B.ssm_shard_decode_stage2(desc[0], wst[0], q0, slots_dev, ssm[0], yd, wsd[0])
+
+    def step(evs=None):
+        if evs:
+            evs[0].record()
+        prefill()
+        if evs:
+            evs[1].record()
+        for k in range(steps_dec):
+            decode(k)
+        if evs:
+            evs[2].record()
+
+    log(f"warmup {args.warmup} step(s)")
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+
+    log("one profiled step (every kernel bracketed by events) for the breakdown")
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True)
+    step()
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    breakdown = B.ssm_timing_collect()
+    dominant = max(breakdown, key=lambda n: breakdown[n][1])
+
+    log(f"timed region: {args.steps} step(s); events bracket {dominant} only")
+    B.ssm_timing_enable(True, dominant)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    B.ssm_timing_enable(False)
+    dom_launches, dom_ms = B.ssm_timing_collect()[dominant]
+    pre_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    dec_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    step_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
+    assert B.take_status(wsp[0]) == 0 and B.take_status(wsd[0]) == 0
+    log(f"prefill {np.mean(pre_ms):.3f} ms, decode {1e3 * np.mean(dec_ms) / steps_dec:.2f} us/step, "
+        f"step {step_ms:.3f} ms (host wall {1e3 * wall / args.steps:.3f} ms)")
+
+    kernels = {}
+    for name, (n, ms) in sorted(breakdown.items(), key=lambda kv: -kv[1][1]):
+        roof, amt, unit = algorithmic(name, sh, T, Bsz, Bsz)
+        avg = ms / n
+        a = achieved(roof, amt, avg)
+        peak = PEAK_BF16_TFLOPS if roof == "mfma" else PEAK_HBM_GBS
+        kernels[name] = {"launches": n, "avg_us": round(1e3 * avg, 3), "share_of_step": round(ms / sum(v[1] for v in breakdown.values()), 4),
+                         "bound": roof, "achieved": None if a is None else round(a, 1), "unit": unit,
+                         "frac": None if a is None else round(a / peak, 4)}
+    roof, amt, unit = algorithmic(dominant, sh, T, Bsz, Bsz)
+    dom_avg = dom_ms / dom_launches
+    ach = achieved(roof, amt, dom_avg)
+    peak = PEAK_BF16_TFLOPS if roof == "mfma" else PEAK_HBM_GBS
+    roofline = {"kernel": dominant, "bound": roof, "achieved": None if ach is None else round(ach, 2), "peak": peak,
+                "unit": unit, "frac": None if ach is None else round(ach / peak, 4), "traffic": None,
+                "avg_us": round(1e3 * dom_avg, 3), "launches_timed": dom_launches,
+                "algorithmic_per_launch": amt}
+
+    scan_ms = sum(breakdown[k][1] for k in breakdown if k.startswith("prefill.scan"))
+    result = {
+        "metric": METRIC, "value": round(T / (np.mean(pre_ms) * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "Mamba-2.8B-shaped mixer layer, shard 0 of a 2-way channel split: d_model 2560, "
+                               "d_inner 2560 of 5120, d_state 16, dt_rank 160, d_conv 4; batch 8 x prefill 2048, "
+                               "then 128 decode steps; bf16 activations/weights, fp32 state; seed 1",
+                   "d_model": sh.d_model, "d_inner_shard": sh.d_shard, "d_inner_total": sh.d_inner,
+                   "d_state": sh.d_state, "dt_rank": sh.dt_rank, "d_conv": sh.d_conv, "batch": Bsz,
+                   "prefill_len": L, "decode_steps": steps_dec, "shard": "0 of 2"},
+        "prefill_ms": round(float(np.mean(pre_ms)), 4),
+        "decode_us_per_step": round(float(1e3 * np.mean(dec_ms) / steps_dec), 3),
+        "scan_tokens_per_s": round(T / (scan_ms * 1e-3), 1) if scan_ms > 0 else None,
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    return result, (sh, full, x_host, xdec_host, slots, S)
+
+
+def cpu_baseline(ctx):
+    """The oracle (float64 numpy, untuned) on a bounded sample of the same workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import mixer as om
+
+    sh, full, x_host, xdec_host, slots, S = ctx
+    w64 = {k: np.asarray(v, np.float64) for k, v in full.items() if not k.startswith("_")}
+    shards = [om.shard_weights(w64, r, sh.shard_count) for r in range(sh.shard_count)]
+    E, N, K = sh.d_shard, sh.d_state, sh.d_conv
+    nb = len(slots)
+    L = x_host.shape[0] // nb
+    cu = np.arange(0, nb * L + 1, L)
+    sl = np.arange(nb)
+    zc = np.zeros((nb, E, K - 1))
+    zs = np.zeros((nb, E, N))
+    xs = x_host.astype(np.float64)
+    # the other rank's x_proj partials are inputs here, as on the GPU (not timed)
+    o1 = om.prefill_stage1(shards[1], xs, cu, sl, np.zeros(nb), zc, sh.act)
+    t0 = time.perf_counter()
+    s1 = om.prefill_stage1(shards[0], xs, cu, sl, np.zeros(nb), zc, sh.act)
+    s2 = om.prefill_stage2(shards[0], s1, s1["x_dbl"] + o1["x_dbl"], cu, sl, np.zeros(nb), zs, sh.act)
+    t_pre = time.perf_counter() - t0
+    cp, sp, cp1 = s1["conv_pool"], s2["ssm_pool"], o1["conv_pool"]
+    nsteps = xdec_host.shape[0]
+    t_dec = 0.0
+    for k in range(nsteps):
+        xd = xdec_host[k].astype(np.float64)
+        d1o = om.decode_stage1(shards[1], xd, sl, cp1, sh.act)
+        cp1 = d1o["conv_pool"]
+        t0 = time.perf_counter()
+        d1 = om.decode_stage1(shards[0], xd, sl, cp, sh.act)
+        d2 = om.decode_stage2(shards[0], d1, d1["x_dbl"] + d1o["x_dbl"], sl, sp, sh.act)
+        t_dec += time.perf_counter() - t0
+        cp, sp = d1["conv_pool"], d2["ssm_pool"]
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": round(nb * L / t_pre, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"the whole step on the host: shard 0 prefill of {nb} x {L} tokens (stage 1 + stage 2, "
+                      f"float64 numpy, untuned) and {nsteps} decode steps of {nb} sequences; the other shard's "
+                      f"x_proj partials are precomputed inputs, as on the GPU",
+            "decode_us_per_step": round(1e6 * t_dec / nsteps, 1), "prefill_s": round(t_pre, 2),
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported (this build runs on one GPU)",
+              file=sys.stderr)
+        sys.exit(2)
+    result, ctx = run(args)
+    if not args.no_cpu_baseline:
+        log("CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(ctx)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -222,6 +222,23 @@ int ssm_decode_ssm(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, c
                    const int32_t* cache_slot, float* ssm_pool, int32_t num_slots, void* g,
                    void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------ measurement
+ * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
+ * the library launches from the calling thread is bracketed by two HIP events on the
+ * launch stream (the events add a few microseconds of device time per launch; leave
+ * timing off in production). */
+typedef struct ssm_kernel_time {
+    char name[48];       /* kernel role, e.g. "prefill.in_proj", "decode.state_update" */
+    int64_t launches;    /* launches recorded since the last collection */
+    double total_ms;     /* summed event-to-event device time */
+} ssm_kernel_time_t;
+/* on: 1 to record, 0 to stop. only: NULL to time every kernel, else the one kernel
+ * name to time (keeps the event overhead off the other launches). */
+int ssm_timing_enable(int32_t on, const char* only);
+/* Waits for the recorded events, sums time per kernel name into out[0 .. *count), at
+ * most max entries, and forgets the records. SSM_E_HIP if an event could not be read. */
+int ssm_timing_collect(ssm_kernel_time_t* out, int32_t max, int32_t* count);
+
 #ifdef __cplusplus
 }
 #endif

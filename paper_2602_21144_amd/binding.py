@@ -45,6 +45,10 @@ class Weights(ctypes.Structure):
         "dt_proj_b", "A_log", "D")]
 
 
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
+
+
 class SeqMetaC(ctypes.Structure):
     _fields_ = [("cu_seqlens", ctypes.c_void_p), ("cache_slot", ctypes.c_void_p),
                 ("has_initial_state", ctypes.c_void_p), ("nseq", ctypes.c_int32)]
@@ -75,6 +79,8 @@ _SIGS = {
     "ssm_selective_scan": ([_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_decode_conv": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_decode_ssm": ([_P, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_timing_enable": ([_I32, ctypes.c_char_p], _I32),
+    "ssm_timing_collect": ([_P, _I32, _P], _I32),
 }
 
 
@@ -302,3 +308,15 @@ def ssm_decode_ssm(desc, weights, u, dt, xz, x_dbl, cache_slot, ssm_pool, g, ws,
 def scan_scratch_workspace_bytes(desc: Desc, T: int, nseq: int) -> int:
     """Workspace large enough for ssm_selective_scan at (T, nseq) (header + scan scratch)."""
     return prefill_workspace_bytes(desc, T, nseq)
+
+
+def ssm_timing_enable(on: bool = True, only: Optional[str] = None):
+    _check(lib().ssm_timing_enable(1 if on else 0, only.encode() if only else None))
+
+
+def ssm_timing_collect(max_kernels: int = 64) -> Dict[str, tuple]:
+    """{kernel role: (launches, total ms)} since the last collection (waits for the events)."""
+    buf = (KernelTime * max_kernels)()
+    n = ctypes.c_int32()
+    _check(lib().ssm_timing_collect(buf, max_kernels, ctypes.byref(n)))
+    return {buf[i].name.decode(): (int(buf[i].launches), float(buf[i].total_ms)) for i in range(n.value)}

@@ -154,10 +154,18 @@ int check_ws(void* ws, size_t have, size_t need) {
 }
 
 int gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int adt, const void* B, int64_t ldb, int bdt,
-         void* C, int64_t ldc, int cdt, hipStream_t s, const char* what) {
-    SSM_TRY_HIP(launch_gemm_nt(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s), what);
+         void* C, int64_t ldc, int cdt, hipStream_t s, const char* what, GemmRole role = kGemmGeneric) {
+    KernelTimer kt(what, s);
+    SSM_TRY_HIP(launch_gemm_nt(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, role), what);
     return SSM_OK;
 }
+
+// one timed launch of a non-GEMM kernel
+#define SSM_TIMED(name, s, expr)                 \
+    do {                                         \
+        KernelTimer kt_(name, s);                \
+        SSM_TRY_HIP((expr), name);               \
+    } while (0)
 
 ConvArgs conv_args(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int64_t T,
                    const int32_t* cu, const int32_t* slot, const int32_t* hi, int nseq, void* conv_pool, int S,
@@ -199,12 +207,12 @@ int prefill1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void
              const ssm_seq_meta_t* m, void* conv_pool, int32_t S, float* xdbl, const PrefillWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    SSM_TRY(gemm(T, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "in_proj"));
+    SSM_TRY(gemm(T, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "prefill.in_proj", kGemmInProj));
     ConvArgs ca = conv_args(d, w, L.xz, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq, conv_pool,
                             S, L.u, L.status);
-    SSM_TRY_HIP(launch_conv_prefill(ca, adt == SSM_BF16, s), "conv1d");
-    SSM_TRY_HIP(launch_conv_state_update(ca, adt == SSM_BF16, s), "conv history");
-    SSM_TRY(gemm(T, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "x_proj"));
+    SSM_TIMED("prefill.conv1d", s, launch_conv_prefill(ca, adt == SSM_BF16, s));
+    SSM_TIMED("prefill.conv_history", s, launch_conv_state_update(ca, adt == SSM_BF16, s));
+    SSM_TRY(gemm(T, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "prefill.x_proj", kGemmXProj));
     return SSM_OK;
 }
 
@@ -212,11 +220,11 @@ int prefill2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const floa
              const ssm_seq_meta_t* m, float* ssm_pool, int32_t S, void* y, const PrefillWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
-    SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "dt_proj"));
+    SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, T, m->cu_seqlens, m->cache_slot, m->has_initial_state,
                             m->nseq, ssm_pool, S, L.g, L.status, L.scan);
     SSM_TRY_HIP(launch_scan_prefill(sa, adt == SSM_BF16, s), "selective scan");
-    SSM_TRY(gemm(T, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "out_proj"));
+    SSM_TRY(gemm(T, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "prefill.out_proj", kGemmOutProj));
     return SSM_OK;
 }
 
@@ -224,10 +232,10 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
             void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "in_proj"));
+    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj", kGemmInProj));
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
-    SSM_TRY_HIP(launch_conv_decode(ca, adt == SSM_BF16, s), "decode conv");
-    SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "x_proj"));
+    SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
+    SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj));
     return SSM_OK;
 }
 
@@ -235,11 +243,11 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
             const int32_t* slot, float* ssm_pool, int32_t S, void* y, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
-    SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "dt_proj"));
+    SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "decode.dt_proj", kGemmDtProj));
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, B, nullptr, slot, nullptr, B, ssm_pool, S, L.g, L.status,
                             nullptr);
-    SSM_TRY_HIP(launch_decode_ssm(sa, adt == SSM_BF16, s), "decode state update");
-    SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "out_proj"));
+    SSM_TIMED("decode.state_update", s, launch_decode_ssm(sa, adt == SSM_BF16, s));
+    SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "decode.out_proj", kGemmOutProj));
     return SSM_OK;
 }
 
@@ -441,7 +449,7 @@ int ssm_reduce_add_f32(float* dst, const float* src, int64_t n, hipStream_t s) {
     if (n == 0) return SSM_OK;
     SSM_TRY(check_ptr(dst, "dst"));
     SSM_TRY(check_ptr(src, "src"));
-    SSM_TRY_HIP(launch_reduce_add(dst, src, n, s), "reduce_add");
+    SSM_TIMED("exchange.reduce_add", s, launch_reduce_add(dst, src, n, s));
     return SSM_OK;
 }
 
@@ -459,7 +467,7 @@ int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int
     SSM_TRY(check_ptr(A, "A"));
     SSM_TRY(check_ptr(B, "B"));
     SSM_TRY(check_ptr(C, "C"));
-    return gemm(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, "gemm");
+    return gemm(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, "op.gemm");
 }
 
 int ssm_conv1d_silu(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int64_t T,
@@ -475,8 +483,8 @@ int ssm_conv1d_silu(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, con
     }
     ConvArgs ca = conv_args(d, w, xz, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq, conv_pool, S, u,
                             (int32_t*)ws);
-    SSM_TRY_HIP(launch_conv_prefill(ca, d->act_dtype == SSM_BF16, s), "conv1d");
-    SSM_TRY_HIP(launch_conv_state_update(ca, d->act_dtype == SSM_BF16, s), "conv history");
+    SSM_TIMED("op.conv1d", s, launch_conv_prefill(ca, d->act_dtype == SSM_BF16, s));
+    SSM_TIMED("op.conv_history", s, launch_conv_state_update(ca, d->act_dtype == SSM_BF16, s));
     return SSM_OK;
 }
 
@@ -514,7 +522,7 @@ int ssm_decode_conv(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, con
         SSM_TRY(check_ptr(u, "u"));
     }
     ConvArgs ca = conv_args(d, w, xz, B, nullptr, slot, nullptr, B, conv_pool, S, u, (int32_t*)ws);
-    SSM_TRY_HIP(launch_conv_decode(ca, d->act_dtype == SSM_BF16, s), "decode conv");
+    SSM_TIMED("op.decode_conv", s, launch_conv_decode(ca, d->act_dtype == SSM_BF16, s));
     return SSM_OK;
 }
 
@@ -534,7 +542,7 @@ int ssm_decode_ssm(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, cons
         SSM_TRY(check_ptr(g, "g"));
     }
     ScanArgs sa = scan_args(d, w, u, dt, xz, xdbl, B, nullptr, slot, nullptr, B, pool, S, g, (int32_t*)ws, nullptr);
-    SSM_TRY_HIP(launch_decode_ssm(sa, d->act_dtype == SSM_BF16, s), "decode state update");
+    SSM_TIMED("op.decode_state_update", s, launch_decode_ssm(sa, d->act_dtype == SSM_BF16, s));
     return SSM_OK;
 }
 

@@ -46,10 +46,12 @@ constexpr size_t kWsHeader = 256;
 __host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
 // ---------------------------------------------------------------- launchers
-// GEMM: C[M][N] = A[M][K] * B[N][K]^T. Returns hipError_t of the launch.
+// GEMM: C[M][N] = A[M][K] * B[N][K]^T. Returns hipError_t of the launch. The role picks
+// the kernel instance (each projection has its own symbol in profiles).
+enum GemmRole { kGemmGeneric = 0, kGemmInProj = 1, kGemmXProj = 2, kGemmDtProj = 3, kGemmOutProj = 4 };
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt,
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
-                          hipStream_t s);
+                          hipStream_t s, GemmRole role);
 
 struct ConvArgs {
     const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1
@@ -80,6 +82,20 @@ int scan_window_len(int64_t T, int E);
 size_t scan_scratch_bytes(int64_t max_T, int E, int max_seqs);
 hipError_t launch_scan_prefill(const ScanArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_decode_ssm(const ScanArgs& a, bool bf16_act, hipStream_t s);
+
+// Brackets the launches made while it is alive with timing events (when timing is on).
+class KernelTimer {
+  public:
+    KernelTimer(const char* name, hipStream_t s);
+    ~KernelTimer();
+    KernelTimer(const KernelTimer&) = delete;
+    KernelTimer& operator=(const KernelTimer&) = delete;
+
+  private:
+    const char* name_;
+    hipStream_t s_;
+    hipEvent_t a_;
+};
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);  // bytes: multiple of 4
 hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_t s);

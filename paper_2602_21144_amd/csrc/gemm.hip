@@ -40,7 +40,8 @@ __device__ __forceinline__ bf16x8 cvt8(float4 a, float4 b) {
     return o;
 }
 
-template <int BM, int BN, int WM, int WN, bool A_F32, bool C_F32>
+// ROLE only names the instance (one kernel symbol per projection, so profiles separate them).
+template <int ROLE, int BM, int BN, int WM, int WN, bool A_F32, bool C_F32>
 __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
                                                     const void* __restrict__ Ap, int64_t lda,
                                                     const bf16* __restrict__ B, int64_t ldb,
@@ -181,6 +182,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
 constexpr int kFBK = 16;
 constexpr int kFPad = kFBK + 1;
 
+template <int ROLE>
 __global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const float* __restrict__ A,
                                                    int64_t lda, const float* __restrict__ B, int64_t ldb,
                                                    float* __restrict__ C, int64_t ldc, int tiles_m, int tiles_n) {
@@ -252,44 +254,72 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const fl
     }
 }
 
-template <int BM, int BN, int WM, int WN, bool AF, bool CF>
+template <int ROLE, int BM, int BN, int WM, int WN, bool AF, bool CF>
 hipError_t run_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                     void* C, int64_t ldc, hipStream_t s) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, AF, CF>), dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N,
+    hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, AF, CF>), dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N,
                        (int)K, A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
     return hipGetLastError();
 }
 
-template <bool AF, bool CF>
+template <int ROLE, bool AF, bool CF>
 hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                          void* C, int64_t ldc, hipStream_t s) {
     // Tile by output size: large outputs use 256x256 (each wave 128x128, the most
     // MFMA work per LDS byte); small token counts use narrow tiles to spread the
     // weight read over more workgroups.
-    if (M <= 32) return run_bf16<32, 128, 1, 4, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (M <= 64) return run_bf16<64, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (M <= 32) return run_bf16<ROLE, 32, 128, 1, 4, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (M <= 64) return run_bf16<ROLE, 64, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-    if (big_tiles >= 512) return run_bf16<256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    return run_bf16<128, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (big_tiles >= 512) return run_bf16<ROLE, 256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return run_bf16<ROLE, 128, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
 }  // namespace
 
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt, const void* B,
-                          int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s) {
+                          int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s, GemmRole role) {
     if (M == 0 || N == 0) return hipSuccess;
     if (b_dt == SSM_F32) {
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
-        hipLaunchKernelGGL(gemm_f32_nt, dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, lda,
-                           (const float*)B, ldb, (float*)C, ldc, tm, tn);
+#define SSM_F32_CASE(R)                                                                                             \
+    case R:                                                                                                         \
+        hipLaunchKernelGGL(gemm_f32_nt<R>, dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, \
+                           lda, (const float*)B, ldb, (float*)C, ldc, tm, tn);                                      \
+        break;
+        switch (role) {
+            SSM_F32_CASE(kGemmInProj)
+            SSM_F32_CASE(kGemmXProj)
+            SSM_F32_CASE(kGemmDtProj)
+            SSM_F32_CASE(kGemmOutProj)
+            default: SSM_F32_CASE(kGemmGeneric)
+        }
+#undef SSM_F32_CASE
         return hipGetLastError();
     }
     const bool af = a_dt == SSM_F32, cf = c_dt == SSM_F32;
-    if (af && cf) return dispatch_bf16<true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (af) return dispatch_bf16<true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (cf) return dispatch_bf16<false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    return dispatch_bf16<false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    // the mixer's projections use one operand combination each
+    switch (role) {
+        case kGemmInProj:
+            if (!af && !cf) return dispatch_bf16<kGemmInProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            break;
+        case kGemmXProj:
+            if (!af && cf) return dispatch_bf16<kGemmXProj, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            break;
+        case kGemmDtProj:
+            if (af && !cf) return dispatch_bf16<kGemmDtProj, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            break;
+        case kGemmOutProj:
+            if (!af && !cf) return dispatch_bf16<kGemmOutProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            break;
+        default:
+            break;
+    }
+    if (af && cf) return dispatch_bf16<kGemmGeneric, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (af) return dispatch_bf16<kGemmGeneric, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (cf) return dispatch_bf16<kGemmGeneric, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return dispatch_bf16<kGemmGeneric, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
 }  // namespace ssm

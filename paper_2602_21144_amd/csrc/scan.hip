@@ -308,13 +308,18 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
     scan_layout((char*)a0.h_local, a.T, a.E, a.nseq, nwin, &a, &wflags);
     const int cblocks = a.E / kWave;
     if (nwin > 0) {
+        KernelTimer kt("prefill.scan_local", s);
         if (bf) hipLaunchKernelGGL(scan_local_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
         else hipLaunchKernelGGL(scan_local_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
     }
-    const int64_t lanes = (int64_t)a.E * kN;
-    hipLaunchKernelGGL(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
-                       (const int32_t*)wflags);
+    {
+        KernelTimer kt("prefill.scan_link", s);
+        const int64_t lanes = (int64_t)a.E * kN;
+        hipLaunchKernelGGL(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
+                           (const int32_t*)wflags);
+    }
     if (nwin > 0) {
+        KernelTimer kt("prefill.scan_main", s);
         if (bf) hipLaunchKernelGGL(scan_main_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
         else hipLaunchKernelGGL(scan_main_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
     }
