@@ -228,10 +228,31 @@ int prefill2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const floa
     return SSM_OK;
 }
 
+SkinnyArgs skinny(const void* A, int64_t lda, bool a_f32, const void* B, int64_t ldb, void* C, int64_t ldc, int64_t M,
+                  int64_t N, int64_t K) {
+    SkinnyArgs p{};
+    p.A = A; p.lda = lda; p.a_f32 = a_f32; p.B = (const bf16*)B; p.ldb = ldb; p.C = C; p.ldc = ldc;
+    p.M = (int)M; p.N = (int)N; p.K = (int)K;
+    return p;
+}
+
+#define SSM_SKINNY(name, s, p, epi) SSM_TIMED(name, s, launch_gemm_skinny(p, epi, s))
+
 int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x, int32_t B, const int32_t* slot,
             void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
+    if (adt == SSM_BF16) {
+        // in_proj with the conv window shift + SiLU fused into its epilogue; x_proj
+        SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, nullptr, 0, B, 2 * E, dm);
+        p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
+        p.conv_w = w->conv_w; p.conv_b = w->conv_b; p.conv_pool = conv_pool; p.Kc = d->d_conv;
+        p.u = L.u; p.z = L.xz + E * act_bytes(d); p.ld_z = 2 * E;
+        SSM_SKINNY("decode.in_proj_conv", s, p, kSkinnyConv);
+        SkinnyArgs q = skinny(L.u, E, false, w->x_proj_w, E, xdbl, W, B, W, E);
+        SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
+        return SSM_OK;
+    }
     SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj", kGemmInProj));
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
     SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
@@ -243,6 +264,18 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
             const int32_t* slot, float* ssm_pool, int32_t S, void* y, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
+    if (adt == SSM_BF16) {
+        // dt_proj with the whole recurrence step fused into its epilogue; out_proj
+        SkinnyArgs p = skinny(xdbl, W, true, w->dt_proj_w, R, nullptr, 0, B, E, R);
+        p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
+        p.u = L.u; p.z = L.xz + E * act_bytes(d); p.ld_z = 2 * E;
+        p.xdbl = xdbl; p.ld_xdbl = W; p.R = (int)R; p.b_dt = w->dt_proj_b; p.A_log = w->A_log; p.D = w->D;
+        p.pool = ssm_pool; p.g = L.g;
+        SSM_SKINNY("decode.dt_proj_state", s, p, kSkinnyState);
+        SkinnyArgs q = skinny(L.g, E, false, w->out_proj_w, E, y, dm, B, dm, E);
+        SSM_SKINNY("decode.out_proj", s, q, kSkinnyStoreBf16);
+        return SSM_OK;
+    }
     SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "decode.dt_proj", kGemmDtProj));
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, B, nullptr, slot, nullptr, B, ssm_pool, S, L.g, L.status,
                             nullptr);

@@ -33,9 +33,9 @@ __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcp
 // softplus(v) = log(1 + e^v), v itself above 20. log1p is formed as
 // log(1+w) * w / ((1+w) - 1), which keeps full relative accuracy for small w.
 __device__ __forceinline__ float softplus_f(float v) {
-    float w = fast_exp2(v * kLog2e);
-    float p = 1.0f + w;
-    float l = (p == 1.0f) ? w : fast_log2(p) * kLn2 * (w / (p - 1.0f));
+    const float w = fast_exp2(v * kLog2e);
+    const float p = 1.0f + w;
+    const float l = (p == 1.0f) ? w : fast_log2(p) * kLn2 * w * fast_rcp(p - 1.0f);
     return v > 20.0f ? v : l;
 }
 // SiLU(v) = v / (1 + e^-v)
@@ -52,6 +52,23 @@ enum GemmRole { kGemmGeneric = 0, kGemmInProj = 1, kGemmXProj = 2, kGemmDtProj =
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt,
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
                           hipStream_t s, GemmRole role);
+
+// Few-row (decode) GEMM C = A * B^T with a fused epilogue; bf16 weights.
+enum SkinnyEpi { kSkinnyStoreBf16 = 0, kSkinnyStoreF32 = 1, kSkinnyConv = 2, kSkinnyState = 3 };
+struct SkinnyArgs {
+    const void* A; int64_t lda; bool a_f32;       // A [M][K], bf16 or fp32 (rounded to bf16 on load)
+    const bf16* B; int64_t ldb;                   // B [N][K] bf16
+    void* C; int64_t ldc;                         // plain stores
+    int M, N, K;
+    const int32_t* slot; int S; int32_t* status;  // per-row cache slot (fused epilogues)
+    int E;                                        // channels of the shard
+    // kSkinnyConv (in_proj): conv weights, history pool, u out, gate values out
+    const void* conv_w; const void* conv_b; void* conv_pool; int Kc; void* u; void* z; int64_t ld_z;
+    // kSkinnyState (dt_proj): B and C in xdbl, per-channel parameters, state pool, g out (u, z in)
+    const float* xdbl; int64_t ld_xdbl; int R; const float* b_dt; const float* A_log; const float* D;
+    float* pool; void* g;
+};
+hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s);
 
 struct ConvArgs {
     const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1

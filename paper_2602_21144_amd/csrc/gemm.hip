@@ -267,10 +267,13 @@ template <int ROLE, bool AF, bool CF>
 hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                          void* C, int64_t ldc, hipStream_t s) {
     // Tile by output size: large outputs use 256x256 (each wave 128x128, the most
-    // MFMA work per LDS byte); small token counts use narrow tiles to spread the
-    // weight read over more workgroups.
-    if (M <= 32) return run_bf16<ROLE, 32, 128, 1, 4, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (M <= 64) return run_bf16<ROLE, 64, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    // MFMA work per LDS byte), mid-size ones 128x128 for more workgroups.
+    if (M <= 64) {  // few rows: the weight read dominates; stream it with many narrow workgroups
+        SkinnyArgs p{};
+        p.A = A; p.lda = lda; p.a_f32 = AF; p.B = (const bf16*)B; p.ldb = ldb; p.C = C; p.ldc = ldc;
+        p.M = (int)M; p.N = (int)N; p.K = (int)K;
+        return launch_gemm_skinny(p, CF ? kSkinnyStoreF32 : kSkinnyStoreBf16, s);
+    }
     const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
     if (big_tiles >= 512) return run_bf16<ROLE, 256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     return run_bf16<ROLE, 128, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);

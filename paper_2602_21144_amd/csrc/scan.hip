@@ -43,18 +43,60 @@ __device__ __forceinline__ int seq_of(const int32_t* cu, int nseq, int64_t t) {
 
 int64_t target_windows(int E) { return std::max<int64_t>(1, ((int64_t)kTargetWaves * kWave + E - 1) / E); }
 
-template <typename T>
-__device__ __forceinline__ void load_tok(const ScanArgs& a, int64_t t, int c, float& u, float& dt) {
-    u = to_f32(((const T*)a.u)[t * a.E + c]);
-    dt = to_f32(((const T*)a.dt)[t * a.E + c]);
+constexpr int kTB = 8;  // tokens per block: loads for block i+1 are in flight while block i computes
+
+// Per-lane activations of one block of tokens, prefetched a block ahead.
+template <typename T, bool WITH_Z>
+struct TokBlock {
+    T u[kTB], dt[kTB], z[WITH_Z ? kTB : 1];
+    __device__ __forceinline__ void load(const ScanArgs& a, int64_t b0, int64_t w1, int c) {
+#pragma unroll
+        for (int i = 0; i < kTB; ++i) {
+            const int64_t t = b0 + i < w1 ? b0 + i : w1 - 1;  // clamp: tail entries are never used
+            u[i] = ((const T*)a.u)[t * a.E + c];
+            dt[i] = ((const T*)a.dt)[t * a.E + c];
+            if constexpr (WITH_Z) z[i] = ((const T*)a.z)[t * a.ld_z + c];
+        }
+    }
+};
+
+// B_t and C_t of a block of tokens (2N floats each), staged once per workgroup in LDS.
+// Threads 0..kTB*8-1 each move one float4; all lanes then read them as broadcasts.
+struct BcStage {
+    float4 v;
+    __device__ __forceinline__ void load(const ScanArgs& a, int64_t b0, int64_t w1, int tid, int nthreads) {
+        if (tid < kTB * 8) {
+            const int i = tid >> 3, q = tid & 7;
+            const int64_t t = b0 + i < w1 ? b0 + i : w1 - 1;
+            v = *(const float4*)(a.xdbl + t * a.ld_xdbl + a.R + 4 * q);
+        }
+        (void)nthreads;
+    }
+    __device__ __forceinline__ void store(float (*lds)[2 * kN], int tid) const {
+        if (tid < kTB * 8) *(float4*)&lds[tid >> 3][4 * (tid & 7)] = v;
+    }
+};
+
+__device__ __forceinline__ void load_h(float* h, const float* src) {
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) {
+        const float4 v = ((const float4*)src)[q];
+        h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+    }
+}
+__device__ __forceinline__ void store_h(float* dst, const float* h) {
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) ((float4*)dst)[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
 }
 
 // ---------------------------------------------------------------- pass A
-template <typename T>
-__global__ __launch_bounds__(kWave) void scan_local_kernel(ScanArgs a, int nwin, int32_t* wflags) {
-    const int cblocks = a.E / kWave;
+template <typename T, int CW>
+__global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int nwin, int32_t* wflags) {
+    __shared__ float bc[2][kTB][2 * kN];
+    const int cblocks = a.E / (kWave * CW);
     const int j = blockIdx.x / cblocks;
-    const int c = (blockIdx.x % cblocks) * kWave + threadIdx.x;
+    const int tid = threadIdx.x;
+    const int c = (blockIdx.x % cblocks) * kWave * CW + tid;
     const int64_t w0 = (int64_t)j * a.win, w1 = min(w0 + a.win, a.T);
     const int s_first = uni(seq_of(a.cu, a.nseq, w0));
     const int s_last = uni(seq_of(a.cu, a.nseq, w1 - 1));
@@ -62,7 +104,7 @@ __global__ __launch_bounds__(kWave) void scan_local_kernel(ScanArgs a, int nwin,
     const int64_t b_last = uni(a.cu[s_last]), e_last = uni(a.cu[s_last + 1]);
     const bool carry_out = w1 < a.T && e_last > w1;
     const bool last_cont = b_last < w0;
-    if (blockIdx.x % cblocks == 0 && threadIdx.x == 0)
+    if (blockIdx.x % cblocks == 0 && tid == 0)
         wflags[j] = (b_first < w0 ? kFlagContIn : 0) | (carry_out ? kFlagCarryOut : 0) | (last_cont ? kFlagLastCont : 0);
 
     // copy the initial state of every non-empty sequence that starts in this window
@@ -71,44 +113,63 @@ __global__ __launch_bounds__(kWave) void scan_local_kernel(ScanArgs a, int nwin,
         if (b < w0 || e <= b || !a.has_init[s]) continue;
         const int slot = uni(a.slot[s]);
         if (slot < 0 || slot >= a.S) {
-            if (threadIdx.x == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+            if (tid == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
             continue;
         }
-        const float4* src = (const float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
-        float4* dst = (float4*)(a.h0_seq + ((int64_t)s * a.E + c) * kN);
-#pragma unroll
-        for (int q = 0; q < kN / 4; ++q) dst[q] = src[q];
+        float h[kN];
+        load_h(h, a.pool + ((int64_t)slot * a.E + c) * kN);
+        store_h(a.h0_seq + ((int64_t)s * a.E + c) * kN, h);
     }
     if (!carry_out) return;
 
+    // local end state of the last piece: from zero if it continues an earlier window,
+    // else from the sequence's own initial state
     float A2[kN], h[kN];
 #pragma unroll
     for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
     const float bdt = a.b_dt[c];
-    int64_t t = last_cont ? w0 : b_last;
+    const int64_t t0 = last_cont ? w0 : b_last;
     if (!last_cont && a.has_init[s_last]) {
         const int slot = uni(a.slot[s_last]);
-        const bool ok = slot >= 0 && slot < a.S;
+        if (slot >= 0 && slot < a.S) load_h(h, a.pool + ((int64_t)slot * a.E + c) * kN);
+        else
 #pragma unroll
-        for (int n = 0; n < kN; ++n) h[n] = ok ? a.pool[((int64_t)slot * a.E + c) * kN + n] : 0.0f;
+            for (int n = 0; n < kN; ++n) h[n] = 0.0f;
     } else {
 #pragma unroll
         for (int n = 0; n < kN; ++n) h[n] = 0.0f;
     }
     float sum_delta = 0.0f;
-    for (; t < w1; ++t) {
-        float u, dt;
-        load_tok<T>(a, t, c, u, dt);
-        const float* Bt = a.xdbl + t * a.ld_xdbl + a.R;
-        const float delta = softplus_f(dt + bdt);
-        const float du = delta * u;
-        sum_delta += delta;
+    TokBlock<T, false> nxt;
+    BcStage st;
+    nxt.load(a, t0, w1, c);
+    st.load(a, t0, w1, tid, kWave * CW);
+    st.store(bc[0], tid);
+    __syncthreads();
+    int buf = 0;
+    for (int64_t b0 = t0; b0 < w1; b0 += kTB) {
+        const TokBlock<T, false> cur = nxt;
+        const bool more = b0 + kTB < w1;
+        if (more) {
+            nxt.load(a, b0 + kTB, w1, c);
+            st.load(a, b0 + kTB, w1, tid, kWave * CW);
+        }
+        const int nt = (int)min<int64_t>(kTB, w1 - b0);
 #pragma unroll
-        for (int n = 0; n < kN; ++n) h[n] = fast_exp2(delta * A2[n]) * h[n] + du * Bt[n];
+        for (int i = 0; i < kTB; ++i) {
+            if (i < nt) {
+                const float delta = softplus_f(to_f32(cur.dt[i]) + bdt);
+                const float du = delta * to_f32(cur.u[i]);
+                sum_delta += delta;
+#pragma unroll
+                for (int n = 0; n < kN; ++n) h[n] = fast_exp2(delta * A2[n]) * h[n] + du * bc[buf][i][n];
+            }
+        }
+        if (more) st.store(bc[buf ^ 1], tid);
+        __syncthreads();
+        buf ^= 1;
     }
-    float4* hl = (float4*)(a.h_local + ((int64_t)j * a.E + c) * kN);
-#pragma unroll
-    for (int q = 0; q < kN / 4; ++q) hl[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
+    store_h(a.h_local + ((int64_t)j * a.E + c) * kN, h);
     a.sum_delta[(int64_t)j * a.E + c] = sum_delta;
 }
 
@@ -139,84 +200,113 @@ __global__ __launch_bounds__(256) void scan_link_kernel(ScanArgs a, int nwin, co
 }
 
 // ---------------------------------------------------------------- pass C
-template <typename T>
-__global__ __launch_bounds__(kWave) void scan_main_kernel(ScanArgs a) {
-    const int cblocks = a.E / kWave;
+// One token of the full recurrence for this lane's channel; returns g.
+__device__ __forceinline__ float token_step(float* h, const float* A2, float u, float dt, float z, float bdt, float Dc,
+                                            const float* bcrow) {
+    const float delta = softplus_f(dt + bdt);
+    const float du = delta * u;
+    float y = 0.0f;
+#pragma unroll
+    for (int n = 0; n < kN; ++n) {
+        h[n] = fast_exp2(delta * A2[n]) * h[n] + du * bcrow[n];
+        y += bcrow[kN + n] * h[n];
+    }
+    y += Dc * u;
+    return y * silu_f(z);
+}
+
+template <typename T, int CW>
+__global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
+    __shared__ float bc[2][kTB][2 * kN];
+    const int cblocks = a.E / (kWave * CW);
     const int j = blockIdx.x / cblocks;
-    const int c = (blockIdx.x % cblocks) * kWave + threadIdx.x;
+    const int tid = threadIdx.x;
+    const int c = (blockIdx.x % cblocks) * kWave * CW + tid;
     const int64_t w0 = (int64_t)j * a.win, w1 = min(w0 + a.win, a.T);
     float A2[kN], h[kN];
 #pragma unroll
     for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
     const float bdt = a.b_dt[c], Dc = a.D[c];
+    T* g = (T*)a.g;
+
+    // the sequence holding the first token, and the state entering the window
     int s = uni(seq_of(a.cu, a.nseq, w0));
-    int64_t sb = uni(a.cu[s]);
-    if (sb < w0) {
-        const float4* src = (const float4*)(a.h_in + ((int64_t)j * a.E + c) * kN);
+    int64_t s_beg = uni(a.cu[s]), s_end = uni(a.cu[s + 1]);
+    if (s_beg < w0) {
+        load_h(h, a.h_in + ((int64_t)j * a.E + c) * kN);
+    } else if (a.has_init[s]) {
+        load_h(h, a.h0_seq + ((int64_t)s * a.E + c) * kN);
+    } else {
 #pragma unroll
-        for (int q = 0; q < kN / 4; ++q) {
-            float4 v = src[q];
-            h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
-        }
+        for (int n = 0; n < kN; ++n) h[n] = 0.0f;
     }
-    int64_t t = w0;
-    bool first = true;
-    while (t < w1) {
-        const int64_t se = uni(a.cu[s + 1]);
-        if (se <= t) {  // empty sequence or inconsistent cu_seqlens
-            if (se < t || s + 1 >= a.nseq) {
-                if (threadIdx.x == 0) atomicOr(a.status, SSM_STATUS_BAD_SEQLENS);
-                break;
-            }
-            ++s;
-            first = false;
-            continue;
+    bool ok = true;  // false once cu_seqlens proves inconsistent
+
+    TokBlock<T, true> nxt;
+    BcStage st;
+    nxt.load(a, w0, w1, c);
+    st.load(a, w0, w1, tid, kWave * CW);
+    st.store(bc[0], tid);
+    __syncthreads();
+    int buf = 0;
+    for (int64_t b0 = w0; b0 < w1; b0 += kTB) {
+        const TokBlock<T, true> cur = nxt;
+        const bool more = b0 + kTB < w1;
+        if (more) {
+            nxt.load(a, b0 + kTB, w1, c);
+            st.load(a, b0 + kTB, w1, tid, kWave * CW);
         }
-        if (!first || sb >= w0) {
-            // a sequence starting here: zeros, or the initial state copied in pass A
-            if (a.has_init[s]) {
-                const float4* src = (const float4*)(a.h0_seq + ((int64_t)s * a.E + c) * kN);
+        const int nt = (int)min<int64_t>(kTB, w1 - b0);
+        if (ok && s_end >= b0 + nt) {
+            // no sequence ends inside this block: straight-line recurrence from registers
 #pragma unroll
-                for (int q = 0; q < kN / 4; ++q) {
-                    float4 v = src[q];
-                    h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+            for (int i = 0; i < kTB; ++i)
+                if (i < nt)
+                    g[(b0 + i) * a.E + c] = from_f32<T>(token_step(h, A2, to_f32(cur.u[i]), to_f32(cur.dt[i]),
+                                                                   to_f32(cur.z[i]), bdt, Dc, bc[buf][i]));
+        } else if (ok) {
+            // a sequence ends in this block: store its state, start the next one (empty
+            // sequences are left to the link pass); operands are re-read by token index
+#pragma unroll 1
+            for (int i = 0; i < nt && ok; ++i) {
+                const int64_t t = b0 + i;
+                while (t >= s_end) {
+                    if (s_end < t || s + 1 >= a.nseq) {
+                        ok = false;
+                        if (tid == 0) atomicOr(a.status, SSM_STATUS_BAD_SEQLENS);
+                        break;
+                    }
+                    if (s_end > s_beg) {
+                        const int slot = uni(a.slot[s]);
+                        if (slot >= 0 && slot < a.S) store_h(a.pool + ((int64_t)slot * a.E + c) * kN, h);
+                        else if (tid == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+                    }
+                    ++s;
+                    s_beg = uni(a.cu[s]);
+                    s_end = uni(a.cu[s + 1]);
+                    if (s_end > s_beg && a.has_init[s]) {
+                        load_h(h, a.h0_seq + ((int64_t)s * a.E + c) * kN);
+                    } else {
+#pragma unroll
+                        for (int n = 0; n < kN; ++n) h[n] = 0.0f;
+                    }
                 }
-            } else {
-#pragma unroll
-                for (int n = 0; n < kN; ++n) h[n] = 0.0f;
+                if (!ok) break;
+                const float u = to_f32(((const T*)a.u)[t * a.E + c]);
+                const float dt = to_f32(((const T*)a.dt)[t * a.E + c]);
+                const float z = to_f32(((const T*)a.z)[t * a.ld_z + c]);
+                g[t * a.E + c] = from_f32<T>(token_step(h, A2, u, dt, z, bdt, Dc, bc[buf][i]));
             }
         }
-        first = false;
-        const int64_t te = min(se, w1);
-        for (; t < te; ++t) {
-            float u, dt;
-            load_tok<T>(a, t, c, u, dt);
-            const float z = to_f32(((const T*)a.z)[t * a.ld_z + c]);
-            const float* Bt = a.xdbl + t * a.ld_xdbl + a.R;
-            const float delta = softplus_f(dt + bdt);
-            const float du = delta * u;
-            float y = 0.0f;
-#pragma unroll
-            for (int n = 0; n < kN; ++n) {
-                h[n] = fast_exp2(delta * A2[n]) * h[n] + du * Bt[n];
-                y += Bt[kN + n] * h[n];
-            }
-            y += Dc * u;
-            ((T*)a.g)[t * a.E + c] = from_f32<T>(y * silu_f(z));
-        }
-        if (se <= w1) {  // the sequence ends in this window: store its final state
-            const int slot = uni(a.slot[s]);
-            if (slot >= 0 && slot < a.S) {
-                float4* dst = (float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
-#pragma unroll
-                for (int q = 0; q < kN / 4; ++q) dst[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
-            } else if (threadIdx.x == 0) {
-                atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-            }
-            if (s + 1 >= a.nseq) break;
-            ++s;
-            sb = uni(a.cu[s]);
-        }
+        if (more) st.store(bc[buf ^ 1], tid);
+        __syncthreads();
+        buf ^= 1;
+    }
+    // a sequence ending exactly at the window end stores its state here
+    if (ok && s_end == w1 && s_end > s_beg) {
+        const int slot = uni(a.slot[s]);
+        if (slot >= 0 && slot < a.S) store_h(a.pool + ((int64_t)slot * a.E + c) * kN, h);
+        else if (tid == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
     }
 }
 
@@ -306,11 +396,14 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
     const int nwin = num_windows(a.T, a.win);
     int32_t* wflags = nullptr;
     scan_layout((char*)a0.h_local, a.T, a.E, a.nseq, nwin, &a, &wflags);
-    const int cblocks = a.E / kWave;
+    const int cw = (a.E % (kWave * 4) == 0) ? 4 : 1;  // waves per workgroup sharing a window
+    const dim3 grid((unsigned)(nwin * (a.E / (kWave * cw)))), block(kWave * cw);
     if (nwin > 0) {
         KernelTimer kt("prefill.scan_local", s);
-        if (bf) hipLaunchKernelGGL(scan_local_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
-        else hipLaunchKernelGGL(scan_local_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a, nwin, wflags);
+        if (bf && cw == 4) hipLaunchKernelGGL((scan_local_kernel<bf16, 4>), grid, block, 0, s, a, nwin, wflags);
+        else if (bf) hipLaunchKernelGGL((scan_local_kernel<bf16, 1>), grid, block, 0, s, a, nwin, wflags);
+        else if (cw == 4) hipLaunchKernelGGL((scan_local_kernel<float, 4>), grid, block, 0, s, a, nwin, wflags);
+        else hipLaunchKernelGGL((scan_local_kernel<float, 1>), grid, block, 0, s, a, nwin, wflags);
     }
     {
         KernelTimer kt("prefill.scan_link", s);
@@ -320,8 +413,10 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
     }
     if (nwin > 0) {
         KernelTimer kt("prefill.scan_main", s);
-        if (bf) hipLaunchKernelGGL(scan_main_kernel<bf16>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
-        else hipLaunchKernelGGL(scan_main_kernel<float>, dim3(nwin * cblocks), dim3(kWave), 0, s, a);
+        if (bf && cw == 4) hipLaunchKernelGGL((scan_main_kernel<bf16, 4>), grid, block, 0, s, a);
+        else if (bf) hipLaunchKernelGGL((scan_main_kernel<bf16, 1>), grid, block, 0, s, a);
+        else if (cw == 4) hipLaunchKernelGGL((scan_main_kernel<float, 4>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((scan_main_kernel<float, 1>), grid, block, 0, s, a);
     }
     return hipGetLastError();
 }

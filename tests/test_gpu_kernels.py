@@ -169,10 +169,12 @@ def _scan_inputs(rng, T, E, R, act, stress=False):
 
 
 @pytest.mark.parametrize("act", ["f32", "bf16"])
-@pytest.mark.parametrize("lens", [[70, 1, 0, 33, 100, 31, 65], [300], [1, 2, 3, 31, 32, 33, 64, 65, 0, 5]])
-def test_selective_scan(B, act, lens):
-    rng = np.random.default_rng(sum(lens) + len(lens))
-    shape = synth.LayerShape(64, 128, 16, 16, 4, 1, act)
+@pytest.mark.parametrize("E", [128, 512])
+@pytest.mark.parametrize("lens", [[70, 1, 0, 33, 100, 31, 65], [300], [1, 2, 3, 31, 32, 33, 64, 65, 0, 5],
+                                  [7, 0, 0, 9, 1]])
+def test_selective_scan(B, act, E, lens):
+    rng = np.random.default_rng(sum(lens) + len(lens) + E)
+    shape = synth.LayerShape(64, E, 16, 16, 4, 1, act)
     E, N, R = shape.d_shard, 16, 16
     S = len(lens) + 3
     cu, slots, hi = _meta_case(rng, lens, S)
