@@ -52,6 +52,12 @@ def algorithmic(name, sh, T, Bd, nseq):
         "prefill.conv_history": ("hbm", 2 * nseq * E * (K - 1) * s),
         "prefill.scan_main": ("hbm", 4 * T * E * s + T * 2 * N * 4 + nseq * E * N * 4 + E * (N + 2) * 4),
         "decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
+        # in_proj with the conv window fused: weights, x_t, u and z out, history read + write
+        "decode.in_proj_conv": ("hbm", 2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
+                                + E * (K + 1) * s),
+        # dt_proj with the state step fused: weights, delta, B and C, u and z, g, state read + write
+        "decode.dt_proj_state": ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4
+                                 + E * (N + 2) * 4),
         "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
         "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
         "decode.dt_proj": ("hbm", E * R * s + M * R * 4 + M * E * s),

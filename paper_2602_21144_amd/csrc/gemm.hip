@@ -178,6 +178,223 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
     }
 }
 
+// bf16 operands, K a multiple of BK: tiles move global -> LDS on the DMA path
+// (global_load_lds_dwordx4: each lane writes 16 bytes at its lane slot of a 1 KB LDS
+// block), so there are no staging registers and no ds_write instructions. A lane picks
+// the global chunk that belongs at its slot under the XOR swizzle. The LDS holds a ring
+// of NS stages: tile k+NS-1 is in flight while tile k is multiplied, which covers
+// NS-1 tiles of MFMA time of memory latency. The DMA is issued from inline assembly
+// (M0 = LDS destination) and its completion is awaited by explicit vmcnt waits, so the
+// compiler does not serialise the prefetch behind each tile's LDS reads. Rows past M
+// or N are clamped to a valid row (their results are never stored). Fragments of
+// k-substep s+1 are read from LDS while the MFMAs of substep s run.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// wait until at most n of this wave's vector-memory loads are outstanding (n < 64).
+// GFX9 s_waitcnt immediate: vmcnt in bits [3:0] and [15:14]; expcnt [6:4] and
+// lgkmcnt [11:8] at their maxima (no wait on them).
+template <int n> __device__ __forceinline__ void wait_vm() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// chunk permutation of an LDS row: 16 lanes reading one chunk column of 16 consecutive
+// rows hit distinct 16-byte bank groups (128-byte rows: key (r>>1)&7; 64-byte: (r>>2)&3)
+template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
+    if constexpr (BK == 64) return chunk ^ ((row >> 1) & 7);
+    else return chunk ^ ((row >> 2) & 3);
+}
+
+// WM x WN waves; with 8 waves two share each SIMD, so one wave's barrier and LDS waits
+// are covered by the other's MFMAs.
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
+                                                              int64_t lda, const bf16* __restrict__ B, int64_t ldb,
+                                                              void* __restrict__ Cp, int64_t ldc, int tiles_m,
+                                                              int tiles_n) {
+    constexpr int NW = WM * WN;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int CPR = BK / 8;             // 16-byte chunks per row
+    constexpr int RPB = 64 / CPR;           // rows per 1 KB DMA block
+    constexpr int AG = BM / RPB / NW, BG = BN / RPB / NW;  // DMA blocks per wave per stage
+    constexpr int OPS = AG + BG;
+    constexpr int SUB = BK / 16;            // MFMA k-substeps per stage
+    static_assert(AG >= 1 && BG >= 1 && NS >= 2, "tile");
+    static_assert(SUB % 2 == 0, "fragment sets alternate within a tile");
+    __shared__ __attribute__((aligned(1024))) bf16 As[NS][BM * BK];
+    __shared__ __attribute__((aligned(1024))) bf16 Bs[NS][BN * BK];
+
+    int tm, tn;
+    tile_of(tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    const int lr = lane / CPR, lp = lane % CPR;
+    const bf16* asrc[AG];
+    const bf16* bsrc[BG];
+#pragma unroll
+    for (int q = 0; q < AG; ++q) {
+        const int r = (wave * AG + q) * RPB + lr;
+        asrc[q] = A + (int64_t)min(m0 + r, M - 1) * lda + swz_k<BK>(r, lp) * 8;
+    }
+#pragma unroll
+    for (int q = 0; q < BG; ++q) {
+        const int r = (wave * BG + q) * RPB + lr;
+        bsrc[q] = B + (int64_t)min(n0 + r, N - 1) * ldb + swz_k<BK>(r, lp) * 8;
+    }
+    const uint32_t a_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&As[0][0];
+    const uint32_t b_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&Bs[0][0];
+    auto dma = [&](int kt, int stage) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int q = 0; q < AG; ++q)
+            dma16(asrc[q] + k0, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + q) * RPB) * BK * 2)));
+#pragma unroll
+        for (int q = 0; q < BG; ++q)
+            dma16(bsrc[q] + k0, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + q) * RPB) * BK * 2)));
+    };
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+    int arow[TM], brow[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * 32 + (lane & 31);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * 32 + (lane & 31);
+
+    const int nk = K / BK;
+    bf16x8 fa[2][TM], fb[2][TN];
+    auto frag = [&](int stage, int s, int set) {
+        const bf16* as = As[stage];
+        const bf16* bs = Bs[stage];
+        const int c = s * 2 + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[set][i] = *(const bf16x8*)&as[arow[i] * BK + swz_k<BK>(arow[i], c) * 8];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[set][j] = *(const bf16x8*)&bs[brow[j] * BK + swz_k<BK>(brow[j], c) * 8];
+    };
+    auto mfma = [&](int set) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+    };
+    // one MFMA per fragment read, then the remaining MFMAs of the substep
+    auto interleave = [&]() {
+#pragma unroll
+        for (int q = 0; q < TM + TN; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        if (TM * TN > TM + TN) __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
+    };
+
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st)
+        if (st < nk) dma(st, st);
+    wait_vm<(NS - 2) * OPS>();
+    __syncthreads();
+    frag(0, 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt % NS;
+        if (kt + NS - 1 < nk) dma(kt + NS - 1, (kt + NS - 1) % NS);
+        // substeps 0 .. SUB-2, each reading the fragments of the next
+#pragma unroll
+        for (int s = 0; s + 1 < SUB; ++s) {
+            frag(cur, s + 1, (s + 1) & 1);
+            mfma(s & 1);
+            interleave();
+        }
+        // Tile kt+1 must be complete in LDS (this wave's DMA, then all waves'), and this
+        // wave's reads of stage cur must be done before anyone refills it. The barrier
+        // sits before the last substep so its MFMAs cover the first reads of tile kt+1.
+        if (kt + 1 < nk) {
+            const int newer = min(NS - 2, nk - 2 - kt);  // tiles newer than kt+1 in flight
+            if (newer >= NS - 2) wait_vm<(NS - 2) * OPS>();
+            else wait_vm<0>();  // tail: wait for everything
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments of the last substep are in
+        __syncthreads();
+        if (kt + 1 < nk) frag((kt + 1) % NS, 0, SUB & 1);
+        mfma((SUB - 1) & 1);
+        interleave();
+    }
+
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WTM + i * 32 + (lane & 31);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = n0 + wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+                const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
+                const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+                if constexpr (C_F32) {
+                    float* p = (float*)Cp + (int64_t)m * ldc + n;
+                    if (n + 3 < N) {
+                        *(float4*)p = make_float4(v0, v1, v2, v3);
+                    } else {
+                        if (n < N) p[0] = v0;
+                        if (n + 1 < N) p[1] = v1;
+                        if (n + 2 < N) p[2] = v2;
+                    }
+                } else {
+                    bf16* p = (bf16*)Cp + (int64_t)m * ldc + n;
+                    if (n + 3 < N) {
+                        bf16x4 o;
+                        o[0] = (bf16)v0; o[1] = (bf16)v1; o[2] = (bf16)v2; o[3] = (bf16)v3;
+                        *(bf16x4*)p = o;
+                    } else {
+                        if (n < N) p[0] = (bf16)v0;
+                        if (n + 1 < N) p[1] = (bf16)v1;
+                        if (n + 2 < N) p[2] = (bf16)v2;
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF>
+hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
+                   int64_t ldc, hipStream_t s) {
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    hipLaunchKernelGGL((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
+                       (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
+    return hipGetLastError();
+}
+
+// Tile shape by a wave-quantisation cost model: whole rounds of 256 workgroups (one per
+// CU) times tile area over the shape's measured efficiency (256x256 does the most MFMA
+// work per LDS byte; 128x128 gives more workgroups when the grid is small).
+template <int ROLE, bool CF>
+hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+                        void* C, int64_t ldc, hipStream_t s) {
+    auto cost = [&](int bm, int bn, double eff) {
+        const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+        return (double)((tiles + 255) / 256) * bm * bn / eff;
+    };
+    if (K % 64 == 0 && cost(256, 256, 1.0) <= cost(128, 128, 0.83))
+        return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (K % 64 == 0) return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return run_dma<ROLE, 128, 128, 32, 4, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+}
+
 // fp32 operands on v_mfma_f32_16x16x4_f32: 64x64 tiles, k 16 per stage, four waves of 32x32.
 constexpr int kFBK = 16;
 constexpr int kFPad = kFBK + 1;
@@ -274,8 +491,12 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
         p.M = (int)M; p.N = (int)N; p.K = (int)K;
         return launch_gemm_skinny(p, CF ? kSkinnyStoreF32 : kSkinnyStoreBf16, s);
     }
+    if constexpr (!AF) {
+        if (K % 32 == 0) return dispatch_dma<ROLE, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    }
+    // staged path: fp32 A (rounded while staging) or a K tail; short K favours more tiles
     const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-    if (big_tiles >= 512) return run_bf16<ROLE, 256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (big_tiles >= 512 && K > 256) return run_bf16<ROLE, 256, 256, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     return run_bf16<ROLE, 128, 128, 2, 2, AF, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
