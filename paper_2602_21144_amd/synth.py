@@ -151,8 +151,8 @@ def make_general_layer(shape: LayerShape, seed: int) -> Dict[str, np.ndarray]:
 
 
 def make_tokens(rng: np.random.Generator, n: int, d_model: int, act: str) -> np.ndarray:
-    """``n`` token activations x ~ N(0, 1), stored in the act dtype (float32 array)."""
-    return _store(rng.normal(0.0, 1.0, size=(n, d_model)).astype(np.float32), act)
+    """``n`` token activations x ~ N(0, 1), drawn as float32 and stored in the act dtype."""
+    return _store(rng.standard_normal(size=(n, d_model), dtype=np.float32), act)
 
 
 def make_slots(rng: np.random.Generator, nseq: int, spare: int = 16) -> np.ndarray:

@@ -141,27 +141,35 @@ def host(t):
 def oracle_tp_sequence(full64: dict, shape: synth.LayerShape, x_seq, decode_x=None, ranks=(0,)):
     """Oracle of one sequence through all shards (fresh state): prefill, then decode steps.
 
-    Returns dict rank -> {"y": [L, dm], "conv": [E, K-1], "ssm": [E, N], "dec_y": [steps, dm]}.
+    Stage 1 runs on every shard (their x_proj partials are summed, the first reduction);
+    stage 2 only on the ranks asked for. Returns rank -> {"y": [L, dm], "conv": [E, K-1],
+    "ssm": [E, N], "dec_y": [steps, dm]}.
     """
     from oracle import mixer as om
     P = shape.shard_count
     shards = [om.shard_weights(full64, r, P) for r in range(P)]
     E, N, K = shape.d_shard, shape.d_state, shape.d_conv
     L = x_seq.shape[0]
-    cps = [np.zeros((1, E, K - 1)) for _ in range(P)]
-    sps = [np.zeros((1, E, N)) for _ in range(P)]
-    s1, s2, _ = om.tp_prefill(shards, np.asarray(x_seq, np.float64), [0, L], [0], [0], cps, sps, shape.act)
-    out = {r: {"y": s2[r]["y"], "conv": s1[r]["conv_pool"][0], "ssm": s2[r]["ssm_pool"][0], "dec_y": []}
-           for r in ranks}
+    x64 = np.asarray(x_seq, np.float64)
+    cu, sl, hi = [0, L], [0], [0]
+    s1 = [om.prefill_stage1(w, x64, cu, sl, hi, np.zeros((1, E, K - 1)), shape.act) for w in shards]
+    red = np.sum([s["x_dbl"] for s in s1], axis=0)
+    out, sps = {}, {}
+    for r in ranks:
+        s2 = om.prefill_stage2(shards[r], s1[r], red, cu, sl, hi, np.zeros((1, E, N)), shape.act)
+        out[r] = {"y": s2["y"], "conv": s1[r]["conv_pool"][0], "ssm": s2["ssm_pool"][0], "dec_y": []}
+        sps[r] = s2["ssm_pool"]
     cps = [s["conv_pool"] for s in s1]
-    sps = [s["ssm_pool"] for s in s2]
     if decode_x is not None:
         for t in range(decode_x.shape[0]):
-            d1, d2, _ = om.tp_decode_step(shards, np.asarray(decode_x[t:t + 1], np.float64), [0], cps, sps, shape.act)
+            xt = np.asarray(decode_x[t:t + 1], np.float64)
+            d1 = [om.decode_stage1(w, xt, [0], cp, shape.act) for w, cp in zip(shards, cps)]
+            dred = np.sum([d["x_dbl"] for d in d1], axis=0)
             cps = [d["conv_pool"] for d in d1]
-            sps = [d["ssm_pool"] for d in d2]
             for r in ranks:
-                out[r]["dec_y"].append(d2[r]["y"][0])
+                d2 = om.decode_stage2(shards[r], d1[r], dred, [0], sps[r], shape.act)
+                sps[r] = d2["ssm_pool"]
+                out[r]["dec_y"].append(d2["y"][0])
         for r in ranks:
             out[r]["dec_y"] = np.array(out[r]["dec_y"])
             out[r]["conv"] = cps[r][0]
