@@ -283,12 +283,23 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
+                         "to scale hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported (this build runs on one GPU)",
               file=sys.stderr)
         sys.exit(2)
     result, ctx = run(args)
+    if args.copy_calibration:
+        import torch
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copied 1 GiB for counter calibration")
     if not args.no_cpu_baseline:
         log("CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(ctx)

@@ -226,7 +226,7 @@ int ssm_decode_ssm(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, c
  * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
  * the library launches from the calling thread is bracketed by two HIP events on the
  * launch stream (the events add a few microseconds of device time per launch; leave
- * timing off in production). */
+ * timing off in production). Launches on a stream under graph capture are not timed. */
 typedef struct ssm_kernel_time {
     char name[48];       /* kernel role, e.g. "prefill.in_proj", "decode.state_update" */
     int64_t launches;    /* launches recorded since the last collection */

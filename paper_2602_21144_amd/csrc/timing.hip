@@ -37,6 +37,12 @@ hipEvent_t take_event() {
 KernelTimer::KernelTimer(const char* name, hipStream_t s) : name_(name), s_(s), a_(nullptr) {
     if (!g_on) return;
     if (!g_only.empty() && g_only != name) return;
+    // no timing inside graph capture: event records there are not timestamps
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s_, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+        (void)hipGetLastError();
+        return;
+    }
     a_ = take_event();
     if (a_ && hipEventRecord(a_, s_) != hipSuccess) {
         g_pool.push_back(a_);
