@@ -12,8 +12,9 @@ region because it is the other GPU's work, added by the library's reduce kernel)
 stage 2 (dt_proj, selective scan, out_proj); the same for every decode step.
 
 Prints one JSON line: prefill tokens/s (value), decode us/step, ms per step, a roofline
-entry for the kernel that takes the most time in a step (its duration measured with HIP
-events on the launch stream during the timed region), a per-kernel breakdown from one
+entry for the kernel that takes the most time in a step (its duration measured during the
+timed region by HIP events bound to each of its dispatches on the launch stream, its HBM
+traffic from the committed rocprofv3 counter summary), a per-kernel breakdown from one
 extra profiled step, and the CPU oracle timed on a bounded sample on the host.
 """
 from __future__ import annotations
@@ -70,6 +71,41 @@ def algorithmic(name, sh, T, Bd, nseq):
     if name == "exchange.reduce_add":
         return "hbm", None, "GB/s"
     return "hbm", None, "GB/s"
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mamba2.8b_shard0of2_b8x2048_dec128.traffic.txt")
+ROLE_SOURCE = {"prefill.in_proj": "gemm.hip", "prefill.out_proj": "gemm.hip", "prefill.x_proj": "gemm.hip",
+               "prefill.dt_proj": "gemm.hip", "prefill.conv1d": "conv.hip", "prefill.conv_history": "conv.hip",
+               "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip", "prefill.scan_main": "scan.hip",
+               "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip", "decode.dt_proj_state": "skinny.hip",
+               "decode.out_proj": "skinny.hip", "exchange.reduce_add": "misc.hip"}
+
+
+def source_sha(src):
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("common.h", src):
+        with open(os.path.join(ROOT, "paper_2602_21144_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(role):
+    """HBM bytes per launch of a kernel role from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary (already scaled by the copy calibration), or None when there is
+    no entry or the kernel's source has changed since the counters were taken."""
+    src = ROLE_SOURCE.get(role)
+    if src is None or not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            parts = line.split()
+            if line.startswith("#") or len(parts) < 5 or parts[0] != role:
+                continue
+            if parts[4] != source_sha(src):
+                return None
+            return {"fetch": float(parts[2]), "write": float(parts[3])}
+    return None
 
 
 def achieved(roof, amount, avg_ms):
@@ -207,8 +243,11 @@ def run(args):
     dom_avg = dom_ms / dom_launches
     ach = achieved(roof, amt, dom_avg)
     peak = PEAK_BF16_TFLOPS if roof == "mfma" else PEAK_HBM_GBS
+    tr = measured_traffic(dominant)
     roofline = {"kernel": dominant, "bound": roof, "achieved": None if ach is None else round(ach, 2), "peak": peak,
-                "unit": unit, "frac": None if ach is None else round(ach / peak, 4), "traffic": None,
+                "unit": unit, "frac": None if ach is None else round(ach / peak, 4),
+                "traffic": None if tr is None else round(tr["fetch"] + tr["write"]),
+                "traffic_fetch_write": None if tr is None else [round(tr["fetch"]), round(tr["write"])],
                 "avg_us": round(1e3 * dom_avg, 3), "launches_timed": dom_launches,
                 "algorithmic_per_launch": amt}
 

@@ -224,13 +224,15 @@ int ssm_decode_ssm(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, c
 
 /* ------------------------------------------------------------ measurement
  * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
- * the library launches from the calling thread is bracketed by two HIP events on the
- * launch stream (the events add a few microseconds of device time per launch; leave
- * timing off in production). Launches on a stream under graph capture are not timed. */
+ * the library launches from the calling thread is launched with hipExtLaunchKernel and
+ * a start/stop event pair that takes that dispatch's own begin and end timestamps, so a
+ * kernel's time excludes any wait in the queue before it. Leave timing off in
+ * production (each timed launch takes two events). Launches on a stream under graph
+ * capture are not timed. */
 typedef struct ssm_kernel_time {
     char name[48];       /* kernel role, e.g. "prefill.in_proj", "decode.state_update" */
     int64_t launches;    /* launches recorded since the last collection */
-    double total_ms;     /* summed event-to-event device time */
+    double total_ms;     /* summed kernel execution time, begin to end of each dispatch */
 } ssm_kernel_time_t;
 /* on: 1 to record, 0 to stop. only: NULL to time every kernel, else the one kernel
  * name to time (keeps the event overhead off the other launches). */

@@ -1,5 +1,6 @@
 // Internal declarations shared by the gfx950 kernels and the C-ABI layer.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -100,7 +101,9 @@ size_t scan_scratch_bytes(int64_t max_T, int E, int max_seqs);
 hipError_t launch_scan_prefill(const ScanArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_decode_ssm(const ScanArgs& a, bool bf16_act, hipStream_t s);
 
-// Brackets the launches made while it is alive with timing events (when timing is on).
+// Names the launches made while it is alive; when timing is on (and the stream is not
+// being captured into a graph), each of those launches is timed by the kernel's own
+// dispatch timestamps (see launch_timed_events).
 class KernelTimer {
   public:
     KernelTimer(const char* name, hipStream_t s);
@@ -109,10 +112,23 @@ class KernelTimer {
     KernelTimer& operator=(const KernelTimer&) = delete;
 
   private:
-    const char* name_;
-    hipStream_t s_;
-    hipEvent_t a_;
+    const char* prev_;
 };
+
+// For a launch under an active KernelTimer: hands out a start/stop event pair that
+// hipExtLaunchKernel binds to the dispatch itself (begin and end of the kernel, not of
+// the queue position), and records it under the timer's name. False when not timing.
+bool launch_timed_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Every kernel of the library is launched through this macro.
+#define SSM_LAUNCH(K, grid, block, shm, s, ...)                                             \
+    do {                                                                                    \
+        hipEvent_t e0_, e1_;                                                                \
+        if (::ssm::launch_timed_events(&e0_, &e1_))                                         \
+            hipExtLaunchKernelGGL(K, grid, block, shm, s, e0_, e1_, 0, __VA_ARGS__);        \
+        else                                                                                \
+            hipLaunchKernelGGL(K, grid, block, shm, s, __VA_ARGS__);                        \
+    } while (0)
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);  // bytes: multiple of 4
 hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_t s);

@@ -213,10 +213,10 @@ __global__ __launch_bounds__(256) void conv_decode_kernel(ConvArgs a) {
         if ((threads) <= 0) return hipSuccess;                                                \
         const dim3 grid_((unsigned)(((threads) + 255) / 256)), block_(256);                  \
         switch ((a).K) {                                                                      \
-            case 1: hipLaunchKernelGGL((KERN<T, 1>), grid_, block_, 0, s, a); break;         \
-            case 2: hipLaunchKernelGGL((KERN<T, 2>), grid_, block_, 0, s, a); break;         \
-            case 3: hipLaunchKernelGGL((KERN<T, 3>), grid_, block_, 0, s, a); break;         \
-            default: hipLaunchKernelGGL((KERN<T, 4>), grid_, block_, 0, s, a); break;        \
+            case 1: SSM_LAUNCH((KERN<T, 1>), grid_, block_, 0, s, a); break;         \
+            case 2: SSM_LAUNCH((KERN<T, 2>), grid_, block_, 0, s, a); break;         \
+            case 3: SSM_LAUNCH((KERN<T, 3>), grid_, block_, 0, s, a); break;         \
+            default: SSM_LAUNCH((KERN<T, 4>), grid_, block_, 0, s, a); break;        \
         }                                                                                     \
         return hipGetLastError();                                                             \
     } while (0)

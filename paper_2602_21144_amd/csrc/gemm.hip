@@ -374,7 +374,7 @@ template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF>
 hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                    int64_t ldc, hipStream_t s) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
                        (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
     return hipGetLastError();
 }
@@ -475,7 +475,7 @@ template <int ROLE, int BM, int BN, int WM, int WN, bool AF, bool CF>
 hipError_t run_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                     void* C, int64_t ldc, hipStream_t s) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, AF, CF>), dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N,
+    SSM_LAUNCH((gemm_bf16_nt<ROLE, BM, BN, WM, WN, AF, CF>), dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N,
                        (int)K, A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
     return hipGetLastError();
 }
@@ -509,7 +509,7 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
 #define SSM_F32_CASE(R)                                                                                             \
     case R:                                                                                                         \
-        hipLaunchKernelGGL(gemm_f32_nt<R>, dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, \
+        SSM_LAUNCH(gemm_f32_nt<R>, dim3(tm * tn), dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, \
                            lda, (const float*)B, ldb, (float*)C, ldc, tm, tn);                                      \
         break;
         switch (role) {

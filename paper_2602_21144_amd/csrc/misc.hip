@@ -48,13 +48,13 @@ unsigned grid_for(int64_t items) { return (unsigned)std::max<int64_t>(1, std::mi
 
 hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(reduce_add_kernel, dim3(grid_for((n + 3) / 4)), dim3(256), 0, s, dst, src, n);
+    SSM_LAUNCH(reduce_add_kernel, dim3(grid_for((n + 3) / 4)), dim3(256), 0, s, dst, src, n);
     return hipGetLastError();
 }
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return hipSuccess;
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(bytes / 4)), dim3(256), 0, s, (uint32_t*)p, bytes / 4);
+    SSM_LAUNCH(fill_zero_kernel, dim3(grid_for(bytes / 4)), dim3(256), 0, s, (uint32_t*)p, bytes / 4);
     return hipGetLastError();
 }
 
@@ -64,10 +64,10 @@ hipError_t launch_copy_rows(void* dst, int64_t ld_dst, const void* src, int64_t 
     const bool a16 = ((uintptr_t)dst % 16 == 0) && ((uintptr_t)src % 16 == 0) && ld_dst % 16 == 0 &&
                      ld_src % 16 == 0 && row_bytes % 16 == 0;
     if (a16) {
-        hipLaunchKernelGGL(copy_rows16_kernel, dim3(grid_for(rows * row_bytes / 16)), dim3(256), 0, s, (char*)dst,
+        SSM_LAUNCH(copy_rows16_kernel, dim3(grid_for(rows * row_bytes / 16)), dim3(256), 0, s, (char*)dst,
                            ld_dst, (const char*)src, ld_src, rows, row_bytes / 16);
     } else {
-        hipLaunchKernelGGL(copy_rows1_kernel, dim3(grid_for(rows * row_bytes)), dim3(256), 0, s, (char*)dst, ld_dst,
+        SSM_LAUNCH(copy_rows1_kernel, dim3(grid_for(rows * row_bytes)), dim3(256), 0, s, (char*)dst, ld_dst,
                            (const char*)src, ld_src, rows, row_bytes);
     }
     return hipGetLastError();

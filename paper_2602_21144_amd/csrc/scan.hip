@@ -400,23 +400,23 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
     const dim3 grid((unsigned)(nwin * (a.E / (kWave * cw)))), block(kWave * cw);
     if (nwin > 0) {
         KernelTimer kt("prefill.scan_local", s);
-        if (bf && cw == 4) hipLaunchKernelGGL((scan_local_kernel<bf16, 4>), grid, block, 0, s, a, nwin, wflags);
-        else if (bf) hipLaunchKernelGGL((scan_local_kernel<bf16, 1>), grid, block, 0, s, a, nwin, wflags);
-        else if (cw == 4) hipLaunchKernelGGL((scan_local_kernel<float, 4>), grid, block, 0, s, a, nwin, wflags);
-        else hipLaunchKernelGGL((scan_local_kernel<float, 1>), grid, block, 0, s, a, nwin, wflags);
+        if (bf && cw == 4) SSM_LAUNCH((scan_local_kernel<bf16, 4>), grid, block, 0, s, a, nwin, wflags);
+        else if (bf) SSM_LAUNCH((scan_local_kernel<bf16, 1>), grid, block, 0, s, a, nwin, wflags);
+        else if (cw == 4) SSM_LAUNCH((scan_local_kernel<float, 4>), grid, block, 0, s, a, nwin, wflags);
+        else SSM_LAUNCH((scan_local_kernel<float, 1>), grid, block, 0, s, a, nwin, wflags);
     }
     {
         KernelTimer kt("prefill.scan_link", s);
         const int64_t lanes = (int64_t)a.E * kN;
-        hipLaunchKernelGGL(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
+        SSM_LAUNCH(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
                            (const int32_t*)wflags);
     }
     if (nwin > 0) {
         KernelTimer kt("prefill.scan_main", s);
-        if (bf && cw == 4) hipLaunchKernelGGL((scan_main_kernel<bf16, 4>), grid, block, 0, s, a);
-        else if (bf) hipLaunchKernelGGL((scan_main_kernel<bf16, 1>), grid, block, 0, s, a);
-        else if (cw == 4) hipLaunchKernelGGL((scan_main_kernel<float, 4>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((scan_main_kernel<float, 1>), grid, block, 0, s, a);
+        if (bf && cw == 4) SSM_LAUNCH((scan_main_kernel<bf16, 4>), grid, block, 0, s, a);
+        else if (bf) SSM_LAUNCH((scan_main_kernel<bf16, 1>), grid, block, 0, s, a);
+        else if (cw == 4) SSM_LAUNCH((scan_main_kernel<float, 4>), grid, block, 0, s, a);
+        else SSM_LAUNCH((scan_main_kernel<float, 1>), grid, block, 0, s, a);
     }
     return hipGetLastError();
 }
@@ -425,8 +425,8 @@ hipError_t launch_decode_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
     const int64_t lanes = (int64_t)a.nseq * a.E;
     if (lanes <= 0) return hipSuccess;
     const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
-    if (bf) hipLaunchKernelGGL(decode_ssm_kernel<bf16>, grid, block, 0, s, a);
-    else hipLaunchKernelGGL(decode_ssm_kernel<float>, grid, block, 0, s, a);
+    if (bf) SSM_LAUNCH(decode_ssm_kernel<bf16>, grid, block, 0, s, a);
+    else SSM_LAUNCH(decode_ssm_kernel<float>, grid, block, 0, s, a);
     return hipGetLastError();
 }
 

@@ -196,7 +196,7 @@ template <int MB, int NW, bool AF, int EPI>
 void launch_one(const SkinnyArgs& p, dim3 grid, hipStream_t s) {
     // k-steps per wave issued together: bounded by the VGPRs a wave may hold at NW waves
     constexpr int KU = MB <= 16 ? 8 : (MB <= 32 ? 6 : 4);
-    hipLaunchKernelGGL((gemm_skinny_kernel<MB, NW, KU, AF, EPI>), grid, dim3(NW * 64), 0, s, p);
+    SSM_LAUNCH((gemm_skinny_kernel<MB, NW, KU, AF, EPI>), grid, dim3(NW * 64), 0, s, p);
 }
 
 template <int MB, bool AF, int EPI>

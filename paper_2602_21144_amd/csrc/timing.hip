@@ -1,7 +1,8 @@
 // Per-kernel device timing for measurement runs: when enabled, each kernel the library
-// launches on the calling thread is bracketed by a pair of HIP events on its stream.
-// Events come from a pool that is reused across collections, so the launch path does
-// no event creation once the pool is warm.
+// launches on the calling thread gets a start/stop event pair bound to its own dispatch
+// (hipExtLaunchKernel), so the elapsed time is the kernel's execution alone, not the
+// time it waited in the queue. Events come from a pool that is reused across
+// collections, so the launch path creates no events once the pool is warm.
 #include <cstring>
 #include <string>
 #include <vector>
@@ -32,33 +33,37 @@ hipEvent_t take_event() {
     return e;
 }
 
+thread_local const char* g_cur = nullptr;  // name of the active timer, null when not timing
+
 }  // namespace
 
-KernelTimer::KernelTimer(const char* name, hipStream_t s) : name_(name), s_(s), a_(nullptr) {
+KernelTimer::KernelTimer(const char* name, hipStream_t s) : prev_(g_cur) {
+    g_cur = nullptr;
     if (!g_on) return;
     if (!g_only.empty() && g_only != name) return;
-    // no timing inside graph capture: event records there are not timestamps
+    // nothing is timed inside graph capture: captured launches carry no timestamps
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s_, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
         (void)hipGetLastError();
         return;
     }
-    a_ = take_event();
-    if (a_ && hipEventRecord(a_, s_) != hipSuccess) {
-        g_pool.push_back(a_);
-        a_ = nullptr;
-    }
+    g_cur = name;
 }
 
-KernelTimer::~KernelTimer() {
-    if (!a_) return;
-    hipEvent_t b = take_event();
-    if (!b || hipEventRecord(b, s_) != hipSuccess) {
-        g_pool.push_back(a_);
-        if (b) g_pool.push_back(b);
-        return;
+KernelTimer::~KernelTimer() { g_cur = prev_; }
+
+bool launch_timed_events(hipEvent_t* start, hipEvent_t* stop) {
+    if (!g_cur) return false;
+    hipEvent_t a = take_event();
+    hipEvent_t b = a ? take_event() : nullptr;
+    if (!b) {
+        if (a) g_pool.push_back(a);
+        return false;
     }
-    g_recs.push_back({name_, a_, b});
+    g_recs.push_back({g_cur, a, b});
+    *start = a;
+    *stop = b;
+    return true;
 }
 
 }  // namespace ssm
