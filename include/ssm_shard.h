@@ -129,7 +129,8 @@ int ssm_shard_check_meta_host(const int32_t* cu_seqlens, const int32_t* cache_sl
 int ssm_shard_prefill_workspace_bytes(const ssm_shard_desc_t* desc, int64_t max_tokens,
                                       int32_t max_seqs, size_t* bytes);
 int ssm_shard_decode_workspace_bytes(const ssm_shard_desc_t* desc, int32_t max_batch, size_t* bytes);
-/* Zero the workspace status word (call once after allocating a workspace). */
+/* Zero the workspace status word (call once after allocating a workspace). Calls that
+ * share a workspace must not overlap in time. */
 int ssm_shard_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 /* Synchronise the stream, read the status word into *status and clear it. */
 int ssm_shard_take_status(void* ws, size_t ws_bytes, int32_t* status, hipStream_t stream);

@@ -212,51 +212,113 @@ def _w(weights):
     return weights if isinstance(weights, Weights) else weights_struct(weights)
 
 
-def ssm_shard_prefill(desc, weights, x, meta: SeqMeta, conv_pool, ssm_pool, y_partial, ws, stream=None):
+# Each ABI call is marshalled by a _m_<name> function returning (ctypes arguments, objects
+# those arguments point into). The wrapper of the same name makes the call once; bind()
+# keeps the marshalled arguments for repeated calls with the same tensors.
+
+def _m_ssm_shard_prefill(desc, weights, x, meta: SeqMeta, conv_pool, ssm_pool, y_partial, ws, stream=None):
     w = _w(weights)
-    _check(lib().ssm_shard_prefill(ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c),
-                                   _ptr(conv_pool), _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _ptr(ws),
-                                   ws.numel(), _stream(stream)))
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c), _ptr(conv_pool),
+            _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w, meta)
+
+
+def _m_ssm_shard_prefill_stage1(desc, weights, x, meta: SeqMeta, conv_pool, x_dbl_partial, ws, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c), _ptr(conv_pool),
+            conv_pool.shape[0], _ptr(x_dbl_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w, meta)
+
+
+def _m_ssm_shard_prefill_stage2(desc, weights, x_dbl, meta: SeqMeta, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), meta.T, ctypes.byref(meta.c), _ptr(ssm_pool),
+            ssm_pool.shape[0], _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w, meta)
+
+
+def _m_ssm_shard_decode_step(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0], _ptr(cache_slot), _ptr(conv_pool),
+            _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w)
+
+
+def _m_ssm_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0], _ptr(cache_slot), _ptr(conv_pool),
+            conv_pool.shape[0], _ptr(x_dbl_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w)
+
+
+def _m_ssm_shard_decode_stage2(desc, weights, x_dbl, cache_slot, ssm_pool, y_partial, ws, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), x_dbl.shape[0], _ptr(cache_slot), _ptr(ssm_pool),
+            ssm_pool.shape[0], _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w)
+
+
+def _m_ssm_reduce_add_f32(dst, src, stream=None):
+    if dst.dtype != torch.float32 or src.dtype != torch.float32 or dst.numel() != src.numel():
+        raise ValueError("ssm_reduce_add_f32: two float32 tensors of equal size expected")
+    return (_ptr(dst), _ptr(src), dst.numel(), _stream(stream)), ()
+
+
+_MARSHAL = {name[3:]: fn for name, fn in list(globals().items()) if name.startswith("_m_ssm_")}
+
+
+def _call(name, *args, **kw):
+    a, _keep = _MARSHAL[name](*args, **kw)
+    _check(getattr(lib(), name)(*a))
+
+
+def ssm_shard_prefill(desc, weights, x, meta: SeqMeta, conv_pool, ssm_pool, y_partial, ws, stream=None):
+    _call("ssm_shard_prefill", desc, weights, x, meta, conv_pool, ssm_pool, y_partial, ws, stream)
 
 
 def ssm_shard_prefill_stage1(desc, weights, x, meta: SeqMeta, conv_pool, x_dbl_partial, ws, stream=None):
-    w = _w(weights)
-    _check(lib().ssm_shard_prefill_stage1(ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c),
-                                          _ptr(conv_pool), conv_pool.shape[0], _ptr(x_dbl_partial), _ptr(ws),
-                                          ws.numel(), _stream(stream)))
+    _call("ssm_shard_prefill_stage1", desc, weights, x, meta, conv_pool, x_dbl_partial, ws, stream)
 
 
 def ssm_shard_prefill_stage2(desc, weights, x_dbl, meta: SeqMeta, ssm_pool, y_partial, ws, stream=None):
-    w = _w(weights)
-    _check(lib().ssm_shard_prefill_stage2(ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), meta.T,
-                                          ctypes.byref(meta.c), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(y_partial),
-                                          _ptr(ws), ws.numel(), _stream(stream)))
+    _call("ssm_shard_prefill_stage2", desc, weights, x_dbl, meta, ssm_pool, y_partial, ws, stream)
 
 
 def ssm_shard_decode_step(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream=None):
-    w = _w(weights)
-    _check(lib().ssm_shard_decode_step(ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0],
-                                       _ptr(cache_slot), _ptr(conv_pool), _ptr(ssm_pool), conv_pool.shape[0],
-                                       _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)))
+    _call("ssm_shard_decode_step", desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream)
 
 
 def ssm_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream=None):
-    w = _w(weights)
-    _check(lib().ssm_shard_decode_stage1(ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0],
-                                         _ptr(cache_slot), _ptr(conv_pool), conv_pool.shape[0], _ptr(x_dbl_partial),
-                                         _ptr(ws), ws.numel(), _stream(stream)))
+    _call("ssm_shard_decode_stage1", desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream)
 
 
 def ssm_shard_decode_stage2(desc, weights, x_dbl, cache_slot, ssm_pool, y_partial, ws, stream=None):
-    w = _w(weights)
-    _check(lib().ssm_shard_decode_stage2(ctypes.byref(desc), ctypes.byref(w), _ptr(x_dbl), x_dbl.shape[0],
-                                         _ptr(cache_slot), _ptr(ssm_pool), ssm_pool.shape[0], _ptr(y_partial),
-                                         _ptr(ws), ws.numel(), _stream(stream)))
+    _call("ssm_shard_decode_stage2", desc, weights, x_dbl, cache_slot, ssm_pool, y_partial, ws, stream)
 
 
 def ssm_reduce_add_f32(dst, src, stream=None):
-    assert dst.dtype == torch.float32 and src.dtype == torch.float32 and dst.numel() == src.numel()
-    _check(lib().ssm_reduce_add_f32(_ptr(dst), _ptr(src), dst.numel(), _stream(stream)))
+    _call("ssm_reduce_add_f32", dst, src, stream)
+
+
+class BoundCall:
+    """One ABI call with its arguments marshalled once. Calling it issues the call again
+    with the same pointers, sizes and stream: the tensors must stay alive, unmoved and
+    of the same shape (the object keeps references to them)."""
+
+    __slots__ = ("_f", "_args", "_keep", "name")
+
+    def __init__(self, name, args, keep):
+        self.name = name
+        self._f = getattr(lib(), name)
+        self._args = args
+        self._keep = keep
+
+    def __call__(self):
+        rc = self._f(*self._args)
+        if rc != SSM_OK:
+            _check(rc)
+
+
+def bind(name: str, *args, **kw) -> BoundCall:
+    """bind("ssm_shard_decode_stage1", desc, weights, x_t, ...) -> a callable issuing that call.
+    Available for the prefill, decode and reduce entry points."""
+    a, keep = _MARSHAL[name](*args, **kw)
+    tensors = tuple(v for v in list(args) + list(kw.values()) if isinstance(v, torch.Tensor))
+    return BoundCall(name, a, keep + tensors)
 
 
 def _dt(t: torch.Tensor) -> int:

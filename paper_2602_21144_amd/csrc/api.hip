@@ -242,14 +242,14 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
             void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    if (adt == SSM_BF16) {
+    if (adt == SSM_BF16 && d->d_conv >= 2) {
         // in_proj with the conv window shift + SiLU fused into its epilogue; x_proj
         SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, nullptr, 0, B, 2 * E, dm);
         p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
         p.conv_w = w->conv_w; p.conv_b = w->conv_b; p.conv_pool = conv_pool; p.Kc = d->d_conv;
         p.u = L.u; p.z = L.xz + E * act_bytes(d); p.ld_z = 2 * E;
-        SSM_SKINNY("decode.in_proj_conv", s, p, kSkinnyConv);
         SkinnyArgs q = skinny(L.u, E, false, w->x_proj_w, E, xdbl, W, B, W, E);
+        SSM_SKINNY("decode.in_proj_conv", s, p, kSkinnyConv);
         SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
         return SSM_OK;
     }
@@ -271,8 +271,8 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
         p.u = L.u; p.z = L.xz + E * act_bytes(d); p.ld_z = 2 * E;
         p.xdbl = xdbl; p.ld_xdbl = W; p.R = (int)R; p.b_dt = w->dt_proj_b; p.A_log = w->A_log; p.D = w->D;
         p.pool = ssm_pool; p.g = L.g;
-        SSM_SKINNY("decode.dt_proj_state", s, p, kSkinnyState);
         SkinnyArgs q = skinny(L.g, E, false, w->out_proj_w, E, y, dm, B, dm, E);
+        SSM_SKINNY("decode.dt_proj_state", s, p, kSkinnyState);
         SSM_SKINNY("decode.out_proj", s, q, kSkinnyStoreBf16);
         return SSM_OK;
     }

@@ -18,50 +18,72 @@ namespace {
 
 enum Epi { kEpiStoreBf16 = 0, kEpiStoreF32 = 1, kEpiConv = 2, kEpiState = 3 };
 
-template <bool A_F32>
-__device__ __forceinline__ bf16x8 load_a(const void* A, int64_t lda, int row, int k) {
-    if constexpr (A_F32) {
-        const float* p = (const float*)A + (int64_t)row * lda + k;
-        const float4 x = *(const float4*)p, y = *(const float4*)(p + 4);
-        bf16x8 o;
-        o[0] = (bf16)x.x; o[1] = (bf16)x.y; o[2] = (bf16)x.z; o[3] = (bf16)x.w;
-        o[4] = (bf16)y.x; o[5] = (bf16)y.y; o[6] = (bf16)y.z; o[7] = (bf16)y.w;
-        return o;
-    } else {
-        return *(const bf16x8*)((const bf16*)A + (int64_t)row * lda + k);
+// An A fragment as loaded: 8 bf16, or 8 fp32 rounded to bf16 when it enters the MFMA.
+template <bool A_F32> struct ARaw {
+    u32x4 v;
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) { v = buffer_load16(r, off); }
+    __device__ __forceinline__ bf16x8 get() const { return __builtin_bit_cast(bf16x8, v); }
+};
+template <> struct ARaw<true> {
+    u32x4 v0, v1;
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+        v0 = buffer_load16(r, off);
+        v1 = buffer_load16(r, off == kOffOutOfRange ? off : off + 16);
     }
-}
+    __device__ __forceinline__ bf16x8 get() const {
+        const f32x4 x = __builtin_bit_cast(f32x4, v0), y = __builtin_bit_cast(f32x4, v1);
+        bf16x8 o;
+        o[0] = (bf16)x[0]; o[1] = (bf16)x[1]; o[2] = (bf16)x[2]; o[3] = (bf16)x[3];
+        o[4] = (bf16)y[0]; o[5] = (bf16)y[1]; o[6] = (bf16)y[2]; o[7] = (bf16)y[3];
+        return o;
+    }
+};
 
-// Epilogue operands of one output element, loaded before the K loop so that their
-// latency overlaps the weight stream.
+// Epilogue operands of one output element. load_slot() issues the cache-slot index
+// before the weight loads; load() issues the operands (some addressed by that slot)
+// right after them, so that the slot's latency, the weight stream and the operand
+// fetch overlap. Both are branch-free: every thread loads from in-range (clamped)
+// rows, slots and taps, and apply() decides what the values mean, so the compiler
+// keeps all of these loads in flight together.
 template <int EPI> struct EpiIn {
+    __device__ __forceinline__ void load_slot(const SkinnyArgs&, int) {}
     __device__ __forceinline__ void load(const SkinnyArgs&, int, int) {}
 };
 
+__device__ __forceinline__ bool slot_ok(int slot, int S) { return slot >= 0 && slot < S; }
+
 // in_proj: column n < E is channel n of the SSM path (conv window), n >= E the gate.
+// Needs 2 <= d_conv <= 4 (at least one cached tap).
 template <> struct EpiIn<kEpiConv> {
     int slot;
-    float w[kMaxConv], hv[kMaxConv - 1], bias;
-    __device__ __forceinline__ void load(const SkinnyArgs& p, int m, int n) {
-        slot = -1;
-        if (n >= p.E) return;
-        slot = p.slot[m];
-        if (slot < 0 || slot >= p.S) return;
+    float w[kMaxConv], hv[kMaxConv - 1], bias, wlast;  // wlast = w[K - 1], the current token's tap
+    __device__ __forceinline__ void load_slot(const SkinnyArgs& p, int m) { slot = p.slot[m]; }
+    __device__ __forceinline__ void load(const SkinnyArgs& p, int, int n) {
         const int K = p.Kc;
-        const bf16* hist = (const bf16*)p.conv_pool + ((int64_t)slot * p.E + n) * (K - 1);
-        const bf16* wr = (const bf16*)p.conv_w + (int64_t)n * K;
+        const int c = n < p.E ? n : 0;  // gate columns read channel 0 and ignore it
+        const int sc = slot_ok(slot, p.S) ? slot : 0;
+        const bf16* hist = (const bf16*)p.conv_pool + ((int64_t)sc * p.E + c) * (K - 1);
+        const bf16* wr = (const bf16*)p.conv_w + (int64_t)c * K;
 #pragma unroll
-        for (int j = 0; j < kMaxConv; ++j) w[j] = j < K ? (float)wr[j] : 0.0f;
+        for (int j = 0; j < kMaxConv; ++j) w[j] = (float)wr[j < K ? j : K - 1];
 #pragma unroll
-        for (int j = 0; j < kMaxConv - 1; ++j) hv[j] = j < K - 1 ? (float)hist[j] : 0.0f;
-        bias = (float)((const bf16*)p.conv_b)[n];
+        for (int j = 0; j < kMaxConv - 1; ++j) hv[j] = (float)hist[j < K - 1 ? j : K - 2];
+        bias = (float)((const bf16*)p.conv_b)[c];
+        wlast = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kMaxConv; ++j) {
+            if (j == K - 1) wlast = w[j];  // static indices only: the arrays stay in registers
+            w[j] = j < K ? w[j] : 0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxConv - 1; ++j) hv[j] = j < K - 1 ? hv[j] : 0.0f;
     }
     __device__ __forceinline__ void apply(const SkinnyArgs& p, int m, int n, float v) const {
         if (n >= p.E) {
             ((bf16*)p.z)[(int64_t)m * p.ld_z + (n - p.E)] = (bf16)v;
             return;
         }
-        if (slot < 0 || slot >= p.S) {
+        if (!slot_ok(slot, p.S)) {
             atomicOr(p.status, SSM_STATUS_BAD_SLOT);
             ((bf16*)p.u)[(int64_t)m * p.E + n] = (bf16)0.0f;
             return;
@@ -72,7 +94,7 @@ template <> struct EpiIn<kEpiConv> {
 #pragma unroll
         for (int j = 0; j < kMaxConv - 1; ++j)
             if (j < K - 1) acc += w[j] * hv[j];
-        acc += w[K - 1] * x;
+        acc += wlast * x;
         ((bf16*)p.u)[(int64_t)m * p.E + n] = (bf16)silu_f(acc);
         bf16* hist = (bf16*)p.conv_pool + ((int64_t)slot * p.E + n) * (K - 1);
 #pragma unroll
@@ -86,10 +108,10 @@ template <> struct EpiIn<kEpiConv> {
 template <> struct EpiIn<kEpiState> {
     int slot;
     float h[kN], a[kN], bc[2 * kN], u, z, bdt, Dn;
+    __device__ __forceinline__ void load_slot(const SkinnyArgs& p, int m) { slot = p.slot[m]; }
     __device__ __forceinline__ void load(const SkinnyArgs& p, int m, int n) {
-        slot = p.slot[m];
-        if (slot < 0 || slot >= p.S) return;
-        const float4* hp = (const float4*)(p.pool + ((int64_t)slot * p.E + n) * kN);
+        const int sc = slot_ok(slot, p.S) ? slot : 0;
+        const float4* hp = (const float4*)(p.pool + ((int64_t)sc * p.E + n) * kN);
         const float4* al = (const float4*)(p.A_log + (int64_t)n * kN);
         const float4* bt = (const float4*)(p.xdbl + (int64_t)m * p.ld_xdbl + p.R);
 #pragma unroll
@@ -109,7 +131,7 @@ template <> struct EpiIn<kEpiState> {
         Dn = p.D[n];
     }
     __device__ __forceinline__ void apply(const SkinnyArgs& p, int m, int n, float v) {
-        if (slot < 0 || slot >= p.S) {
+        if (!slot_ok(slot, p.S)) {
             atomicOr(p.status, SSM_STATUS_BAD_SLOT);
             ((bf16*)p.g)[(int64_t)m * p.E + n] = (bf16)0.0f;
             return;
@@ -132,8 +154,9 @@ template <> struct EpiIn<kEpiState> {
 };
 
 // NW waves split K; every thread owns at most one output element of the 16-column tile
-// (NW * 64 >= MB * 16), whose epilogue operands it fetches before the K loop. Each wave
-// issues the loads of up to KU k-steps (32 each) before its MFMAs.
+// (NW * 64 >= MB * 16). Each wave issues the loads of up to KU k-steps (32 each) before
+// its MFMAs; the first batch goes out right after the epilogue's slot index and before
+// the epilogue operands.
 template <int MB, int NW, int KU, bool A_F32, int EPI>
 __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(SkinnyArgs p) {
     static_assert(NW * 64 >= MB * 16, "one epilogue element per thread");
@@ -145,37 +168,55 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(SkinnyArgs p) {
     const int e = threadIdx.x;
     const int em = m0 + e / 16, en = n0 + (e & 15);
     const bool ework = e < MB * 16 && em < p.M && en < p.N;
+    const int emc = em < p.M ? em : p.M - 1, enc = en < p.N ? en : p.N - 1;  // in-range for the fetch
     EpiIn<EPI> ein;
-    if constexpr (EPI == kEpiConv || EPI == kEpiState) {
-        if (ework) ein.load(p, em, en);
-    }
+    ein.load_slot(p, emc);
 
     const int ksteps = (p.K + 31) / 32;
     const int per = (ksteps + NW - 1) / NW;
     const int s0 = wave * per, s1 = min(ksteps, s0 + per);
-    const int brow = n0 + (lane & 15);
     const int kl = (lane >> 4) * 8;
-    const bool bok = brow < p.N;
+    // the tile's weight rows and activation rows as buffer resources: rows past N or M
+    // lie outside them and read as zero, as do k-steps outside this wave's share
+    constexpr int asz = A_F32 ? 4 : 2;
+    const __amdgpu_buffer_rsrc_t rb =
+        buffer_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(min(16, p.N - n0) * p.ldb * 2));
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc((const char*)p.A + (int64_t)m0 * p.lda * asz,
+                                                  (uint32_t)(min(MB, p.M - m0) * p.lda * asz));
     f32x4 acc[MT];
 #pragma unroll
     for (int i = 0; i < MT; ++i) acc[i] = f32x4{};
-    for (int s = s0; s < s1; s += KU) {
-        bf16x8 bf[KU], af[KU][MT];
+    u32x4 bf[KU];
+    ARaw<A_F32> af[KU][MT];
+    auto load_batch = [&](int s) {
 #pragma unroll
         for (int u = 0; u < KU; ++u) {
             const int k = (s + u) * 32 + kl;
             const bool kok = (s + u < s1) && k < p.K;
-            bf[u] = (kok && bok) ? *(const bf16x8*)(p.B + (int64_t)brow * p.ldb + k) : bf16x8{};
+            bf[u] = buffer_load16(rb, kok ? (uint32_t)(((lane & 15) * p.ldb + k) * 2) : kOffOutOfRange);
 #pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const int arow = m0 + i * 16 + (lane & 15);
-                af[u][i] = (kok && arow < p.M) ? load_a<A_F32>(p.A, p.lda, arow, k) : bf16x8{};
-            }
+            for (int i = 0; i < MT; ++i)
+                af[u][i].load(ra, kok ? (uint32_t)(((i * 16 + (lane & 15)) * p.lda + k) * asz) : kOffOutOfRange);
         }
+    };
+    auto mma_batch = [&]() {
 #pragma unroll
         for (int u = 0; u < KU; ++u)
 #pragma unroll
-            for (int i = 0; i < MT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][i], bf[u], acc[i], 0, 0, 0);
+            for (int i = 0; i < MT; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][i].get(), __builtin_bit_cast(bf16x8, bf[u]),
+                                                                 acc[i], 0, 0, 0);
+    };
+    load_batch(s0);
+    // keep the order: weights in flight, then the slot-addressed epilogue fetch (which waits
+    // only for the slot index), then the MFMAs (which wait for the weights)
+    __builtin_amdgcn_sched_barrier(0);
+    ein.load(p, emc, enc);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_batch();
+    for (int s = s0 + KU; s < s1; s += KU) {
+        load_batch(s);
+        mma_batch();
     }
     // lane l holds column l % 16 and rows 4 (l / 16) + r of each 16-row tile
 #pragma unroll
@@ -192,25 +233,41 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(SkinnyArgs p) {
     else ein.apply(p, em, en, v);
 }
 
-template <int MB, int NW, bool AF, int EPI>
+template <int MB, int NW, int KU, bool AF, int EPI>
 void launch_one(const SkinnyArgs& p, dim3 grid, hipStream_t s) {
-    // k-steps per wave issued together: bounded by the VGPRs a wave may hold at NW waves
-    constexpr int KU = MB <= 16 ? 8 : (MB <= 32 ? 6 : 4);
     SSM_LAUNCH((gemm_skinny_kernel<MB, NW, KU, AF, EPI>), grid, dim3(NW * 64), 0, s, p);
+}
+
+// 16-row tiles: each wave issues all of its k-steps at once when they fit in registers
+template <int NW, bool AF, int EPI>
+void launch_ku16(const SkinnyArgs& p, dim3 grid, int per, hipStream_t s) {
+    if (per <= 2) launch_one<16, NW, 2, AF, EPI>(p, grid, s);
+    else if (per <= 4) launch_one<16, NW, 4, AF, EPI>(p, grid, s);
+    else if constexpr (AF) launch_one<16, NW, 8, AF, EPI>(p, grid, s);  // fp32 A takes twice the registers
+    else if (per <= 8) launch_one<16, NW, 8, AF, EPI>(p, grid, s);
+    else launch_one<16, NW, 12, AF, EPI>(p, grid, s);
 }
 
 template <int MB, bool AF, int EPI>
 hipError_t launch_mb(const SkinnyArgs& p, hipStream_t s) {
     const dim3 grid((unsigned)((p.N + 15) / 16), (unsigned)((p.M + MB - 1) / MB));
-    // enough waves that each streams at most 8 k-steps, and one thread per output element
-    // (the state epilogue keeps a state row per thread: at most 8 waves, 256 VGPRs each)
     const int ksteps = (p.K + 31) / 32;
-    constexpr int NWMIN = MB * 16 / 64;
-    constexpr int NWMAX = EPI == kEpiState ? 8 : 16;
-    const int want = (ksteps + 7) / 8;
-    if ((want > 8 || NWMIN > 8) && NWMAX >= 16) launch_one<MB, NWMAX, AF, EPI>(p, grid, s);
-    else if (want > 4 || NWMIN > 4) launch_one<MB, (NWMIN > 8 ? NWMAX : 8), AF, EPI>(p, grid, s);
-    else launch_one<MB, (NWMIN > 4 ? NWMAX : 4), AF, EPI>(p, grid, s);
+    if constexpr (MB == 16) {
+        // many tiles: 8 waves, so two workgroups share a CU and every tile starts in the first
+        // round; few tiles: 16 waves, so each wave's share of K stays short. (The state
+        // epilogue keeps a state row per thread: at most 8 waves.)
+        if constexpr (EPI == kEpiState) launch_ku16<8, AF, EPI>(p, grid, (ksteps + 7) / 8, s);
+        else if ((int64_t)grid.x * grid.y < 128) launch_ku16<16, AF, EPI>(p, grid, (ksteps + 15) / 16, s);
+        else launch_ku16<8, AF, EPI>(p, grid, (ksteps + 7) / 8, s);
+    } else {
+        // one thread per output element; enough waves that each streams at most 8 k-steps
+        constexpr int KU = (MB <= 32 ? 6 : 4) / (AF ? 2 : 1);
+        constexpr int NWMIN = MB * 16 / 64;
+        constexpr int NWMAX = EPI == kEpiState ? 8 : 16;
+        const int want = (ksteps + 7) / 8;
+        if ((want > 8 || NWMIN > 8) && NWMAX >= 16) launch_one<MB, NWMAX, KU, AF, EPI>(p, grid, s);
+        else launch_one<MB, (NWMIN > 8 ? NWMAX : 8), KU, AF, EPI>(p, grid, s);
+    }
     return hipGetLastError();
 }
 
@@ -237,3 +294,4 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s)
 }
 
 }  // namespace ssm
+
