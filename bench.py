@@ -48,7 +48,8 @@ def algorithmic(name, sh, T, Bd, nseq):
         "prefill.in_proj": ("mfma", 2.0 * T * 2 * E * dm),
         "prefill.out_proj": ("mfma", 2.0 * T * dm * E),
         "prefill.x_proj": ("hbm", T * E * s + W * E * s + T * W * 4),
-        "prefill.dt_proj": ("hbm", T * R * 4 + E * R * s + T * E * s),
+        "prefill.dt_round": ("hbm", T * R * 4 + T * R * 2),  # delta rounded to bf16 once
+        "prefill.dt_proj": ("hbm", T * R * s + E * R * s + T * E * s),
         "prefill.conv1d": ("hbm", 2 * T * E * s + E * (K + 1) * s),
         "prefill.conv_history": ("hbm", 2 * nseq * E * (K - 1) * s),
         "prefill.scan_main": ("hbm", 4 * T * E * s + T * 2 * N * 4 + nseq * E * N * 4 + E * (N + 2) * 4),
@@ -75,7 +76,7 @@ def algorithmic(name, sh, T, Bd, nseq):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mamba2.8b_shard0of2_b8x2048_dec128.traffic.txt")
 ROLE_SOURCE = {"prefill.in_proj": "gemm.hip", "prefill.out_proj": "gemm.hip", "prefill.x_proj": "gemm.hip",
-               "prefill.dt_proj": "gemm.hip", "prefill.conv1d": "conv.hip", "prefill.conv_history": "conv.hip",
+               "prefill.dt_proj": "gemm.hip", "prefill.dt_round": "gemm.hip", "prefill.conv1d": "conv.hip", "prefill.conv_history": "conv.hip",
                "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip", "prefill.scan_main": "scan.hip",
                "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip", "decode.dt_proj_state": "skinny.hip",
                "decode.out_proj": "skinny.hip", "exchange.reduce_add": "misc.hip"}

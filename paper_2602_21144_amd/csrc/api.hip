@@ -99,6 +99,7 @@ int check_meta(const ssm_seq_meta_t* m, int64_t T) {
 struct PrefillWs {
     int32_t* status;
     char *xz, *u, *dt, *g;
+    char* delta16;  // [T][R] bf16: delta rounded for dt_proj (bf16 activations)
     float* xdbl;
     char* scan;
     size_t total;
@@ -117,6 +118,7 @@ PrefillWs prefill_layout(const ssm_shard_desc_t* d, int64_t T, int nseq, void* b
     L.xdbl = (float*)take((size_t)T * W * 4);
     L.dt = take((size_t)T * E * s);
     L.g = take((size_t)T * E * s);
+    L.delta16 = take(d->act_dtype == SSM_BF16 ? (size_t)T * d->dt_rank * 2 : 0);
     L.scan = take(scan_scratch_bytes(T, (int)E, nseq));
     L.total = off;
     return L;
@@ -220,7 +222,13 @@ int prefill2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const floa
              const ssm_seq_meta_t* m, float* ssm_pool, int32_t S, void* y, const PrefillWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
-    SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
+    if (adt == SSM_BF16 && R % 32 == 0 && T > 64) {
+        // delta is rounded to bf16 once, so dt_proj runs on the DMA-fed bf16 tiles
+        SSM_TIMED("prefill.dt_round", s, launch_round_bf16_rows(xdbl, W, L.delta16, T, (int)R, s));
+        SSM_TRY(gemm(T, E, R, L.delta16, R, adt, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
+    } else {
+        SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
+    }
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, T, m->cu_seqlens, m->cache_slot, m->has_initial_state,
                             m->nseq, ssm_pool, S, L.g, L.status, L.scan);
     SSM_TRY_HIP(launch_scan_prefill(sa, adt == SSM_BF16, s), "selective scan");

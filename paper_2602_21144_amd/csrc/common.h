@@ -61,6 +61,8 @@ __host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_
 // GEMM: C[M][N] = A[M][K] * B[N][K]^T. Returns hipError_t of the launch. The role picks
 // the kernel instance (each projection has its own symbol in profiles).
 enum GemmRole { kGemmGeneric = 0, kGemmInProj = 1, kGemmXProj = 2, kGemmDtProj = 3, kGemmOutProj = 4 };
+// o [M][K] bf16 (dense) = a [M][K] fp32 (row stride lda) rounded to nearest even; K % 8 == 0
+hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t M, int K, hipStream_t s);
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt,
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
                           hipStream_t s, GemmRole role);

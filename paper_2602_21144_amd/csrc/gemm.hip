@@ -305,7 +305,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
 #pragma unroll
     for (int st = 0; st < NS - 1; ++st)
         if (st < nk) dma(st, st);
-    wait_vm<(NS - 2) * OPS>();
+    // tile 0 complete: NS-2 newer tiles may stay in flight, unless K has fewer tiles than that
+    if (nk >= NS - 1) wait_vm<(NS - 2) * OPS>();
+    else wait_vm<0>();
     __syncthreads();
     frag(0, 0, 0);
     for (int kt = 0; kt < nk; ++kt) {
@@ -480,6 +482,18 @@ hipError_t run_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
     return hipGetLastError();
 }
 
+// o[m][k] = bf16(a[m][k]) (round to nearest even), 8 values per thread; K % 8 == 0
+__global__ __launch_bounds__(256) void round_bf16_rows_kernel(const float* __restrict__ a, int64_t lda,
+                                                              bf16* __restrict__ o, int64_t M, int K) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int kg = K / 8;
+    if (i >= M * kg) return;
+    const int64_t m = i / kg;
+    const int k = (int)(i % kg) * 8;
+    const float* p = a + m * lda + k;
+    *(bf16x8*)(o + m * K + k) = cvt8(*(const float4*)p, *(const float4*)(p + 4));
+}
+
 template <int ROLE, bool AF, bool CF>
 hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                          void* C, int64_t ldc, hipStream_t s) {
@@ -491,6 +505,13 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
         p.M = (int)M; p.N = (int)N; p.K = (int)K;
         return launch_gemm_skinny(p, CF ? kSkinnyStoreF32 : kSkinnyStoreBf16, s);
     }
+    if constexpr (ROLE == kGemmXProj && !AF) {
+        // x_proj: few output columns (R + 2N), long K; one 64-row tile spans all of N so
+        // that every activation row is read once, with a 3-deep ring to cover the latency
+        // that four waves per CU leave exposed
+        if (K % 64 == 0 && N <= 192) return run_dma<ROLE, 64, 192, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (K % 64 == 0 && N <= 256) return run_dma<ROLE, 64, 256, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    }
     if constexpr (!AF) {
         if (K % 32 == 0) return dispatch_dma<ROLE, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     }
@@ -501,6 +522,13 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
 }
 
 }  // namespace
+
+hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t M, int K, hipStream_t s) {
+    const int64_t n8 = M * (K / 8);
+    if (n8 <= 0) return hipSuccess;
+    SSM_LAUNCH(round_bf16_rows_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, a, lda, (bf16*)o, M, K);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt, const void* B,
                           int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s, GemmRole role) {
@@ -533,6 +561,7 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
             break;
         case kGemmDtProj:
             if (af && !cf) return dispatch_bf16<kGemmDtProj, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            if (!af && !cf) return dispatch_bf16<kGemmDtProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
             break;
         case kGemmOutProj:
             if (!af && !cf) return dispatch_bf16<kGemmOutProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);

@@ -32,7 +32,7 @@ def _dev(a, dt):
 
 
 # ----------------------------------------------------------------------- GEMM
-GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (33, 200, 160), (64, 96, 224), (100, 300, 256), (257, 513, 64),
+GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 96, 224), (100, 300, 256), (257, 513, 64),
                (1000, 520, 768), (2048, 2048, 512), (300, 5120, 2560), (4089, 4091, 256), (200, 300, 96)]
 
 
