@@ -80,6 +80,7 @@ ROLE_SOURCE = {"prefill.in_proj": "gemm.hip", "prefill.out_proj": "gemm.hip", "p
                "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip", "prefill.scan_main": "scan.hip",
                "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip", "decode.dt_proj_state": "skinny.hip",
                "decode.out_proj": "skinny.hip", "exchange.reduce_add": "misc.hip"}
+ROLE_SOURCE.update({f"exchange.{op}_{c}": "codec.hip" for op in ("encode", "decode") for c in ("f16", "bf16", "fp8", "int8")})
 
 
 def source_sha(src):
@@ -281,7 +282,59 @@ def run(args):
         "roofline": roofline,
         "kernels": kernels,
     }
+    if not args.no_codec:
+        log("quantized exchange codecs on this workload's two exchange tensors (outside the timed region)")
+        xa = torch.empty(T, W, dtype=torch.float32, device=dev)
+        B.ssm_shard_prefill_stage1(desc[0], wst[0], x, meta, conv[0], xa, wsp[0])   # shard 0's x_proj partial
+        y1 = torch.empty(T, sh.d_model, dtype=act, device=dev)
+        ssm1 = torch.zeros(S, E, N, dtype=torch.float32, device=dev)
+        B.ssm_shard_prefill_stage2(desc[1], wst[1], p0, meta, ssm1, y1, wsp[1])      # shard 1's out_proj partial
+        result["codec"] = codec_figures(B, torch, {"x_dbl": [xa, p1_pref], "y_partial": [y, y1]})
     return result, (sh, full, x_host, xdec_host, slots, S)
+
+
+def codec_figures(B, torch, tensors):
+    """Section IV-D exchange codecs on real partials of the two exchange points: encode and
+    decode-accumulate device time (per-dispatch events), algorithmic GB/s, payload bytes,
+    and the largest error of the decoded sum relative to the largest exact sum entry."""
+    out = {}
+    for tname, parts in tensors.items():
+        rows, cols = parts[0].shape
+        src_b = parts[0].element_size()
+        exact = parts[0].float() + parts[1].float()
+        amax = float(exact.abs().max())
+        for codec in ("f16", "bf16", "fp8", "int8"):
+            pays = [B.exchange_payload(codec, rows, cols) for _ in parts]
+            acc = torch.empty(rows, cols, dtype=torch.float32, device=parts[0].device)
+
+            def once():
+                for r, t in enumerate(parts):
+                    B.ssm_exchange_encode(codec, t, pays[r])
+                for r in range(len(parts)):
+                    B.ssm_exchange_decode_accumulate(codec, pays[r], acc, accumulate=r > 0)
+            once()
+            torch.cuda.synchronize()
+            B.ssm_timing_collect()
+            B.ssm_timing_enable(True)
+            for _ in range(10):
+                once()
+            torch.cuda.synchronize()
+            B.ssm_timing_enable(False)
+            t = B.ssm_timing_collect()
+            enc = t[f"exchange.encode_{codec}"]
+            dec = t[f"exchange.decode_{codec}"]
+            pb = B.exchange_payload_bytes(codec, rows, cols)
+            enc_us, dec_us = 1e3 * enc[1] / enc[0], 1e3 * dec[1] / dec[0]
+            # algorithmic bytes: encode reads the partial and writes the payload; decode reads the
+            # payload and reads + writes the fp32 sum (the first rank's decode writes it only)
+            enc_b = rows * cols * src_b + pb
+            dec_b = pb + rows * cols * 4 * 1.5
+            out[f"{tname}.{codec}"] = {
+                "rows": rows, "cols": cols, "payload_bytes": pb, "raw_bytes": rows * cols * src_b,
+                "encode_us": round(enc_us, 3), "encode_GBps": round(enc_b / enc_us / 1e3, 1),
+                "decode_accumulate_us": round(dec_us, 3), "decode_accumulate_GBps": round(dec_b / dec_us / 1e3, 1),
+                "max_err_rel_to_max": float(f"{float((acc - exact).abs().max()) / max(amax, 1e-30):.3e}")}
+    return out
 
 
 def cpu_baseline(ctx):
@@ -335,6 +388,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
                          "to scale hardware byte counters)")

@@ -188,6 +188,32 @@ int ssm_shard_slice_weights(const ssm_shard_desc_t* desc, const ssm_shard_weight
 /* dst[i] += src[i] for i < n (float32): the x_proj exchange when all shards run on one GPU. */
 int ssm_reduce_add_f32(float* dst, const float* src, int64_t n, hipStream_t stream);
 
+/* --------------------------------------------------- quantized exchange
+ * Section IV-D: the two remaining AllReduces (the x_proj output, fp32, and the out_proj
+ * partial, act dtype) may carry a lower precision than the computation -- FP16 in the
+ * paper -- and are converted back for what follows. One exchange of P partials is an
+ * encode on every rank and, on the receiver, a decode of each payload added into an
+ * fp32 sum in rank order (an all-gather of payloads followed by a local reduction).
+ *   SSM_CODEC_F16, SSM_CODEC_BF16: element-wise rounding (ties to even), 2 bytes/value;
+ *     values beyond the half range become infinities, as IEEE conversion does.
+ *   SSM_CODEC_FP8_E4M3: OCP FP8 E4M3 of x * (448 / max|row|), 1 byte/value, one fp32
+ *     scale per row (amax / 448); SSM_CODEC_INT8: round-half-even of x * (127 / max|row|)
+ *     clamped to [-127, 127], one fp32 scale per row (amax / 127). A zero row has scale 0.
+ * Payload layout (device memory, caller-owned): scaled codecs first hold the [rows] fp32
+ * scales, padded to a multiple of 256 bytes, then the [rows][cols] codes, dense; the
+ * 2-byte codecs hold only the codes. Inputs must be finite. cols, ld_src and ld_acc are
+ * multiples of 8 and the pointers 16-byte aligned (else SSM_E_ALIGN); a payload smaller
+ * than the size query returns SSM_E_WORKSPACE. Stream-ordered, no allocation. */
+typedef enum ssm_codec { SSM_CODEC_F16 = 0, SSM_CODEC_BF16 = 1, SSM_CODEC_FP8_E4M3 = 2, SSM_CODEC_INT8 = 3 } ssm_codec_t;
+int ssm_exchange_payload_bytes(int32_t codec, int64_t rows, int64_t cols, size_t* bytes);
+/* payload <- encode(src), src [rows][cols] of src_dtype (ssm_dtype_t) with row stride ld_src */
+int ssm_exchange_encode(int32_t codec, const void* src, int32_t src_dtype, int64_t rows, int64_t cols,
+                        int64_t ld_src, void* payload, size_t payload_bytes, hipStream_t stream);
+/* acc [rows][cols] fp32 (row stride ld_acc) = decode(payload) (+ acc when accumulate != 0) */
+int ssm_exchange_decode_accumulate(int32_t codec, const void* payload, size_t payload_bytes, int64_t rows,
+                                   int64_t cols, float* acc, int64_t ld_acc, int32_t accumulate,
+                                   hipStream_t stream);
+
 /* ------------------------------------------------------- stage operators
  * The kernels the entry points above are built from, exposed for kernel-level checks.
  *

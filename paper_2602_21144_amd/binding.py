@@ -79,6 +79,9 @@ _SIGS = {
     "ssm_selective_scan": ([_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_decode_conv": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_decode_ssm": ([_P, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_exchange_payload_bytes": ([_I32, _I64, _I64, _P], _I32),
+    "ssm_exchange_encode": ([_I32, _P, _I32, _I64, _I64, _I64, _P, _SZ, _P], _I32),
+    "ssm_exchange_decode_accumulate": ([_I32, _P, _SZ, _I64, _I64, _P, _I64, _I32, _P], _I32),
     "ssm_timing_enable": ([_I32, ctypes.c_char_p], _I32),
     "ssm_timing_collect": ([_P, _I32, _P], _I32),
 }
@@ -319,6 +322,39 @@ def bind(name: str, *args, **kw) -> BoundCall:
     a, keep = _MARSHAL[name](*args, **kw)
     tensors = tuple(v for v in list(args) + list(kw.values()) if isinstance(v, torch.Tensor))
     return BoundCall(name, a, keep + tensors)
+
+
+SSM_CODEC = {"f16": 0, "bf16": 1, "fp8": 2, "int8": 3}
+
+
+def exchange_payload_bytes(codec: str, rows: int, cols: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_exchange_payload_bytes(SSM_CODEC[codec], rows, cols, ctypes.byref(n)))
+    return n.value
+
+
+def exchange_payload(codec: str, rows: int, cols: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(exchange_payload_bytes(codec, rows, cols), 16), dtype=torch.uint8, device=device)
+
+
+def ssm_exchange_encode(codec: str, src: torch.Tensor, payload: torch.Tensor, stream=None):
+    """payload <- encode(src); src is [rows][cols] float32 or bfloat16 with unit column stride."""
+    rows, cols = src.shape
+    if src.stride(1) != 1:
+        raise ValueError("unit column stride expected")
+    _check(lib().ssm_exchange_encode(SSM_CODEC[codec], ctypes.c_void_p(src.data_ptr()), _dt(src), rows, cols,
+                                     src.stride(0), _ptr(payload), payload.numel(), _stream(stream)))
+
+
+def ssm_exchange_decode_accumulate(codec: str, payload: torch.Tensor, acc: torch.Tensor, accumulate: bool,
+                                   stream=None):
+    """acc [rows][cols] float32 = decode(payload) (+ acc when accumulate)."""
+    rows, cols = acc.shape
+    if acc.dtype != torch.float32 or acc.stride(1) != 1:
+        raise ValueError("float32 accumulator with unit column stride expected")
+    _check(lib().ssm_exchange_decode_accumulate(SSM_CODEC[codec], _ptr(payload), payload.numel(), rows, cols,
+                                                ctypes.c_void_p(acc.data_ptr()), acc.stride(0),
+                                                1 if accumulate else 0, _stream(stream)))
 
 
 def _dt(t: torch.Tensor) -> int:

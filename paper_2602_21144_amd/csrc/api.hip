@@ -494,6 +494,57 @@ int ssm_reduce_add_f32(float* dst, const float* src, int64_t n, hipStream_t s) {
     return SSM_OK;
 }
 
+namespace {
+const char* const kCodecEncodeName[] = {"exchange.encode_f16", "exchange.encode_bf16", "exchange.encode_fp8",
+                                        "exchange.encode_int8"};
+const char* const kCodecDecodeName[] = {"exchange.decode_f16", "exchange.decode_bf16", "exchange.decode_fp8",
+                                        "exchange.decode_int8"};
+
+int check_codec_shape(int32_t codec, int64_t rows, int64_t cols) {
+    if (codec < SSM_CODEC_F16 || codec > SSM_CODEC_INT8) return fail(SSM_E_INVAL, "codec %d", codec);
+    if (rows < 0 || cols < 0) return fail(SSM_E_INVAL, "payload shape %lld x %lld", (long long)rows, (long long)cols);
+    if (cols % 8 != 0) return fail(SSM_E_ALIGN, "cols %lld is not a multiple of 8", (long long)cols);
+    return SSM_OK;
+}
+}  // namespace
+
+int ssm_exchange_payload_bytes(int32_t codec, int64_t rows, int64_t cols, size_t* bytes) {
+    SSM_TRY(check_codec_shape(codec, rows, cols));
+    if (!bytes) return fail(SSM_E_INVAL, "bytes is null");
+    *bytes = codec_payload_bytes(codec, rows, cols);
+    return SSM_OK;
+}
+
+int ssm_exchange_encode(int32_t codec, const void* src, int32_t src_dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                        void* payload, size_t payload_bytes, hipStream_t s) {
+    SSM_TRY(check_codec_shape(codec, rows, cols));
+    if (src_dtype != SSM_F32 && src_dtype != SSM_BF16) return fail(SSM_E_INVAL, "src_dtype %d", src_dtype);
+    if (rows == 0 || cols == 0) return SSM_OK;
+    if (ld_src < cols) return fail(SSM_E_INVAL, "ld_src %lld < cols %lld", (long long)ld_src, (long long)cols);
+    if (ld_src % 8 != 0) return fail(SSM_E_ALIGN, "ld_src %lld is not a multiple of 8", (long long)ld_src);
+    SSM_TRY(check_ptr(src, "src"));
+    SSM_TRY(check_ptr(payload, "payload"));
+    if (payload_bytes < codec_payload_bytes(codec, rows, cols))
+        return fail(SSM_E_WORKSPACE, "payload %zu bytes < %zu needed", payload_bytes, codec_payload_bytes(codec, rows, cols));
+    SSM_TIMED(kCodecEncodeName[codec], s, launch_codec_encode(codec, src, src_dtype == SSM_BF16, ld_src, rows, cols, payload, s));
+    return SSM_OK;
+}
+
+int ssm_exchange_decode_accumulate(int32_t codec, const void* payload, size_t payload_bytes, int64_t rows, int64_t cols,
+                                   float* acc, int64_t ld_acc, int32_t accumulate, hipStream_t s) {
+    SSM_TRY(check_codec_shape(codec, rows, cols));
+    if (rows == 0 || cols == 0) return SSM_OK;
+    if (ld_acc < cols) return fail(SSM_E_INVAL, "ld_acc %lld < cols %lld", (long long)ld_acc, (long long)cols);
+    if (ld_acc % 8 != 0) return fail(SSM_E_ALIGN, "ld_acc %lld is not a multiple of 8", (long long)ld_acc);
+    SSM_TRY(check_ptr(payload, "payload"));
+    SSM_TRY(check_ptr(acc, "acc"));
+    if (payload_bytes < codec_payload_bytes(codec, rows, cols))
+        return fail(SSM_E_WORKSPACE, "payload %zu bytes < %zu needed", payload_bytes, codec_payload_bytes(codec, rows, cols));
+    SSM_TIMED(kCodecDecodeName[codec], s,
+              launch_codec_decode_acc(codec, payload, rows, cols, acc, ld_acc, accumulate != 0, s));
+    return SSM_OK;
+}
+
 int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t adt, const void* B, int64_t ldb,
                 int32_t bdt, void* C, int64_t ldc, int32_t cdt, hipStream_t s) {
     if (M < 0 || N < 0 || K < 0 || M > INT32_MAX || N > INT32_MAX || K > INT32_MAX)

@@ -143,6 +143,14 @@ bool launch_timed_events(hipEvent_t* start, hipEvent_t* stop);
             hipLaunchKernelGGL(K, grid, block, shm, s, __VA_ARGS__);                        \
     } while (0)
 
+// Quantized exchange payloads (codec.hip). codec: SSM_CODEC_*; cols % 8 == 0.
+size_t codec_scale_bytes(int64_t rows);
+size_t codec_payload_bytes(int codec, int64_t rows, int64_t cols);
+hipError_t launch_codec_encode(int codec, const void* src, bool src_bf16, int64_t ld, int64_t rows, int64_t cols,
+                               void* payload, hipStream_t s);
+hipError_t launch_codec_decode_acc(int codec, const void* payload, int64_t rows, int64_t cols, float* acc, int64_t ld,
+                                   bool accumulate, hipStream_t s);
+
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t s);  // bytes: multiple of 4
 hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_t s);
 hipError_t launch_copy_rows(void* dst, int64_t ld_dst, const void* src, int64_t ld_src,

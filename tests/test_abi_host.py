@@ -123,3 +123,25 @@ def test_channel_splitter_layout_matches_oracle_on_host():
         assert np.array_equal(s["W_in"], full["W_in"][rows])
         assert np.array_equal(s["W_x"], full["W_x"][:, r * E:(r + 1) * E])
         assert np.array_equal(s["W_out"], full["W_out"][:, r * E:(r + 1) * E])
+
+
+def test_exchange_codec_host_checks(B):
+    """Payload sizes follow the documented layout; bad arguments fail before any launch."""
+    L = B.lib()
+    n = ctypes.c_size_t()
+    assert L.ssm_exchange_payload_bytes(0, 16384, 192, ctypes.byref(n)) == 0 and n.value == 16384 * 192 * 2
+    assert L.ssm_exchange_payload_bytes(1, 3, 8, ctypes.byref(n)) == 0 and n.value == 48
+    # scaled codecs: fp32 scales padded to 256 bytes, then one byte per value
+    assert L.ssm_exchange_payload_bytes(2, 100, 2560, ctypes.byref(n)) == 0 and n.value == 512 + 100 * 2560
+    assert L.ssm_exchange_payload_bytes(3, 64, 16, ctypes.byref(n)) == 0 and n.value == 256 + 64 * 16
+    assert L.ssm_exchange_payload_bytes(4, 1, 8, ctypes.byref(n)) == -1           # unknown codec
+    assert L.ssm_exchange_payload_bytes(0, 1, 12, ctypes.byref(n)) == -2          # cols not a multiple of 8
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: every call below fails its host checks first
+    assert L.ssm_exchange_encode(0, None, 0, 4, 8, 8, fake, 4096, None) == -1     # null source
+    assert L.ssm_exchange_encode(0, fake, 2, 4, 8, 8, fake, 4096, None) == -1     # bad source dtype
+    assert L.ssm_exchange_encode(2, fake, 0, 4, 8, 4, fake, 4096, None) == -1     # ld < cols
+    assert L.ssm_exchange_encode(2, fake, 0, 4, 8, 12, fake, 4096, None) == -2    # ld not a multiple of 8
+    assert L.ssm_exchange_encode(2, fake, 0, 4, 8, 8, fake, 100, None) == -3      # payload too small
+    assert L.ssm_exchange_decode_accumulate(3, fake, 100, 4, 8, fake, 8, 0, None) == -3
+    assert L.ssm_exchange_decode_accumulate(3, fake, 4096, 4, 8, None, 8, 0, None) == -1
+    assert L.ssm_exchange_encode(1, fake, 0, 0, 8, 8, None, 0, None) == 0         # empty: nothing to do
