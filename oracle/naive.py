@@ -76,3 +76,65 @@ def mixer_sequence(w, x_rows: Sequence[Sequence[float]], conv_hist: Optional[Seq
             y_inner.append(acc * _silu(zs[c]))
         ys.append([sum(float(w["W_out"][m][c]) * y_inner[c] for c in range(E)) for m in range(dm)])
     return ys, hist, h
+
+
+def mamba2_sequence(w, nheads: int, headdim: int, d_state: int, ngroups: int, x_rows: Sequence[Sequence[float]],
+                    eps: float = 1e-5):
+    """One fresh sequence through a full-width Mamba-2 mixer, token by token, with scalar
+    loops: packed [z | x | B | C | dt] projection, causal K-tap conv + SiLU over [x | B | C],
+    Delta = softplus(dt + dt_bias) per head, per head h <- exp(Delta*A) h + Delta*x B^T,
+    y = h C + D x, g = y*SiLU(z), RMS normalisation over groups of d_inner/ngroups
+    channels times norm_w, output projection. Returns (outputs, final states [h][p][n])."""
+    H, Pd, N, G = nheads, headdim, d_state, ngroups
+    E = H * Pd
+    Cc = E + 2 * G * N
+    W_in = [_row(w["W_in"], i) for i in range(len(w["W_in"]))]
+    K = len(w["conv_w"][0])
+    conv_w = [_row(w["conv_w"], c) for c in range(Cc)]
+    conv_b = [float(v) for v in w["conv_b"]]
+    A = [-math.exp(float(v)) for v in w["A_log"]]
+    D = [float(v) for v in w["D"]]
+    dtb = [float(v) for v in w["dt_bias"]]
+    nw = [float(v) for v in w["norm_w"]]
+    W_out = [_row(w["W_out"], i) for i in range(len(w["W_out"]))]
+    hist = [[0.0] * Cc for _ in range(K - 1)]
+    h = [[[0.0] * N for _ in range(Pd)] for _ in range(H)]
+    outs = []
+    for xr in x_rows:
+        xr = [float(v) for v in xr]
+        proj = [sum(W_in[i][j] * xr[j] for j in range(len(xr))) for i in range(len(W_in))]
+        z = proj[:E]
+        xbc = proj[E:E + Cc]
+        dt = proj[E + Cc:E + Cc + H]
+        window = hist + [xbc]
+        u = []
+        for c in range(Cc):
+            a = conv_b[c]
+            for j in range(K):
+                a += conv_w[c][j] * window[j][c]
+            u.append(_silu(a))
+        hist = window[1:]
+        xs = u[:E]
+        Bv = u[E:E + G * N]
+        Cv = u[E + G * N:E + 2 * G * N]
+        y = [0.0] * E
+        for hh in range(H):
+            grp = hh // (H // G)
+            delta = _softplus(dt[hh] + dtb[hh])
+            decay = math.exp(delta * A[hh])
+            for p in range(Pd):
+                xv = xs[hh * Pd + p]
+                acc = 0.0
+                for n in range(N):
+                    h[hh][p][n] = decay * h[hh][p][n] + delta * xv * Bv[grp * N + n]
+                    acc += h[hh][p][n] * Cv[grp * N + n]
+                y[hh * Pd + p] = acc + D[hh] * xv
+        g = [y[c] * _silu(z[c]) for c in range(E)]
+        gs = E // G
+        gn = [0.0] * E
+        for k in range(G):
+            ms = sum(g[c] * g[c] for c in range(k * gs, (k + 1) * gs)) / gs
+            for c in range(k * gs, (k + 1) * gs):
+                gn[c] = g[c] / math.sqrt(ms + eps) * nw[c]
+        outs.append([sum(W_out[i][c] * gn[c] for c in range(E)) for i in range(len(W_out))])
+    return outs, h

@@ -181,3 +181,83 @@ def packed_schedule(lengths: List[int], chunk: int) -> List[dict]:
             i += 1
         out.append({"start": w0, "stop": w1, "pieces": pieces})
     return out
+
+
+# ------------------------------------------------------------------ Mamba-2 (SSD) mixer
+@dataclasses.dataclass(frozen=True)
+class Mamba2Shape:
+    """Dimensions of one Mamba-2 mixer layer and of the shard run on one GPU. The split
+    is by heads; B/C groups are split when ngroups is a multiple of the shard count and
+    replicated on every shard otherwise."""
+    d_model: int
+    nheads: int           # total heads
+    headdim: int          # P
+    d_state: int          # N
+    ngroups: int = 1      # G, B/C groups (heads nheads/G per group)
+    d_conv: int = 4       # K
+    shard_count: int = 1
+    act: str = "bf16"
+
+    @property
+    def d_inner(self) -> int:
+        return self.nheads * self.headdim
+
+    @property
+    def heads_shard(self) -> int:
+        assert self.nheads % self.shard_count == 0
+        return self.nheads // self.shard_count
+
+    @property
+    def d_shard(self) -> int:
+        return self.heads_shard * self.headdim
+
+    @property
+    def groups_split(self) -> bool:
+        return self.ngroups % self.shard_count == 0
+
+    @property
+    def groups_shard(self) -> int:
+        return self.ngroups // self.shard_count if self.groups_split else self.ngroups
+
+    @property
+    def conv_dim_shard(self) -> int:
+        return self.d_shard + 2 * self.groups_shard * self.d_state
+
+    @property
+    def in_rows_shard(self) -> int:
+        return 2 * self.d_shard + 2 * self.groups_shard * self.d_state + self.heads_shard
+
+
+MAMBA2_CONFIGS: Dict[str, dict] = {
+    # Mamba-2 2.7B-shaped (80 heads of 64, N 128, one B/C group), shard 1 of a 2-way split;
+    # batch 8 x prefill 2048, then 128 decode steps.
+    "mamba2_2.7b_tp2": dict(shape=Mamba2Shape(2560, 80, 64, 128, 1, 4, 2, "bf16"), seed=11,
+                            batch=8, prefill_len=2048, decode_steps=128),
+}
+
+
+def make_mamba2_layer(shape: Mamba2Shape, seed: int, stress: bool = False,
+                      rng: Optional[np.random.Generator] = None) -> Dict[str, np.ndarray]:
+    """Full-width Mamba-2 weights (float32 arrays; act-dtype ones rounded). Draw order:
+    W_in ([z | x | B | C | dt] rows), conv_w, conv_b ([x | B | C] channels), dt0, A, W_out.
+    dt_bias = softplus^-1(dt0) with dt0 log-uniform in [1e-3, 0.1] per head; A_log =
+    log(U[1, 16]) per head; D = 1 (0 under stress); norm weight 1. Stress draws the
+    matrices at 1/sqrt(fan_in) so that the state path carries y."""
+    g = rng if rng is not None else np.random.Generator(np.random.PCG64(seed))
+    dm, H, P, N, G, K = shape.d_model, shape.nheads, shape.headdim, shape.d_state, shape.ngroups, shape.d_conv
+    E = H * P
+    s = (lambda fan: 1.0 / math.sqrt(fan)) if stress else (lambda fan: 0.02)
+    W_in = g.normal(0.0, s(dm), size=(2 * E + 2 * G * N + H, dm)).astype(np.float32)
+    conv_w = g.normal(0.0, s(K), size=(E + 2 * G * N, K)).astype(np.float32)
+    conv_b = g.normal(0.0, 0.02, size=(E + 2 * G * N,)).astype(np.float32)
+    dt0 = np.exp(g.uniform(math.log(1e-3), math.log(0.1), size=(H,)))
+    A = g.uniform(1.0, 16.0, size=(H,))
+    W_out = g.normal(0.0, 0.02 if not stress else s(E), size=(dm, E)).astype(np.float32)
+    act = shape.act
+    return {
+        "W_in": _store(W_in, act), "conv_w": _store(conv_w, act), "conv_b": _store(conv_b, act),
+        "dt_bias": (dt0 + np.log(-np.expm1(-dt0))).astype(np.float32),
+        "A_log": np.log(A).astype(np.float32),
+        "D": np.zeros(H, np.float32) if stress else np.ones(H, np.float32),
+        "norm_w": np.ones(E, np.float32), "W_out": _store(W_out, act), "_rng": g,
+    }
