@@ -249,6 +249,65 @@ int ssm_decode_ssm(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, c
                    const int32_t* cache_slot, float* ssm_pool, int32_t num_slots, void* g,
                    void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------- Mamba-2 (SSD) shard
+ * Section II-A and Section IV-E: Mamba-2 keeps the mixer pipeline (projection,
+ * convolution, state update, gating, output projection) with a multi-head state whose
+ * update maps onto matrix products; the split is by heads and reuses the same cache and
+ * exchange principles. Per head h (scalar decay, headdim P, N states per row):
+ *   Delta_t = softplus(dt_t + dt_bias_h);  S_t = exp(-exp(A_log_h) Delta_t) S_{t-1} + Delta_t x_t B_t^T
+ *   y_t = S_t C_t + D_h x_t;  g_t = y_t * SiLU(z_t);  g_norm = g / sqrt(mean_group(g^2) + 1e-5) * norm_w
+ * with B_t, C_t of the head's group, and y_partial = out_proj(g_norm).
+ * Shard: H = nheads_total / shard_count heads, E = H * headdim channels; B/C groups are
+ * split (Gs = ngroups_total / shard_count) when ngroups_total is a multiple of
+ * shard_count, else every shard holds all of them (Gs = ngroups_total). The gated
+ * norm's group is d_inner / ngroups_total channels: stage 1 ends with each shard's
+ * partial sum of g^2 per token and norm group [T][ngroups_total] (float32); the caller
+ * sums these over shards (the exchange; identity for one shard) and stage 2 normalises
+ * and projects, reading the g that stage 1 left in the same workspace.
+ * Requirements: headdim == 64, d_state == 128, act_dtype SSM_BF16, nheads_total a
+ * multiple of shard_count and of ngroups_total, H a multiple of 8, d_model a multiple
+ * of 16, 2 <= d_conv <= 4. Caches: conv [S][E + 2 Gs N][d_conv - 1] act (oldest first,
+ * channels x | B | C), state [S][H][64][128] float32. */
+typedef struct ssm2_shard_desc {
+    int32_t d_model, nheads_total, headdim, d_state, ngroups_total, d_conv;
+    int32_t shard_index, shard_count;
+    int32_t act_dtype;
+} ssm2_shard_desc_t;
+/* Shard weights (device, caller-owned). in_proj rows in order z (E), x (E), B (Gs*N),
+ * C (Gs*N), dt (H); conv channels x (E), B (Gs*N), C (Gs*N). A full-width layer uses the
+ * same struct with the full sizes (shard_count 1) and is the input of the splitter. */
+typedef struct ssm2_shard_weights {
+    const void* in_proj_w;   /* [2E + 2 Gs N + H][d_model] act */
+    const void* conv_w;      /* [E + 2 Gs N][d_conv] act */
+    const void* conv_b;      /* [E + 2 Gs N] act */
+    const void* out_proj_w;  /* [d_model][E] act */
+    const float* dt_bias;    /* [H] */
+    const float* A_log;      /* [H] */
+    const float* D;          /* [H] */
+    const float* norm_w;     /* [E] */
+} ssm2_shard_weights_t;
+int ssm2_shard_check_desc(const ssm2_shard_desc_t* desc);
+int ssm2_shard_prefill_workspace_bytes(const ssm2_shard_desc_t* desc, int64_t max_tokens, int32_t max_seqs,
+                                       size_t* bytes);
+int ssm2_shard_decode_workspace_bytes(const ssm2_shard_desc_t* desc, int32_t max_batch, size_t* bytes);
+/* Copy this shard's slices out of full-width weights (the layout above with shard_count 1). */
+int ssm2_shard_slice_weights(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* full,
+                             const ssm2_shard_weights_t* out, hipStream_t stream);
+/* Packed prefill, x [T][d_model] act; metadata as for ssm_shard_prefill. */
+int ssm2_shard_prefill_stage1(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* w, const void* x,
+                              int64_t T, const ssm_seq_meta_t* meta, void* conv_pool, float* ssm_pool,
+                              int32_t num_slots, float* sumsq_partial, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+int ssm2_shard_prefill_stage2(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* w, const float* sumsq,
+                              int64_t T, void* y_partial, void* ws, size_t ws_bytes, hipStream_t stream);
+/* One token per sequence, x_t [batch][d_model]; cache_slot [batch] device int32. */
+int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* w, const void* x_t,
+                             int32_t batch, const int32_t* cache_slot, void* conv_pool, float* ssm_pool,
+                             int32_t num_slots, float* sumsq_partial, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+int ssm2_shard_decode_stage2(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* w, const float* sumsq,
+                             int32_t batch, void* y_partial, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------ measurement
  * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
  * the library launches from the calling thread is launched with hipExtLaunchKernel and

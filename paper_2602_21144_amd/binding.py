@@ -54,6 +54,17 @@ class SeqMetaC(ctypes.Structure):
                 ("has_initial_state", ctypes.c_void_p), ("nseq", ctypes.c_int32)]
 
 
+class Desc2(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "d_model", "nheads_total", "headdim", "d_state", "ngroups_total", "d_conv", "shard_index", "shard_count",
+        "act_dtype")]
+
+
+class Weights2(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "in_proj_w", "conv_w", "conv_b", "out_proj_w", "dt_bias", "A_log", "D", "norm_w")]
+
+
 _lib: Optional[ctypes.CDLL] = None
 _P, _I32, _I64, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
 
@@ -82,6 +93,14 @@ _SIGS = {
     "ssm_exchange_payload_bytes": ([_I32, _I64, _I64, _P], _I32),
     "ssm_exchange_encode": ([_I32, _P, _I32, _I64, _I64, _I64, _P, _SZ, _P], _I32),
     "ssm_exchange_decode_accumulate": ([_I32, _P, _SZ, _I64, _I64, _P, _I64, _I32, _P], _I32),
+    "ssm2_shard_check_desc": ([_P], _I32),
+    "ssm2_shard_prefill_workspace_bytes": ([_P, _I64, _I32, _P], _I32),
+    "ssm2_shard_decode_workspace_bytes": ([_P, _I32, _P], _I32),
+    "ssm2_shard_slice_weights": ([_P, _P, _P, _P], _I32),
+    "ssm2_shard_prefill_stage1": ([_P, _P, _P, _I64, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm2_shard_prefill_stage2": ([_P, _P, _P, _I64, _P, _P, _SZ, _P], _I32),
+    "ssm2_shard_decode_stage1": ([_P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm2_shard_decode_stage2": ([_P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_timing_enable": ([_I32, ctypes.c_char_p], _I32),
     "ssm_timing_collect": ([_P, _I32, _P], _I32),
 }
@@ -322,6 +341,102 @@ def bind(name: str, *args, **kw) -> BoundCall:
     a, keep = _MARSHAL[name](*args, **kw)
     tensors = tuple(v for v in list(args) + list(kw.values()) if isinstance(v, torch.Tensor))
     return BoundCall(name, a, keep + tensors)
+
+
+# ------------------------------------------------------------------ Mamba-2 (SSD) shard
+_W2KEYS = {"in_proj_w": "W_in", "conv_w": "conv_w", "conv_b": "conv_b", "out_proj_w": "W_out",
+           "dt_bias": "dt_bias", "A_log": "A_log", "D": "D", "norm_w": "norm_w"}
+_W2_F32 = ("dt_bias", "A_log", "D", "norm_w")
+
+
+def make_desc2(shape, shard_index: int = 0, full: bool = False) -> Desc2:
+    """Descriptor of shard `shard_index` (or of the unsplit layer with full=True)."""
+    d = Desc2(shape.d_model, shape.nheads, shape.headdim, shape.d_state, shape.ngroups, shape.d_conv,
+              0 if full else shard_index, 1 if full else shape.shard_count, SSM_BF16)
+    _check(lib().ssm2_shard_check_desc(ctypes.byref(d)))
+    return d
+
+
+def upload_weights2(host: Dict[str, np.ndarray], device="cuda") -> Dict[str, torch.Tensor]:
+    return {k: torch.from_numpy(np.ascontiguousarray(host[k], np.float32)).to(
+        device=device, dtype=torch.float32 if k in _W2_F32 else torch.bfloat16) for k in _W2KEYS.values()}
+
+
+def weights2_struct(dev: Dict[str, torch.Tensor]) -> Weights2:
+    return Weights2(*[_ptr(dev[_W2KEYS[f]]) for f, _ in Weights2._fields_])
+
+
+def empty_shard_weights2(shape, device="cuda") -> Dict[str, torch.Tensor]:
+    E, H, dm, K = shape.d_shard, shape.heads_shard, shape.d_model, shape.d_conv
+    rows, Cc = shape.in_rows_shard, shape.conv_dim_shard
+    b, f = torch.bfloat16, torch.float32
+    shapes = {"W_in": ((rows, dm), b), "conv_w": ((Cc, K), b), "conv_b": ((Cc,), b), "W_out": ((dm, E), b),
+              "dt_bias": ((H,), f), "A_log": ((H,), f), "D": ((H,), f), "norm_w": ((E,), f)}
+    return {k: torch.empty(sz, dtype=t, device=device) for k, (sz, t) in shapes.items()}
+
+
+def ssm2_shard_slice_weights(desc: Desc2, full: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor], stream=None):
+    fw, ow = weights2_struct(full), weights2_struct(out)
+    _check(lib().ssm2_shard_slice_weights(ctypes.byref(desc), ctypes.byref(fw), ctypes.byref(ow), _stream(stream)))
+
+
+def m2_prefill_workspace_bytes(desc: Desc2, max_tokens: int, max_seqs: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm2_shard_prefill_workspace_bytes(ctypes.byref(desc), max_tokens, max_seqs, ctypes.byref(n)))
+    return n.value
+
+
+def m2_decode_workspace_bytes(desc: Desc2, max_batch: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm2_shard_decode_workspace_bytes(ctypes.byref(desc), max_batch, ctypes.byref(n)))
+    return n.value
+
+
+def _w2(weights):
+    return weights if isinstance(weights, Weights2) else weights2_struct(weights)
+
+
+def _m_ssm2_shard_prefill_stage1(desc, weights, x, meta: SeqMeta, conv_pool, ssm_pool, sumsq_partial, ws, stream=None):
+    w = _w2(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x), meta.T, ctypes.byref(meta.c), _ptr(conv_pool),
+            _ptr(ssm_pool), conv_pool.shape[0], _ptr(sumsq_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w, meta)
+
+
+def _m_ssm2_shard_prefill_stage2(desc, weights, sumsq, T, y_partial, ws, stream=None):
+    w = _w2(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(sumsq), T, _ptr(y_partial), _ptr(ws), ws.numel(),
+            _stream(stream)), (desc, w)
+
+
+def _m_ssm2_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, sumsq_partial, ws, stream=None):
+    w = _w2(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0], _ptr(cache_slot), _ptr(conv_pool),
+            _ptr(ssm_pool), conv_pool.shape[0], _ptr(sumsq_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w)
+
+
+def _m_ssm2_shard_decode_stage2(desc, weights, sumsq, batch, y_partial, ws, stream=None):
+    w = _w2(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(sumsq), batch, _ptr(y_partial), _ptr(ws), ws.numel(),
+            _stream(stream)), (desc, w)
+
+
+_MARSHAL.update({name[3:]: fn for name, fn in list(globals().items()) if name.startswith("_m_ssm2_")})
+
+
+def ssm2_shard_prefill_stage1(desc, weights, x, meta, conv_pool, ssm_pool, sumsq_partial, ws, stream=None):
+    _call("ssm2_shard_prefill_stage1", desc, weights, x, meta, conv_pool, ssm_pool, sumsq_partial, ws, stream)
+
+
+def ssm2_shard_prefill_stage2(desc, weights, sumsq, T, y_partial, ws, stream=None):
+    _call("ssm2_shard_prefill_stage2", desc, weights, sumsq, T, y_partial, ws, stream)
+
+
+def ssm2_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, sumsq_partial, ws, stream=None):
+    _call("ssm2_shard_decode_stage1", desc, weights, x_t, cache_slot, conv_pool, ssm_pool, sumsq_partial, ws, stream)
+
+
+def ssm2_shard_decode_stage2(desc, weights, sumsq, batch, y_partial, ws, stream=None):
+    _call("ssm2_shard_decode_stage2", desc, weights, sumsq, batch, y_partial, ws, stream)
 
 
 SSM_CODEC = {"f16": 0, "bf16": 1, "fp8": 2, "int8": 3}

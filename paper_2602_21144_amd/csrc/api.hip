@@ -639,3 +639,282 @@ int ssm_decode_ssm(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, cons
 }
 
 }  // extern "C"
+
+// ==================================================================== Mamba-2 (SSD) shard
+// Prefill stage 1: in_proj GEMM -> [z | x | B | C | dt]; conv1d+SiLU over [x | B | C]
+// (and the conv history); SSD passes -> g and final states; per-head sums of g^2 summed
+// into norm groups. [exchange of the sums of squares: the caller's.] Stage 2: gated RMS
+// normalisation -> out_proj GEMM. Decode: skinny in_proj, one conv step, one state step.
+namespace {
+
+struct M2 {
+    int64_t dm, Etot, E, H, P, N, G, Gs, Cc, rows, K, r;
+    int hpg, gsize, g_off;
+    bool split;
+};
+
+int m2_dims(const ssm2_shard_desc_t* d, M2* o) {
+    if (!d) return fail(SSM_E_INVAL, "desc is null");
+    if (d->act_dtype != SSM_BF16) return fail(SSM_E_INVAL, "the Mamba-2 shard runs with bf16 activations");
+    if (d->headdim != 64 || d->d_state != 128) return fail(SSM_E_INVAL, "headdim %d / d_state %d: 64 / 128 required", d->headdim, d->d_state);
+    if (d->d_model <= 0 || d->d_model % 16) return fail(SSM_E_INVAL, "d_model %d must be a positive multiple of 16", d->d_model);
+    if (d->shard_count <= 0 || d->shard_index < 0 || d->shard_index >= d->shard_count)
+        return fail(SSM_E_INVAL, "shard %d of %d", d->shard_index, d->shard_count);
+    if (d->ngroups_total <= 0 || d->nheads_total <= 0 || d->nheads_total % d->ngroups_total)
+        return fail(SSM_E_INVAL, "nheads %d must be a positive multiple of ngroups %d", d->nheads_total, d->ngroups_total);
+    if (d->nheads_total % d->shard_count) return fail(SSM_E_INVAL, "nheads %d not divisible by %d shards", d->nheads_total, d->shard_count);
+    if (d->d_conv < 2 || d->d_conv > kMaxConv) return fail(SSM_E_INVAL, "d_conv %d not in [2, %d]", d->d_conv, kMaxConv);
+    M2 m{};
+    m.dm = d->d_model; m.P = 64; m.N = 128; m.G = d->ngroups_total; m.K = d->d_conv; m.r = d->shard_index;
+    m.H = d->nheads_total / d->shard_count;
+    if (m.H % 8) return fail(SSM_E_INVAL, "%lld heads per shard: a multiple of 8 is required", (long long)m.H);
+    m.E = m.H * m.P; m.Etot = (int64_t)d->nheads_total * m.P;
+    m.split = m.G % d->shard_count == 0;
+    m.Gs = m.split ? m.G / d->shard_count : m.G;
+    m.Cc = m.E + 2 * m.Gs * m.N;
+    m.rows = 2 * m.E + 2 * m.Gs * m.N + m.H;
+    m.hpg = (int)(d->nheads_total / m.G);
+    m.gsize = (int)(m.Etot / m.G);
+    m.g_off = m.split ? (int)(m.r * m.Gs) : 0;
+    *o = m;
+    return SSM_OK;
+}
+
+int m2_check_weights(const ssm2_shard_weights_t* w) {
+    if (!w) return fail(SSM_E_INVAL, "weights is null");
+    const void* ps[] = {w->in_proj_w, w->conv_w, w->conv_b, w->out_proj_w, w->dt_bias, w->A_log, w->D, w->norm_w};
+    const char* names[] = {"in_proj_w", "conv_w", "conv_b", "out_proj_w", "dt_bias", "A_log", "D", "norm_w"};
+    for (int i = 0; i < 8; ++i) {
+        if (!ps[i]) return fail(SSM_E_INVAL, "weights.%s is null", names[i]);
+        if (!aligned16(ps[i])) return fail(SSM_E_ALIGN, "weights.%s is not 16-byte aligned", names[i]);
+    }
+    return SSM_OK;
+}
+
+struct M2Ws {
+    int32_t* status;
+    char *zx, *u, *g, *gn;
+    float* hs;
+    char* plan;
+    int32_t* count;
+    float *states, *lsum;
+    int win, maxw;
+    size_t total;
+};
+
+M2Ws m2_layout(const M2& m, int64_t T, int nseq, bool prefill, void* base) {
+    M2Ws L{};
+    char* b = (char*)base;
+    size_t off = kWsHeader;
+    auto take = [&](size_t bytes) { char* p = b ? b + off : nullptr; off += align256(bytes); return p; };
+    L.status = (int32_t*)b;
+    L.zx = take((size_t)T * m.rows * 2);
+    L.u = take((size_t)T * m.Cc * 2);
+    L.g = take((size_t)T * m.E * 2);
+    L.gn = take((size_t)T * m.E * 2);
+    L.hs = (float*)take((size_t)T * m.H * 4);
+    if (prefill) {
+        L.win = ssd_window_len(T, (int)m.H);
+        L.maxw = ssd_max_windows(T, nseq, L.win);
+        L.plan = take((size_t)L.maxw * 16);
+        L.count = (int32_t*)take(16);
+        L.states = (float*)take(ssd_state_bytes(L.maxw, (int)m.H));
+        L.lsum = (float*)take((size_t)L.maxw * m.H * 4);
+    }
+    L.total = off;
+    return L;
+}
+
+SsdPublic m2_ssd(const M2& m, const ssm2_shard_weights_t* w, const M2Ws& L, float* pool, int S, int32_t* status) {
+    SsdPublic p{};
+    p.zx = L.zx; p.ld_zx = m.rows; p.u = L.u; p.ld_u = m.Cc;
+    p.dt_col = (int)(2 * m.E + 2 * m.Gs * m.N); p.b_col = (int)m.E; p.c_col = (int)(m.E + m.Gs * m.N);
+    p.H = (int)m.H; p.h_global0 = (int)(m.r * m.H); p.hpg = m.hpg; p.g_off = m.g_off;
+    p.dt_bias = w->dt_bias; p.A_log = w->A_log; p.D = w->D;
+    p.g = L.g; p.hs = L.hs; p.pool = pool; p.S = S; p.status = status;
+    return p;
+}
+
+ConvArgs m2_conv(const M2& m, const ssm2_shard_weights_t* w, const M2Ws& L, int64_t T, const int32_t* cu,
+                 const int32_t* slot, const int32_t* hi, int nseq, void* conv_pool, int S) {
+    ConvArgs a{};
+    a.xz = L.zx + m.E * 2; a.ld_xz = m.rows;   // [x | B | C] columns of the in_proj output
+    a.w = w->conv_w; a.b = w->conv_b; a.u = L.u; a.conv_pool = conv_pool;
+    a.cu = cu; a.slot = slot; a.has_init = hi; a.status = L.status;
+    a.T = T; a.E = (int)m.Cc; a.K = (int)m.K; a.nseq = nseq; a.S = S;
+    return a;
+}
+
+int m2_stage2(const M2& m, const ssm2_shard_weights_t* w, const float* sumsq, int64_t T, void* y, const M2Ws& L,
+              hipStream_t s, const char* norm_name, const char* out_name) {
+    SSM_TIMED(norm_name, s, launch_ssd_norm(L.g, sumsq, w->norm_w, L.gn, T, (int)m.E, (int)m.G, m.gsize,
+                                            (int)(m.r * m.E), 1e-5f, s));
+    return gemm(T, m.dm, m.E, L.gn, m.E, SSM_BF16, w->out_proj_w, m.E, SSM_BF16, y, m.dm, SSM_BF16, s, out_name,
+                kGemmOutProj);
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssm2_shard_check_desc(const ssm2_shard_desc_t* d) {
+    M2 m;
+    return m2_dims(d, &m);
+}
+
+int ssm2_shard_prefill_workspace_bytes(const ssm2_shard_desc_t* d, int64_t max_tokens, int32_t max_seqs, size_t* bytes) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    if (!bytes) return fail(SSM_E_INVAL, "bytes is null");
+    if (max_tokens < 0 || max_seqs < 0) return fail(SSM_E_INVAL, "negative size");
+    *bytes = m2_layout(m, max_tokens, max_seqs, true, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm2_shard_decode_workspace_bytes(const ssm2_shard_desc_t* d, int32_t max_batch, size_t* bytes) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    if (!bytes) return fail(SSM_E_INVAL, "bytes is null");
+    if (max_batch < 0) return fail(SSM_E_INVAL, "negative size");
+    *bytes = m2_layout(m, max_batch, 0, false, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm2_shard_slice_weights(const ssm2_shard_desc_t* d, const ssm2_shard_weights_t* full,
+                             const ssm2_shard_weights_t* out, hipStream_t s) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    SSM_TRY(m2_check_weights(full));
+    SSM_TRY(m2_check_weights(out));
+    const int64_t dm = m.dm, Et = m.Etot, E = m.E, N = m.N, G = m.G, Gs = m.Gs, H = m.H, K = m.K;
+    const int64_t g0 = m.g_off, c0 = m.r * E, h0 = m.r * H;
+    const int64_t rows_full = 2 * Et + 2 * G * N + (int64_t)(Et / m.P);
+    (void)rows_full;
+    auto cp = [&](const void* src, int64_t ld_src, void* dst, int64_t ld_dst, int64_t rows, int64_t row_bytes,
+                  const char* what) -> int {
+        SSM_TRY_HIP(launch_copy_rows(dst, ld_dst, src, ld_src, rows, row_bytes, s), what);
+        return SSM_OK;
+    };
+    const char* fin = (const char*)full->in_proj_w;
+    char* oin = (char*)out->in_proj_w;
+    const int64_t rb = dm * 2;  // bytes per in_proj row
+    SSM_TRY(cp(fin + c0 * rb, rb, oin, rb, E, rb, "slice z rows"));
+    SSM_TRY(cp(fin + (Et + c0) * rb, rb, oin + E * rb, rb, E, rb, "slice x rows"));
+    SSM_TRY(cp(fin + (2 * Et + g0 * N) * rb, rb, oin + 2 * E * rb, rb, Gs * N, rb, "slice B rows"));
+    SSM_TRY(cp(fin + (2 * Et + G * N + g0 * N) * rb, rb, oin + (2 * E + Gs * N) * rb, rb, Gs * N, rb, "slice C rows"));
+    SSM_TRY(cp(fin + (2 * Et + 2 * G * N + h0) * rb, rb, oin + (2 * E + 2 * Gs * N) * rb, rb, H, rb, "slice dt rows"));
+    const char* fcw = (const char*)full->conv_w;
+    char* ocw = (char*)out->conv_w;
+    const int64_t cb = K * 2;
+    SSM_TRY(cp(fcw + c0 * cb, cb, ocw, cb, E, cb, "slice conv x"));
+    SSM_TRY(cp(fcw + (Et + g0 * N) * cb, cb, ocw + E * cb, cb, Gs * N, cb, "slice conv B"));
+    SSM_TRY(cp(fcw + (Et + G * N + g0 * N) * cb, cb, ocw + (E + Gs * N) * cb, cb, Gs * N, cb, "slice conv C"));
+    const char* fcb = (const char*)full->conv_b;
+    char* ocb = (char*)out->conv_b;
+    SSM_TRY(cp(fcb + c0 * 2, 2, ocb, 2, E, 2, "slice conv_b x"));
+    SSM_TRY(cp(fcb + (Et + g0 * N) * 2, 2, ocb + E * 2, 2, Gs * N, 2, "slice conv_b B"));
+    SSM_TRY(cp(fcb + (Et + G * N + g0 * N) * 2, 2, ocb + (E + Gs * N) * 2, 2, Gs * N, 2, "slice conv_b C"));
+    SSM_TRY(cp(full->dt_bias + h0, 4, (void*)out->dt_bias, 4, H, 4, "slice dt_bias"));
+    SSM_TRY(cp(full->A_log + h0, 4, (void*)out->A_log, 4, H, 4, "slice A_log"));
+    SSM_TRY(cp(full->D + h0, 4, (void*)out->D, 4, H, 4, "slice D"));
+    SSM_TRY(cp(full->norm_w + c0, 4, (void*)out->norm_w, 4, E, 4, "slice norm_w"));
+    SSM_TRY(cp((const char*)full->out_proj_w + c0 * 2, Et * 2, (void*)out->out_proj_w, E * 2, dm, E * 2,
+               "slice out_proj columns"));
+    return SSM_OK;
+}
+
+int ssm2_shard_prefill_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weights_t* w, const void* x, int64_t T,
+                              const ssm_seq_meta_t* meta, void* conv_pool, float* ssm_pool, int32_t S,
+                              float* sumsq_partial, void* ws, size_t ws_bytes, hipStream_t s) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    SSM_TRY(m2_check_weights(w));
+    if (T < 0 || S <= 0) return fail(SSM_E_INVAL, "T %lld, num_slots %d", (long long)T, S);
+    SSM_TRY(check_meta(meta, T));
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    M2Ws L = m2_layout(m, T, meta->nseq, true, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L.total));
+    L = m2_layout(m, T, meta->nseq, true, ws);
+    if (meta->nseq == 0) return SSM_OK;
+    if (T > 0) {
+        SSM_TRY(check_ptr(x, "x"));
+        SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
+        SSM_TRY(gemm(T, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
+                     "m2.prefill.in_proj", kGemmInProj));
+    }
+    // (the history update also runs for a batch of empty sequences: fresh ones end with zeros)
+    ConvArgs ca = m2_conv(m, w, L, T, meta->cu_seqlens, meta->cache_slot, meta->has_initial_state, meta->nseq,
+                          conv_pool, S);
+    SSM_TIMED("m2.prefill.conv1d", s, launch_conv_prefill(ca, true, s));
+    SSM_TIMED("m2.prefill.conv_history", s, launch_conv_state_update(ca, true, s));
+    SsdPublic p = m2_ssd(m, w, L, ssm_pool, S, L.status);
+    p.cu = meta->cu_seqlens; p.slot = meta->cache_slot; p.has_init = meta->has_initial_state; p.nseq = meta->nseq;
+    p.win = L.win; p.T = T; p.plan = L.plan; p.plan_count = L.count; p.max_windows = L.maxw; p.states = L.states; p.lsum = L.lsum;
+    SSM_TRY_HIP(launch_ssd_prefill(p, s), "ssd prefill");
+    if (T > 0)
+        SSM_TIMED("m2.prefill.group_sumsq", s, launch_ssd_group_sumsq(L.hs, (int)m.H, (int)(m.r * m.H), m.hpg, (int)m.G,
+                                                                     sumsq_partial, T, s));
+    return SSM_OK;
+}
+
+int ssm2_shard_prefill_stage2(const ssm2_shard_desc_t* d, const ssm2_shard_weights_t* w, const float* sumsq, int64_t T,
+                              void* y, void* ws, size_t ws_bytes, hipStream_t s) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    SSM_TRY(m2_check_weights(w));
+    if (T < 0) return fail(SSM_E_INVAL, "T %lld", (long long)T);
+    if (T == 0) return SSM_OK;
+    SSM_TRY(check_ptr(sumsq, "sumsq"));
+    SSM_TRY(check_ptr(y, "y_partial"));
+    // the stage-1 part of the layout does not depend on the sequence count
+    M2Ws L = m2_layout(m, T, 0, false, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L.total));
+    L = m2_layout(m, T, 0, false, ws);
+    return m2_stage2(m, w, sumsq, T, y, L, s, "m2.prefill.norm", "m2.prefill.out_proj");
+}
+
+int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weights_t* w, const void* x, int32_t B,
+                             const int32_t* slot, void* conv_pool, float* ssm_pool, int32_t S, float* sumsq_partial,
+                             void* ws, size_t ws_bytes, hipStream_t s) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    SSM_TRY(m2_check_weights(w));
+    if (B < 0 || S <= 0) return fail(SSM_E_INVAL, "batch %d, num_slots %d", B, S);
+    M2Ws L = m2_layout(m, B, 0, false, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L.total));
+    L = m2_layout(m, B, 0, false, ws);
+    if (B == 0) return SSM_OK;
+    SSM_TRY(check_ptr(x, "x_t"));
+    if (!slot) return fail(SSM_E_INVAL, "cache_slot is null");
+    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
+    SSM_TRY(gemm(B, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
+                 "m2.decode.in_proj", kGemmInProj));
+    ConvArgs ca = m2_conv(m, w, L, B, nullptr, slot, nullptr, B, conv_pool, S);
+    SSM_TIMED("m2.decode.conv", s, launch_conv_decode(ca, true, s));
+    SsdPublic p = m2_ssd(m, w, L, ssm_pool, S, L.status);
+    p.slot = slot;
+    SSM_TIMED("m2.decode.state", s, launch_ssd_decode(p, B, s));
+    SSM_TIMED("m2.decode.group_sumsq", s, launch_ssd_group_sumsq(L.hs, (int)m.H, (int)(m.r * m.H), m.hpg, (int)m.G,
+                                                                sumsq_partial, B, s));
+    return SSM_OK;
+}
+
+int ssm2_shard_decode_stage2(const ssm2_shard_desc_t* d, const ssm2_shard_weights_t* w, const float* sumsq, int32_t B,
+                             void* y, void* ws, size_t ws_bytes, hipStream_t s) {
+    M2 m;
+    SSM_TRY(m2_dims(d, &m));
+    SSM_TRY(m2_check_weights(w));
+    if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
+    M2Ws L = m2_layout(m, B, 0, false, nullptr);
+    SSM_TRY(check_ws(ws, ws_bytes, L.total));
+    L = m2_layout(m, B, 0, false, ws);
+    if (B == 0) return SSM_OK;
+    SSM_TRY(check_ptr(sumsq, "sumsq"));
+    SSM_TRY(check_ptr(y, "y_partial"));
+    return m2_stage2(m, w, sumsq, B, y, L, s, "m2.decode.norm", "m2.decode.out_proj");
+}
+
+}  // extern "C"

@@ -143,6 +143,33 @@ bool launch_timed_events(hipEvent_t* start, hipEvent_t* stop);
             hipLaunchKernelGGL(K, grid, block, shm, s, __VA_ARGS__);                        \
     } while (0)
 
+// Mamba-2 (SSD) state update of one shard (ssd.hip); headdim 64, d_state 128, bf16.
+struct SsdPublic {
+    const void* zx; int64_t ld_zx;     // in_proj output [T][ld_zx]: z at col 0, dt at dt_col
+    const void* u; int64_t ld_u;       // conv output [T][ld_u]: x at col 0, B at b_col, C at c_col
+    int dt_col, b_col, c_col;
+    int H;                             // heads of the shard
+    int h_global0, hpg, g_off;         // first global head, heads per B/C group, local group offset
+    const float* dt_bias; const float* A_log; const float* D;
+    void* g; float* hs;                // [T][H*64] gated output; [T][H] sums of g^2 per head
+    float* pool;                       // [S][H][64][128]
+    const int32_t* cu; const int32_t* slot; const int32_t* has_init;
+    int32_t* status;
+    int nseq, S, win;
+    int64_t T;
+    void* plan; int32_t* plan_count; int max_windows;
+    float* states; float* lsum;        // [max_windows][H][64][128], [max_windows][H]
+};
+int ssd_window_len(int64_t T, int H);
+int ssd_max_windows(int64_t T, int nseq, int win);
+size_t ssd_state_bytes(int max_windows, int H);
+hipError_t launch_ssd_prefill(const SsdPublic& p, hipStream_t s);
+hipError_t launch_ssd_decode(const SsdPublic& p, int batch, hipStream_t s);
+hipError_t launch_ssd_group_sumsq(const float* hs, int H, int h_global0, int hpg, int G, float* out, int64_t T,
+                                  hipStream_t s);
+hipError_t launch_ssd_norm(const void* g, const float* sumsq, const float* norm_w, void* out, int64_t T, int E, int G,
+                           int gsize, int c_global0, float eps, hipStream_t s);
+
 // Quantized exchange payloads (codec.hip). codec: SSM_CODEC_*; cols % 8 == 0.
 size_t codec_scale_bytes(int64_t rows);
 size_t codec_payload_bytes(int codec, int64_t rows, int64_t cols);
