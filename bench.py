@@ -290,7 +290,107 @@ def run(args):
         ssm1 = torch.zeros(S, E, N, dtype=torch.float32, device=dev)
         B.ssm_shard_prefill_stage2(desc[1], wst[1], p0, meta, ssm1, y1, wsp[1])      # shard 1's out_proj partial
         result["codec"] = codec_figures(B, torch, {"x_dbl": [xa, p1_pref], "y_partial": [y, y1]})
+    if not args.no_mamba2:
+        log("Mamba-2 (SSD) shard on its workload (outside the timed region)")
+        result["mamba2"] = mamba2_figures(B, torch, args.steps, args.warmup)
     return result, (sh, full, x_host, xdec_host, slots, S)
+
+
+def mamba2_figures(B, torch, steps, warmup):
+    """The Mamba-2 (SSD) shard on its 2.7B-shaped workload (shard 0 of 2: 40 heads of 64,
+    N 128, one replicated B/C group): 8 x 2048 prefill and 128 decode steps, the other
+    shard's sums of squares precomputed (the other GPU's work), per-dispatch kernel times."""
+    import numpy as np
+    from paper_2602_21144_amd import synth
+    cfg = synth.MAMBA2_CONFIGS["mamba2_2.7b_tp2"]
+    sh = cfg["shape"]
+    Bsz, L, nd = cfg["batch"], cfg["prefill_len"], cfg["decode_steps"]
+    T = Bsz * L
+    dev = "cuda"
+    full = synth.make_mamba2_layer(sh, cfg["seed"])
+    rng = full["_rng"]
+    x = torch.from_numpy(synth.make_tokens(rng, T, sh.d_model, "bf16")).to(dev, torch.bfloat16)
+    xdec = torch.from_numpy(np.stack([synth.make_tokens(rng, Bsz, sh.d_model, "bf16") for _ in range(nd)])).to(
+        dev, torch.bfloat16)
+    slots = synth.make_slots(rng, Bsz)
+    S = Bsz + 16
+    fd = B.upload_weights2(full, dev)
+    desc = [B.make_desc2(sh, r) for r in range(2)]
+    w = []
+    for r in range(2):
+        o = B.empty_shard_weights2(sh, dev)
+        B.ssm2_shard_slice_weights(desc[r], fd, o)
+        w.append(B.weights2_struct(o))
+        w[-1]._keep = o
+    del fd
+    meta = B.SeqMeta(np.arange(0, T + 1, L), slots, np.zeros(Bsz, np.int32), S, dev)
+    sl = torch.from_numpy(slots).to(dev)
+    conv = [torch.zeros(S, sh.conv_dim_shard, sh.d_conv - 1, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    ssm = [torch.zeros(S, sh.heads_shard, 64, 128, dtype=torch.float32, device=dev) for _ in range(2)]
+    wsp = [B.workspace(B.m2_prefill_workspace_bytes(desc[r], T, Bsz), dev) for r in range(2)]
+    wsd = [B.workspace(B.m2_decode_workspace_bytes(desc[r], Bsz), dev) for r in range(2)]
+    G = sh.ngroups
+    ss0, ss1 = (torch.zeros(T, G, dtype=torch.float32, device=dev) for _ in range(2))
+    q0 = torch.zeros(Bsz, G, dtype=torch.float32, device=dev)
+    q1 = torch.zeros(nd, Bsz, G, dtype=torch.float32, device=dev)
+    y = torch.empty(T, sh.d_model, dtype=torch.bfloat16, device=dev)
+    yd = torch.empty(Bsz, sh.d_model, dtype=torch.bfloat16, device=dev)
+    # the other shard's partial sums of squares (its GPU's work), outside the timed region
+    B.ssm2_shard_prefill_stage1(desc[1], w[1], x, meta, conv[1], ssm[1], ss1, wsp[1])
+    for k in range(nd):
+        B.ssm2_shard_decode_stage1(desc[1], w[1], xdec[k], sl, conv[1], ssm[1], q1[k], wsd[1])
+    pre = (B.bind("ssm2_shard_prefill_stage1", desc[0], w[0], x, meta, conv[0], ssm[0], ss0, wsp[0]),
+           B.bind("ssm_reduce_add_f32", ss0, ss1),
+           B.bind("ssm2_shard_prefill_stage2", desc[0], w[0], ss0, T, y, wsp[0]))
+    dec = [(B.bind("ssm2_shard_decode_stage1", desc[0], w[0], xdec[k], sl, conv[0], ssm[0], q0, wsd[0]),
+            B.bind("ssm_reduce_add_f32", q0, q1[k]),
+            B.bind("ssm2_shard_decode_stage2", desc[0], w[0], q0, Bsz, yd, wsd[0])) for k in range(nd)]
+
+    def step(evs=None):
+        if evs:
+            evs[0].record()
+        for c in pre:
+            c()
+        if evs:
+            evs[1].record()
+        for k in range(nd):
+            for c in dec[k]:
+                c()
+        if evs:
+            evs[2].record()
+    for _ in range(max(warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True)
+    step()
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    bd = B.ssm_timing_collect()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    assert B.take_status(wsp[0]) == 0 and B.take_status(wsd[0]) == 0
+    pre_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    dec_us = float(np.mean([e[1].elapsed_time(e[2]) for e in evs])) * 1e3 / nd
+    kernels = {k: {"launches": n, "avg_us": round(1e3 * ms / n, 3)} for k, (n, ms) in
+               sorted(bd.items(), key=lambda kv: -kv[1][1])}
+    # SSD main pass: per 64-token chunk and head, the four products (two of them on hi/lo
+    # operand pairs) and the bytes the pass must move: x, z, B, C, dt in, g out
+    E, H, N, P, Q = sh.d_shard, sh.heads_shard, 128, 64, 64
+    flops = (T / Q) * H * (2 * Q * Q * N + 2 * Q * Q * P + 4 * Q * N * P + 4 * P * Q * N)
+    nbytes = T * (3 * E * 2 + 2 * sh.groups_shard * N * 2 + H * 2)
+    main = bd.get("prefill.ssd_main", (1, float("nan")))
+    main_s = main[1] / main[0] * 1e-3
+    return {"workload": "Mamba-2 2.7B-shaped mixer layer, shard 0 of a 2-way head split: d_model 2560, 40 of 80 "
+                        "heads of 64, d_state 128, one B/C group (replicated), d_conv 4; batch 8 x prefill 2048, "
+                        "then 128 decode steps; bf16 activations, fp32 state; seed 11",
+            "prefill_ms": round(pre_ms, 4), "prefill_tokens_per_s": round(T / (pre_ms * 1e-3), 1),
+            "decode_us_per_step": round(dec_us, 3),
+            "ssd_main": {"avg_us": round(main_s * 1e6, 3), "TFLOP_per_s": round(flops / main_s / 1e12, 1),
+                         "GB_per_s": round(nbytes / main_s / 1e9, 1), "flops": flops, "bytes": nbytes},
+            "kernels": kernels}
 
 
 def codec_figures(B, torch, tensors):
@@ -389,6 +489,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
+    ap.add_argument("--no-mamba2", action="store_true", help="skip the Mamba-2 (SSD) shard figures")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
                          "to scale hardware byte counters)")
