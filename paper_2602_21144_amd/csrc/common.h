@@ -13,6 +13,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kN = 16;          // states per channel the kernels are built for
 constexpr int kMaxConv = 4;     // largest convolution width
@@ -51,6 +52,9 @@ __device__ __forceinline__ float softplus_f(float v) {
     return v > 20.0f ? v : l;
 }
 // SiLU(v) = v / (1 + e^-v)
+// min(rem, cap) for a row count, in integer arithmetic (the 64-bit min of the device headers
+// is evaluated in double precision, which leaves the result in vector registers)
+__device__ __forceinline__ int rows_upto(int64_t rem, int cap) { return rem < cap ? (int)rem : cap; }
 __device__ __forceinline__ float silu_f(float v) { return v * fast_rcp(1.0f + fast_exp2(-v * kLog2e)); }
 
 // Workspace header: status word at offset 0; regions start 256-byte aligned.

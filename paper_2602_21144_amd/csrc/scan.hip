@@ -154,7 +154,7 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
             nxt.load(a, b0 + kTB, w1, c);
             st.load(a, b0 + kTB, w1, tid, kWave * CW);
         }
-        const int nt = (int)min<int64_t>(kTB, w1 - b0);
+        const int nt = rows_upto(w1 - b0, kTB);
 #pragma unroll
         for (int i = 0; i < kTB; ++i) {
             if (i < nt) {
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
             nxt.load(a, b0 + kTB, w1, c);
             st.load(a, b0 + kTB, w1, tid, kWave * CW);
         }
-        const int nt = (int)min<int64_t>(kTB, w1 - b0);
+        const int nt = rows_upto(w1 - b0, kTB);
         if (ok && s_end >= b0 + nt) {
             // no sequence ends inside this block: straight-line recurrence from registers
 #pragma unroll

@@ -16,8 +16,10 @@
 // Parallel layout: each sequence is cut into windows of whole chunks; a workgroup walks one
 // (window, head) chunk by chunk. Pass A: each window's end state from zero (and its total
 // log-decay); pass B: per state element, windows linked in order from the sequence's
-// initial state; pass C: the full chunk walk from the linked state, writing g, the per-head
-// sums of g^2 and the final state.
+// initial state; pass C: the full chunk walk from the linked state, writing g and the final
+// state; then the per-head sums of g^2 for the gated norm.
+#include <algorithm>
+
 #include "common.h"
 
 namespace ssm {
@@ -33,24 +35,21 @@ constexpr int kWinFirst = 1, kWinLast = 2;
 
 __device__ __forceinline__ float softplus_dev(float v) { return softplus_f(v); }
 
-// bf16 row-major LDS tiles with 16-byte chunks XOR-permuted by row, so that the 32 rows a
-// fragment read touches spread over the banks
-template <int COLS> __device__ __forceinline__ int toff(int row, int col) {
-    constexpr int KC = COLS / 8;
-    static_assert(KC >= 8 && (KC & (KC - 1)) == 0, "power-of-two chunk count");
-    return row * COLS + ((((col >> 3) ^ (row & 7))) << 3) + (col & 7);
-}
+// bf16 row-major LDS tiles padded by 16 bytes per row: a fragment read of 16 consecutive rows
+// at one column covers every bank once, and each access is a per-lane base plus a constant
+constexpr int kLdS = kS + 8;   // row stride (elements) of a [rows][kS] tile
+constexpr int kLdQ = kQ + 8;   // row stride of a [rows][kQ] tile
 
 // one 32x32 MFMA tile: acc += A[rb.., k] * B[k, cb..] over k in [0, K), operands in LDS
-// tiles A[row][k] (COLS_A wide) and Bt[col][k] (COLS_B wide)
-template <int COLS_A, int COLS_B, int K>
+// tiles A[row][k] (row stride LDA) and Bt[col][k] (row stride LDB)
+template <int LDA, int LDB, int K>
 __device__ __forceinline__ void mma_tile(f32x16& acc, const bf16* A, int rb, const bf16* Bt, int cb, int lane) {
     const int r = lane & 31, hk = (lane >> 5) * 8;
 #pragma unroll
     for (int k0 = 0; k0 < K; k0 += 16) {
-        const bf16x8 a = *(const bf16x8*)&A[toff<COLS_A>(rb + r, k0 + hk)];
-        const bf16x8 b = *(const bf16x8*)&Bt[toff<COLS_B>(cb + r, k0 + hk)];
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+        const bf16x8 av = *(const bf16x8*)&A[(rb + r) * LDA + k0 + hk];
+        const bf16x8 bv = *(const bf16x8*)&Bt[(cb + r) * LDB + k0 + hk];
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
     }
 }
 
@@ -96,150 +95,230 @@ __global__ void ssd_plan_kernel(SsdArgs a) {
     if (bad) atomicOr(a.status, SSM_STATUS_BAD_SEQLENS);
 }
 
+// a plan entry is the same for the whole workgroup: keeping it in scalar registers keeps the
+// buffer resources built from it scalar
+__device__ __forceinline__ int4 uniform_plan(int4 p) {
+    return make_int4(__builtin_amdgcn_readfirstlane(p.x), __builtin_amdgcn_readfirstlane(p.y),
+                     __builtin_amdgcn_readfirstlane(p.z), __builtin_amdgcn_readfirstlane(p.w));
+}
+
 // ---------------------------------------------------------------- chunk machinery
+// Wave w of a workgroup (0..3) holds the state rows n in [64 nh, 64 nh + 64), nh = w / 2, of
+// the headdim block [pb, pb + 32), pb = 32 (w % 2), transposed, S^T[n][p], as two 32x32
+// accumulator tiles; in pass C it also owns the output tile (headdim block pb, token block
+// ib = 32 nh). A product whose contraction runs over the rows of an accumulator tile takes
+// that tile as its operand directly: entries 8s..8s+7 of lane l are the rows
+// 16s + 4 hh + {0..3} and 16s + 8 + 4 hh + {0..3} (hh = l / 32), which over both lane halves
+// are the 16 contraction indices of one K-step, each once. The other operand is read from
+// LDS in the same order, as two 8-byte pieces.
+
 struct ChunkLds {
-    bf16 Cs[kQ * kS];      // C      [i][n]
-    bf16 Bs[kQ * kS];      // B      [j][n]
-    bf16 Bt[kS * kQ];      // B^T    [n][j]
-    bf16 Xt[kP * kQ];      // X^T    [p][j]
-    bf16 Wh[kP * kQ];      // (w o X)^T high part [p][j]
-    bf16 Wl[kP * kQ];      // remainder
-    bf16 Ms[kQ * kQ];      // M      [i][j]
-    bf16 Zs[kQ * kP];      // z      [i][p]
-    bf16 Sh[kP * kS];      // state high part [p][n]
-    bf16 Sl[kP * kS];      // remainder
-    float cum[kQ], dl[kQ], rowsq[2][kQ];
+    bf16 Cs[kQ * kLdS];    // C      [i][n]
+    bf16 Bs[kQ * kLdS];    // B      [j][n]
+    bf16 Bt[kS * kLdQ];    // B^T    [n][j]
+    bf16 Xt[kP * kLdQ];    // X^T    [p][j]
+    float4 Zx[4][4][64];   // partial C S^T tile wave w hands to wave w ^ 2 (entry quad, lane)
+    float cum[kQ], dl[kQ], wq[kQ];  // in-chunk cumulative log-decay, Delta, w
 };
 
-__device__ __forceinline__ void split_bf16(float v, bf16& hi, bf16& lo) {
-    hi = (bf16)v;
-    lo = (bf16)(v - (float)hi);
+struct LocalLds {
+    bf16 Bt[kS * kLdQ];
+    bf16 Xt[kP * kLdQ];
+    float cum[kQ], dl[kQ], wq[kQ];
+};
+
+// One chunk's inputs as this thread loads them for staging: B and X with the lane as the
+// token (so that the transposing LDS writes of a wave are contiguous), C rows 16 B at a time,
+// and (threads 0..63) one token's dt. Loads go through buffer resources over the chunk's
+// valid rows, so rows past the chunk end read as zero without a branch.
+struct ChunkRegs {
+    bf16x8 b[4], c[4], x[2];
+    float dt;
+};
+
+template <bool MAIN>
+__device__ __forceinline__ void chunk_load(const SsdArgs& a, ChunkRegs& R, int h, int grp, int64_t t0, int nq) {
+    const int tid = threadIdx.x, wave = tid >> 6, j = tid & 63;
+    const __amdgpu_buffer_rsrc_t ru = buffer_rsrc(a.u + t0 * a.ld_u, (uint32_t)(nq * a.ld_u * 2));
+    const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(a.zx + t0 * a.ld_zx, (uint32_t)(nq * a.ld_zx * 2));
+    const uint32_t row = (uint32_t)(j * a.ld_u);
+#pragma unroll
+    for (int it = 0; it < 4; ++it)   // B[j][n0 .. n0 + 8), n0 = 8 (wave + 4 it)
+        R.b[it] = __builtin_bit_cast(bf16x8, buffer_load16(ru, (row + a.b_col + grp * kS + 8 * (wave + 4 * it)) * 2));
+    if constexpr (MAIN) {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {   // C rows: 16 threads per row
+            const int q = tid + kWG * it, jc = q >> 4, c8 = (q & 15) * 8;
+            R.c[it] = __builtin_bit_cast(bf16x8, buffer_load16(ru, (uint32_t)(jc * a.ld_u + a.c_col + grp * kS + c8) * 2));
+        }
+    }
+#pragma unroll
+    for (int it = 0; it < 2; ++it)   // X[j][p0 .. p0 + 8), p0 = 8 (wave + 4 it)
+        R.x[it] = __builtin_bit_cast(bf16x8, buffer_load16(ru, (row + h * kP + 8 * (wave + 4 * it)) * 2));
+    const unsigned short dv = __builtin_amdgcn_raw_buffer_load_b16(
+        rz, (int)((uint32_t)(j * a.ld_zx + a.dt_col + h) * 2), 0, 0);
+    R.dt = (float)__builtin_bit_cast(bf16, dv);
 }
 
-// Delta and the in-chunk cumulative log-decay (wave 0: one lane per token)
-__device__ __forceinline__ void chunk_decay(const SsdArgs& a, ChunkLds& L, int h, int64_t t0, int nq, float A, float bias) {
-    const int lane = threadIdx.x;
-    if (lane >= 64) return;
-    float d = 0.0f;
-    if (lane < nq) d = softplus_dev((float)a.zx[(t0 + lane) * a.ld_zx + a.dt_col + h] + bias);
-    float c = d * A;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const float o = __shfl_up(c, off, 64);
-        if (lane >= off) c += o;
-    }
-    L.dl[lane] = d;
-    L.cum[lane] = c;
-}
+// x and z of this lane's output entries (token ib + lane % 32, headdim pb + 8q + 4 hh + {0..3})
+struct EpiRegs {
+    bf16x4 x[4], z[4];
+};
 
-// stage B (both layouts) and X^T, and with the decay known the split (w o X)^T
-template <bool WITH_C>
-__device__ __forceinline__ void chunk_stage(const SsdArgs& a, ChunkLds& L, int h, int64_t t0, int nq) {
-    const int tid = threadIdx.x;
-    const int grp = (a.h_global0 + h) / a.hpg - a.g_off;
-    // B and C: 64 rows x 128 columns, 16 columns (32 B) per thread-step
-    for (int q = tid; q < kQ * (kS / 8); q += kWG) {
-        const int j = q / (kS / 8), c8 = (q % (kS / 8)) * 8;
-        bf16x8 bv = bf16x8{}, cv = bf16x8{};
-        if (j < nq) {
-            const bf16* row = a.u + (t0 + j) * a.ld_u;
-            bv = *(const bf16x8*)(row + a.b_col + grp * kS + c8);
-            if constexpr (WITH_C) cv = *(const bf16x8*)(row + a.c_col + grp * kS + c8);
-        }
-        *(bf16x8*)&L.Bs[toff<kS>(j, c8)] = bv;
-        if constexpr (WITH_C) *(bf16x8*)&L.Cs[toff<kS>(j, c8)] = cv;
+__device__ __forceinline__ void epi_load(const SsdArgs& a, EpiRegs& E, int h, int pb, int ib, int64_t t0, int nq,
+                                         int lane) {
+    const int i = ib + (lane & 31), c = h * kP + pb + 4 * (lane >> 5);
+    const __amdgpu_buffer_rsrc_t ru = buffer_rsrc(a.u + t0 * a.ld_u, (uint32_t)(nq * a.ld_u * 2));
+    const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(a.zx + t0 * a.ld_zx, (uint32_t)(nq * a.ld_zx * 2));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) L.Bt[toff<kQ>(c8 + e, j)] = bv[e];
-    }
-    const float clast = L.cum[kQ - 1];
-    for (int q = tid; q < kQ * (kP / 8); q += kWG) {
-        const int j = q / (kP / 8), p8 = (q % (kP / 8)) * 8;
-        bf16x8 xv = bf16x8{}, zv = bf16x8{};
-        if (j < nq) {
-            xv = *(const bf16x8*)(a.u + (t0 + j) * a.ld_u + h * kP + p8);
-            if constexpr (WITH_C) zv = *(const bf16x8*)(a.zx + (t0 + j) * a.ld_zx + h * kP + p8);
-        }
-        if constexpr (WITH_C) *(bf16x8*)&L.Zs[toff<kP>(j, p8)] = zv;
-        const float wj = j < nq ? __expf(clast - L.cum[j]) * L.dl[j] : 0.0f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            L.Xt[toff<kQ>(p8 + e, j)] = xv[e];
-            bf16 hi, lo;
-            split_bf16(wj * (float)xv[e], hi, lo);
-            L.Wh[toff<kQ>(p8 + e, j)] = hi;
-            L.Wl[toff<kQ>(p8 + e, j)] = lo;
-        }
+    for (int q = 0; q < 4; ++q) {
+        E.x[q] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(
+                                                ru, (int)((uint32_t)(i * a.ld_u + c + 8 * q) * 2), 0, 0));
+        E.z[q] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(
+                                                rz, (int)((uint32_t)(i * a.ld_zx + c + 8 * q) * 2), 0, 0));
     }
 }
 
-// S (this wave's two 32x32 tiles of the P x N state) <- exp(cum_last) S + (w o X)^T B
-__device__ __forceinline__ void chunk_state_update(ChunkLds& L, f32x16 (&S)[2], int wave, int lane) {
+// registers -> LDS: B^T, X^T (and B, C); wave 0 turns dt into Delta, the in-chunk cumulative
+// log-decay and w_j = exp(cum_last - cum_j) Delta_j (zero past the chunk end)
+template <bool MAIN, class LDS>
+__device__ __forceinline__ void chunk_put(LDS& L, const ChunkRegs& R, int nq, float A, float bias) {
+    const int tid = threadIdx.x, wave = tid >> 6, j = tid & 63;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int n0 = 8 * (wave + 4 * it);
+        if constexpr (MAIN) *(bf16x8*)&L.Bs[j * kLdS + n0] = R.b[it];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) L.Bt[(n0 + e) * kLdQ + j] = R.b[it][e];
+    }
+    if constexpr (MAIN) {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int q = tid + kWG * it, jc = q >> 4, c8 = (q & 15) * 8;
+            *(bf16x8*)&L.Cs[jc * kLdS + c8] = R.c[it];
+        }
+    }
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        const int p0 = 8 * (wave + 4 * it);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) L.Xt[(p0 + e) * kLdQ + j] = R.x[it][e];
+    }
+    if (tid < 64) {
+        const float d = tid < nq ? softplus_dev(R.dt + bias) : 0.0f;
+        float c = d * A;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const float o = __shfl_up(c, off, 64);
+            if (tid >= off) c += o;
+        }
+        const float clast = __shfl(c, 63, 64);
+        L.dl[tid] = d;
+        L.cum[tid] = c;
+        L.wq[tid] = __expf(clast - c) * d;
+    }
+}
+
+// operand of one K-step read from a bf16 LDS tile: row r, contraction positions
+// k0 + 4 hh + {0..3} and k0 + 8 + 4 hh + {0..3} (accumulator-row order)
+template <int LD>
+__device__ __forceinline__ bf16x8 perm_operand(const bf16* T, int r, int k0, int hh) {
+    const bf16x4 lo = *(const bf16x4*)&T[r * LD + k0 + 4 * hh];
+    const bf16x4 hi = *(const bf16x4*)&T[r * LD + k0 + 8 + 4 * hh];
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// entries 8s..8s+7 of an accumulator tile as an operand: bf16 high part and remainder
+__device__ __forceinline__ void acc_operand(const f32x16& acc, int s, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float v = acc[8 * s + e];
+        const bf16 h = (bf16)v;
+        hi[e] = h;
+        lo[e] = (bf16)(v - (float)h);
+    }
+}
+
+// S^T <- exp(cum_last) S^T + B^T (w o X) on this wave's two tiles; xa[s] is this lane's X^T
+// operand of K-step s (row pb + lane % 32); w o X enters as high part and remainder
+template <class LDS>
+__device__ __forceinline__ void state_update(const LDS& L, f32x16 (&S)[2], const bf16x8 (&xa)[4], int nh, int lane) {
+    const int r = lane & 31, hh = lane >> 5;
     const float dec = __expf(L.cum[kQ - 1]);
-    const int pb = (wave >> 1) * 32;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int nb = ((wave & 1) * 2 + t) * 32;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 16; ++i) S[t][i] *= dec;
-        mma_tile<kQ, kQ, kQ>(S[t], L.Wh, pb, L.Bt, nb, lane);
-        mma_tile<kQ, kQ, kQ>(S[t], L.Wl, pb, L.Bt, nb, lane);
-    }
-}
-
-__device__ __forceinline__ void state_to_lds(ChunkLds& L, const f32x16 (&S)[2], int wave, int lane) {
-    const int pb = (wave >> 1) * 32;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int nb = ((wave & 1) * 2 + t) * 32;
+    for (int s = 0; s < 4; ++s) {
+        const float4 w0 = *(const float4*)&L.wq[16 * s + 4 * hh];
+        const float4 w1 = *(const float4*)&L.wq[16 * s + 8 + 4 * hh];
+        const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        bf16x8 whi, wlo;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            bf16 hi, lo;
-            split_bf16(S[t][i], hi, lo);
-            const int p = acc_row(pb, i, lane), n = acc_col(nb, lane);
-            L.Sh[toff<kS>(p, n)] = hi;
-            L.Sl[toff<kS>(p, n)] = lo;
+        for (int e = 0; e < 8; ++e) {
+            const float v = wv[e] * (float)xa[s][e];
+            const bf16 h = (bf16)v;
+            whi[e] = h;
+            wlo[e] = (bf16)(v - (float)h);
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const bf16x8 bt = perm_operand<kLdQ>(L.Bt, 64 * nh + 32 * t + r, 16 * s, hh);
+            S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bt, whi, S[t], 0, 0, 0);
+            S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bt, wlo, S[t], 0, 0, 0);
         }
     }
 }
 
+// global state [P][N] fp32 <-> this wave's S^T tiles: entry 4q + b of tile t in lane l is
+// p = pb + l % 32, n = 64 nh + 32 t + 8q + 4 hh + b
 __device__ __forceinline__ void state_load(const float* src, f32x16 (&S)[2], int wave, int lane) {
-    const int pb = (wave >> 1) * 32;
+    const int p = 32 * (wave & 1) + (lane & 31), n0 = 64 * (wave >> 1) + 4 * (lane >> 5);
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int nb = ((wave & 1) * 2 + t) * 32;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) S[t][i] = src[acc_row(pb, i, lane) * kS + acc_col(nb, lane)];
-    }
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = *(const float4*)&src[p * kS + n0 + 32 * t + 8 * q];
+            S[t][4 * q] = v.x; S[t][4 * q + 1] = v.y; S[t][4 * q + 2] = v.z; S[t][4 * q + 3] = v.w;
+        }
 }
 
 __device__ __forceinline__ void state_store(float* dst, const f32x16 (&S)[2], int wave, int lane) {
-    const int pb = (wave >> 1) * 32;
+    const int p = 32 * (wave & 1) + (lane & 31), n0 = 64 * (wave >> 1) + 4 * (lane >> 5);
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int nb = ((wave & 1) * 2 + t) * 32;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) dst[acc_row(pb, i, lane) * kS + acc_col(nb, lane)] = S[t][i];
-    }
+        for (int q = 0; q < 4; ++q)
+            *(float4*)&dst[p * kS + n0 + 32 * t + 8 * q] =
+                make_float4(S[t][4 * q], S[t][4 * q + 1], S[t][4 * q + 2], S[t][4 * q + 3]);
 }
 
 // ---------------------------------------------------------------- pass A
-__global__ __launch_bounds__(kWG) void ssd_local_kernel(SsdArgs a) {
-    __shared__ ChunkLds L;
+// Chunk c is staged from registers while chunk c+1's loads are in flight.
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(4))) void ssd_local_kernel(SsdArgs a) {
+    __shared__ LocalLds L;
     const int w = blockIdx.x, h = blockIdx.y;
     if (w >= *a.plan_count) return;
-    const int4 pl = a.plan[w];
+    const int4 pl = uniform_plan(a.plan[w]);
     if (pl.w & kWinLast) return;  // the last window's state is produced by pass C
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nh = wave >> 1, pb = 32 * (wave & 1), r = lane & 31, hh = lane >> 5;
+    const int grp = (a.h_global0 + h) / a.hpg - a.g_off;
     const float A = -__expf(a.A_log[h]), bias = a.dt_bias[h];
     f32x16 S[2] = {f32x16{}, f32x16{}};
     float lsum = 0.0f;
+    ChunkRegs R;
+    chunk_load<false>(a, R, h, grp, pl.y, rows_upto(pl.z - pl.y, kQ));
     for (int64_t t0 = pl.y; t0 < pl.z; t0 += kQ) {
-        const int nq = (int)min<int64_t>(kQ, pl.z - t0);
-        chunk_decay(a, L, h, t0, nq, A, bias);
+        const int nq = rows_upto(pl.z - t0, kQ);
+        chunk_put<false>(L, R, nq, A, bias);
         __syncthreads();
-        chunk_stage<false>(a, L, h, t0, nq);
-        __syncthreads();
-        chunk_state_update(L, S, wave, lane);
+        if (t0 + kQ < pl.z) chunk_load<false>(a, R, h, grp, t0 + kQ, rows_upto(pl.z - t0 - kQ, kQ));
+        bf16x8 xa[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) xa[s] = perm_operand<kLdQ>(L.Xt, pb + r, 16 * s, hh);
+        state_update(L, S, xa, nh, lane);
         lsum += L.cum[kQ - 1];
         __syncthreads();
     }
@@ -280,77 +359,142 @@ __global__ __launch_bounds__(256) void ssd_link_kernel(SsdArgs a) {
 }
 
 // ---------------------------------------------------------------- pass C
-__global__ __launch_bounds__(kWG) void ssd_main_kernel(SsdArgs a) {
+// Per chunk, wave (nh, pb) with token block ib = 32 nh:
+//   Y^T[pb.., ib..] = X^T M^T over the causal j-blocks, M^T = (B C^T) o decay kept in registers
+//   Z^T partials  = S C^T over its own state rows, for both token blocks; the one for the
+//                   other block goes to wave w ^ 2 through LDS
+//   S^T update (its own tiles), then after one barrier: g = (Y + exp(cum_i) Z + D x) SiLU(z)
+// The next chunk's staging needs no barrier of its own: it only overwrites what all waves
+// finished reading before the second barrier.
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2))) void ssd_main_kernel(SsdArgs a) {
     __shared__ ChunkLds L;
     const int w = blockIdx.x, h = blockIdx.y;
     if (w >= *a.plan_count) return;
-    const int4 pl = a.plan[w];
+    const int4 pl = uniform_plan(a.plan[w]);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nh = wave >> 1, pb = 32 * (wave & 1), ib = 32 * nh, r = lane & 31, hh = lane >> 5;
+    const int grp = (a.h_global0 + h) / a.hpg - a.g_off;
     const float A = -__expf(a.A_log[h]), bias = a.dt_bias[h], Dh = a.D[h];
     f32x16 S[2];
     state_load(a.states + ((int64_t)w * a.H + h) * kP * kS, S, wave, lane);
-    state_to_lds(L, S, wave, lane);
-    // this wave's 32x32 tile of the chunk output Y [i][p]
-    const int rb = (wave >> 1) * 32, cb = (wave & 1) * 32;
+    ChunkRegs R;
+    EpiRegs Ep;
+    {
+        const int nq0 = rows_upto(pl.z - pl.y, kQ);
+        chunk_load<true>(a, R, h, grp, pl.y, nq0);
+        epi_load(a, Ep, h, pb, ib, pl.y, nq0, lane);
+    }
     for (int64_t t0 = pl.y; t0 < pl.z; t0 += kQ) {
-        const int nq = (int)min<int64_t>(kQ, pl.z - t0);
-        chunk_decay(a, L, h, t0, nq, A, bias);
+        const int nq = rows_upto(pl.z - t0, kQ);
+        const bool more = t0 + kQ < pl.z;
+        const int nqn = more ? rows_upto(pl.z - t0 - kQ, kQ) : 0;
+        chunk_put<true>(L, R, nq, A, bias);
         __syncthreads();
-        chunk_stage<true>(a, L, h, t0, nq);
-        __syncthreads();
-        // M = (C B^T) o decay mask, written as bf16 [i][j]
-        {
-            f32x16 G = f32x16{};
-            mma_tile<kS, kS, kS>(G, L.Cs, rb, L.Bs, cb, lane);
+        if (more) chunk_load<true>(a, R, h, grp, t0 + kQ, nqn);
+
+        const int i = ib + r;
+        const float ci = L.cum[i], eci = __expf(ci);
+        bf16x8 xa[4];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = acc_row(rb, i, lane), c = acc_col(cb, lane);
-                const float m = (c <= r && r < nq) ? G[i] * __expf(L.cum[r] - L.cum[c]) * L.dl[c] : 0.0f;
-                L.Ms[toff<kQ>(r, c)] = (bf16)m;
+        for (int s = 0; s < 4; ++s) xa[s] = perm_operand<kLdQ>(L.Xt, pb + r, 16 * s, hh);
+        // Y^T = X^T M^T, M^T[j][i] = (B_j . C_i) exp(cum_i - cum_j) Delta_j for j <= i
+        f32x16 Y = f32x16{};
+#pragma unroll
+        for (int jt = 0; jt < 2; ++jt) {
+            if (32 * jt > ib) break;
+            f32x16 G = f32x16{};
+            mma_tile<kLdS, kLdS, kS>(G, L.Bs, 32 * jt, L.Cs, ib, lane);
+            float m[16];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int j0 = 32 * jt + 8 * q + 4 * hh;
+                const float4 cj = *(const float4*)&L.cum[j0];
+                const float4 dj = *(const float4*)&L.dl[j0];
+                const float cv[4] = {cj.x, cj.y, cj.z, cj.w}, dv[4] = {dj.x, dj.y, dj.z, dj.w};
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    // branch-free: the exponent is clamped (it is <= 0 wherever j <= i) and the
+                    // causal mask selects Delta_j
+                    const float ex = __expf(fminf(ci - cv[b], 0.0f));
+                    m[4 * q + b] = G[4 * q + b] * ex * ((j0 + b <= i) ? dv[b] : 0.0f);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                bf16x8 mo;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) mo[e] = (bf16)m[8 * s + e];
+                Y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[2 * jt + s], mo, Y, 0, 0, 0);
             }
         }
-        // C S_in^T (state entering this chunk), before the barrier lets anyone overwrite Sh/Sl
-        f32x16 Z = f32x16{};
-        mma_tile<kS, kS, kS>(Z, L.Cs, rb, L.Sh, cb, lane);
-        mma_tile<kS, kS, kS>(Z, L.Cs, rb, L.Sl, cb, lane);
-        __syncthreads();
-        f32x16 Y = f32x16{};
-        mma_tile<kQ, kQ, kQ>(Y, L.Ms, rb, L.Xt, cb, lane);
-        float sq[16];
+        // Z^T partials over this wave's state rows, for token blocks 0 and 1
+        f32x16 Zp[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int r = acc_row(rb, i, lane), c = acc_col(cb, lane);
-            const float x = (float)L.Xt[toff<kQ>(c, r)];
-            const float yv = Y[i] + __expf(L.cum[r]) * Z[i] + Dh * x;
-            const bf16 gv = (bf16)(yv * silu_f((float)L.Zs[toff<kP>(r, c)]));
-            if (r < nq) a.g[(t0 + r) * a.E + h * kP + c] = gv;
-            const float gf = (float)gv;
-            sq[i] = gf * gf;
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                bf16x8 shi, slo;
+                acc_operand(S[t], s, shi, slo);
+#pragma unroll
+                for (int ix = 0; ix < 2; ++ix) {
+                    const bf16x8 cv = perm_operand<kLdS>(L.Cs, 32 * ix + r, 64 * nh + 32 * t + 16 * s, hh);
+                    Zp[ix] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(shi, cv, Zp[ix], 0, 0, 0);
+                    Zp[ix] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(slo, cv, Zp[ix], 0, 0, 0);
+                }
+            }
+        {
+            const f32x16& give = nh ? Zp[0] : Zp[1];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                L.Zx[wave][q][lane] = make_float4(give[4 * q], give[4 * q + 1], give[4 * q + 2], give[4 * q + 3]);
         }
-        // sum of g^2 over this tile's 32 columns for each of its rows, then over the two
-        // column tiles of the head
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            float v = sq[i];
-#pragma unroll
-            for (int off = 16; off >= 1; off >>= 1) v += __shfl_xor(v, off, 32);
-            sq[i] = v;
-        }
-        if ((lane & 31) == 0) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) L.rowsq[wave & 1][acc_row(rb, i, lane)] = sq[i];
-        }
-        chunk_state_update(L, S, wave, lane);
+        state_update(L, S, xa, nh, lane);
         __syncthreads();
-        if (threadIdx.x < nq) a.hs[(t0 + threadIdx.x) * a.H + h] = L.rowsq[0][threadIdx.x] + L.rowsq[1][threadIdx.x];
-        state_to_lds(L, S, wave, lane);
-        __syncthreads();
+
+        // g = (Y + exp(cum_i) Z + D x) SiLU(z) for token t0 + i, headdim pb + 8q + 4 hh + {0..3}
+        {
+            const f32x16& own = nh ? Zp[1] : Zp[0];
+            const __amdgpu_buffer_rsrc_t rg = buffer_rsrc(a.g + t0 * a.E, (uint32_t)(nq * a.E * 2));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 zo = L.Zx[wave ^ 2][q][lane];
+                const float zv[4] = {zo.x, zo.y, zo.z, zo.w};
+                bf16x4 gv;
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    const int e = 4 * q + b;
+                    const float yv = Y[e] + eci * (own[e] + zv[b]) + Dh * (float)Ep.x[q][b];
+                    gv[b] = (bf16)(yv * silu_f((float)Ep.z[q][b]));
+                }
+                __builtin_amdgcn_raw_buffer_store_b64(
+                    __builtin_bit_cast(u32x2, gv), rg,
+                    (int)((uint32_t)(i * a.E + h * kP + pb + 8 * q + 4 * hh) * 2), 0, 0);
+            }
+        }
+        if (more) epi_load(a, Ep, h, pb, ib, t0 + kQ, nqn, lane);
     }
     if (pl.w & kWinLast) {
         const int slot = a.slot[pl.x];
         if (slot >= 0 && slot < a.S) state_store(a.pool + ((int64_t)slot * a.H + h) * kP * kS, S, wave, lane);
         else if (threadIdx.x == 0) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
     }
+}
+
+// hs[t][h] = sum over the head's 64 channels of g^2: eight lanes per (token, head), each
+// reading 16 consecutive bytes of the [T][H*64] tensor, so a wave reads 1 KB contiguously
+__global__ __launch_bounds__(256) void ssd_head_sumsq_kernel(const bf16* __restrict__ g, int64_t n8,
+                                                             float* __restrict__ hs) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // 8-element piece of g
+    float s = 0.0f;
+    if (i < n8) {
+        const bf16x8 v = *(const bf16x8*)(g + i * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += (float)v[e] * (float)v[e];
+    }
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    s += __shfl_xor(s, 4, 64);
+    if (i < n8 && (i & 7) == 0) hs[i >> 3] = s;
 }
 
 // ---------------------------------------------------------------- decode
@@ -436,12 +580,11 @@ __global__ __launch_bounds__(256) void ssd_norm_kernel(const bf16* __restrict__ 
 }  // namespace
 
 int ssd_window_len(int64_t T, int H) {
-    // enough (window, head) workgroups to fill the chip a few times over
-    int64_t target = (4 * 256 + H - 1) / H;
-    int64_t win = (T + target - 1) / target;
-    int w = kQ;
-    while (w < win && w < 2048) w <<= 1;
-    return w;
+    // about 1280 (window, head) workgroups: two and a half rounds of the 512 that are
+    // resident at once (two per CU); windows are whole chunks, 64 to 2048 tokens
+    const int64_t target = (1280 + H - 1) / H;
+    const int64_t chunks = ((T + target - 1) / target + kQ - 1) / kQ;
+    return (int)std::min<int64_t>(std::max<int64_t>(chunks, 1), 2048 / kQ) * kQ;
 }
 
 int ssd_max_windows(int64_t T, int nseq, int win) { return (int)((T + win - 1) / win + nseq); }
@@ -475,6 +618,11 @@ hipError_t launch_ssd_prefill(const SsdPublic& p, hipStream_t s) {
     {
         KernelTimer kt("prefill.ssd_main", s);
         SSM_LAUNCH(ssd_main_kernel, grid, dim3(kWG), 0, s, a);
+    }
+    {
+        KernelTimer kt("prefill.ssd_head_sumsq", s);
+        const int64_t n8 = p.T * a.H * (kP / 8);
+        if (n8 > 0) SSM_LAUNCH(ssd_head_sumsq_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s, a.g, n8, a.hs);
     }
     return hipGetLastError();
 }
