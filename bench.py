@@ -490,6 +490,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
     ap.add_argument("--no-mamba2", action="store_true", help="skip the Mamba-2 (SSD) shard figures")
+    ap.add_argument("--mamba2-only", action="store_true",
+                    help="print only the Mamba-2 (SSD) shard figures (its own kernel profile; the headline step "
+                         "shares kernel names with it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
                          "to scale hardware byte counters)")
@@ -498,6 +501,13 @@ def main():
         print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported (this build runs on one GPU)",
               file=sys.stderr)
         sys.exit(2)
+    if args.mamba2_only:
+        import torch
+        from paper_2602_21144_amd import binding as B
+        B.lib()
+        torch.cuda.set_device(0)
+        print(json.dumps({"mamba2": mamba2_figures(B, torch, args.steps, args.warmup)}), flush=True)
+        return
     result, ctx = run(args)
     if args.copy_calibration:
         import torch
