@@ -29,14 +29,21 @@ def _row(m, i) -> List[float]:
     return [float(v) for v in m[i]]
 
 
+def _rms_scaled(v: Sequence[float], eps: float, weight: Optional[Sequence[float]] = None) -> List[float]:
+    ms = sum(a * a for a in v) / len(v)
+    inv = 1.0 / math.sqrt(ms + eps)
+    return [a * inv * (1.0 if weight is None else float(weight[i])) for i, a in enumerate(v)]
+
+
 def mixer_sequence(w, x_rows: Sequence[Sequence[float]], conv_hist: Optional[Sequence[Sequence[float]]] = None,
-                   h0: Optional[Sequence[Sequence[float]]] = None):
+                   h0: Optional[Sequence[Sequence[float]]] = None, bcdt_eps: Optional[float] = None):
     """Run one sequence through the full-width layer.
 
     w: dict of full-width weights (W_in [2E,dm], conv_w [E,K], conv_b [E], W_x [R+2N,E],
     W_dt [E,R], b_dt [E], A_log [E,N], D [E], W_out [dm,E]).
     x_rows: L rows of d_model values. conv_hist: [E][K-1] (oldest first) or None.
-    h0: [E][N] or None. Returns (y rows [L][dm], new conv_hist [E][K-1], h [E][N]).
+    h0: [E][N] or None. bcdt_eps: when given, delta, B and C are each divided by their
+    RMS (Falcon-Mamba) before use. Returns (y rows [L][dm], new conv_hist [E][K-1], h [E][N]).
     """
     E = len(w["conv_b"])
     K = len(w["conv_w"][0])
@@ -64,6 +71,8 @@ def mixer_sequence(w, x_rows: Sequence[Sequence[float]], conv_hist: Optional[Seq
         W = R + 2 * N
         dbl = [sum(float(w["W_x"][r][c]) * u[c] for c in range(E)) for r in range(W)]
         delta_lr, Bt, Ct = dbl[:R], dbl[R:R + N], dbl[R + N:]
+        if bcdt_eps is not None:
+            delta_lr, Bt, Ct = (_rms_scaled(delta_lr, bcdt_eps), _rms_scaled(Bt, bcdt_eps), _rms_scaled(Ct, bcdt_eps))
         y_inner = []
         for c in range(E):
             dtc = sum(float(w["W_dt"][c][r]) * delta_lr[r] for r in range(R))
@@ -76,6 +85,18 @@ def mixer_sequence(w, x_rows: Sequence[Sequence[float]], conv_hist: Optional[Seq
             y_inner.append(acc * _silu(zs[c]))
         ys.append([sum(float(w["W_out"][m][c]) * y_inner[c] for c in range(E)) for m in range(dm)])
     return ys, hist, h
+
+
+def stack_sequence(layers, norm_ws, final_w, x_rows: Sequence[Sequence[float]], eps: float,
+                   bcdt_eps: Optional[float] = None):
+    """One fresh sequence through a stack of full-width layers with pre-norm residual
+    blocks: h = RMSNorm_l(resid) * w_l, resid += mixer_l(h), output RMSNorm_final(resid)."""
+    resid = [[float(v) for v in r] for r in x_rows]
+    for w, nw in zip(layers, norm_ws):
+        h = [_rms_scaled(r, eps, nw) for r in resid]
+        ys, _, _ = mixer_sequence(w, h, bcdt_eps=bcdt_eps)
+        resid = [[a + b for a, b in zip(r, y)] for r, y in zip(resid, ys)]
+    return [_rms_scaled(r, eps, final_w) for r in resid]
 
 
 def mamba2_sequence(w, nheads: int, headdim: int, d_state: int, ngroups: int, x_rows: Sequence[Sequence[float]],

@@ -150,6 +150,23 @@ def make_general_layer(shape: LayerShape, seed: int) -> Dict[str, np.ndarray]:
     return out
 
 
+def make_stack(shape: LayerShape, n_layers: int, seed: int, general: bool = False, stress: bool = False) -> dict:
+    """Weights of a stack of mixer layers with pre-norm residual blocks: full-width layer
+    weights per layer (``make_layer`` or ``make_general_layer``, drawn one after another
+    from one generator for make_layer), then per-channel norm weights 1 + U[-0.5, 0.5]
+    (float32) for every layer and for the final norm."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    if general:
+        layers = [make_general_layer(shape, seed * 1000 + l) for l in range(n_layers)]
+    else:
+        layers = [make_layer(shape, seed, stress=stress, rng=g) for _ in range(n_layers)]
+    for w in layers:
+        w.pop("_rng", None)
+    norm_w = [(1.0 + g.uniform(-0.5, 0.5, size=shape.d_model)).astype(np.float32) for _ in range(n_layers)]
+    final_w = (1.0 + g.uniform(-0.5, 0.5, size=shape.d_model)).astype(np.float32)
+    return {"layers": layers, "norm_w": norm_w, "final_w": final_w, "_rng": g}
+
+
 def make_tokens(rng: np.random.Generator, n: int, d_model: int, act: str) -> np.ndarray:
     """``n`` token activations x ~ N(0, 1), drawn as float32 and stored in the act dtype."""
     return _store(rng.standard_normal(size=(n, d_model), dtype=np.float32), act)
