@@ -308,6 +308,62 @@ int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* desc, const ssm2_shard_wei
 int ssm2_shard_decode_stage2(const ssm2_shard_desc_t* desc, const ssm2_shard_weights_t* w, const float* sumsq,
                              int32_t batch, void* y_partial, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------ the layer around the mixer
+ * Section II-B: after out_proj the block returns to the residual stream by adding the
+ * mixer's output to the incoming hidden states. Under tensor parallelism that output is
+ * the sum over ranks of the out_proj partials (Section IV-B's second reduction), so the
+ * add follows that exchange. In front of every mixer the residual is RMS-normalised with
+ * a per-channel weight (pre-norm), and a final RMSNorm follows the last layer. The
+ * residual stream is float32. */
+
+/* residual = base + (parts[0] + ... + parts[n_parts-1]), the parts summed in float32 in
+ * that order; normed = residual / sqrt(mean over the row of residual^2 + eps) * norm_w.
+ *   base      [T][d] of base_dtype (SSM_F32 or SSM_BF16); may equal residual (in place)
+ *   parts     host array of n_parts (0..8) device pointers, each [T][d] of parts_dtype
+ *             (the ranks' out_proj partials, or one already reduced sum)
+ *   residual  [T][d] float32, written;  norm_w [d] float32;  normed [T][d] of normed_dtype
+ * Rows are contiguous. d must be a multiple of 8 and at most 8192. Device memory is the
+ * caller's; nothing else is modified. SSM_E_INVAL for bad sizes, dtypes, null pointers or
+ * a base that partially overlaps residual; SSM_E_ALIGN for pointers not 16-byte aligned. */
+int ssm_residual_rmsnorm(const void* base, int32_t base_dtype, const void* const* parts, int32_t n_parts,
+                         int32_t parts_dtype, float* residual, const float* norm_w, float eps, void* normed,
+                         int32_t normed_dtype, int64_t T, int32_t d, hipStream_t stream);
+
+/* Falcon-Mamba (Section IV-E names it as using the same selective SSM mixer; its model
+ * normalises the token-dependent fields): on the reduced x_proj output x_dbl [T][ld]
+ * float32, in place, the column ranges [0,R) (delta), [R,R+N) (B) and [R+N,R+2N) (C) are
+ * each divided by sqrt(mean of their squares + eps); no weight. It runs after the first
+ * exchange and before stage 2 (prefill or decode). SSM_E_INVAL for ld < R + 2N or eps <= 0. */
+int ssm_bcdt_rmsnorm(float* x_dbl, int64_t T, int32_t R, int32_t N, int64_t ld, float eps, hipStream_t stream);
+
+/* A stack of n_layers mixer layers at full width on one GPU (layer.shard_count == 1: both
+ * exchanges are identities; a split stack is composed from the per-layer calls and the
+ * caller's exchanges). With r_0 = x:
+ *   h = RMSNorm_l(r_l) (act dtype);  [stage 1;  Falcon-Mamba norms if bcdt_eps > 0;  stage 2]
+ *   r_{l+1} = r_l + y_l;  out = RMSNorm_final(r_L) (act dtype).
+ * layers, norm_w, conv_pools and ssm_pools are host arrays of n_layers entries holding
+ * device pointers (norm weights [d_model] float32; pools as for the one-layer calls, one
+ * pair per layer, all with num_slots slots); meta, cache slots and errors as for
+ * ssm_shard_prefill / ssm_shard_decode_step. x, x_t and out are [rows][d_model] act.
+ * The workspace queries give the size for up to max_tokens / max_batch rows. */
+typedef struct ssm_stack_desc {
+    ssm_shard_desc_t layer;   /* every layer's mixer; shard_count 1 */
+    int32_t n_layers;
+    float norm_eps;           /* RMSNorm eps, > 0 (1e-5 for the Mamba models) */
+    float bcdt_eps;           /* > 0: Falcon-Mamba's delta/B/C norms with this eps (1e-6); 0: none */
+} ssm_stack_desc_t;
+int ssm_stack_prefill_workspace_bytes(const ssm_stack_desc_t* desc, int64_t max_tokens, int32_t max_seqs,
+                                      size_t* bytes);
+int ssm_stack_decode_workspace_bytes(const ssm_stack_desc_t* desc, int32_t max_batch, size_t* bytes);
+int ssm_stack_prefill(const ssm_stack_desc_t* desc, const ssm_shard_weights_t* layers, const float* const* norm_w,
+                      const float* final_norm_w, const void* x, int64_t T, const ssm_seq_meta_t* meta,
+                      void* const* conv_pools, float* const* ssm_pools, int32_t num_slots, void* out, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+int ssm_stack_decode_step(const ssm_stack_desc_t* desc, const ssm_shard_weights_t* layers,
+                          const float* const* norm_w, const float* final_norm_w, const void* x_t, int32_t batch,
+                          const int32_t* cache_slot, void* const* conv_pools, float* const* ssm_pools,
+                          int32_t num_slots, void* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------ measurement
  * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
  * the library launches from the calling thread is launched with hipExtLaunchKernel and

@@ -101,6 +101,12 @@ _SIGS = {
     "ssm2_shard_prefill_stage2": ([_P, _P, _P, _I64, _P, _P, _SZ, _P], _I32),
     "ssm2_shard_decode_stage1": ([_P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm2_shard_decode_stage2": ([_P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_residual_rmsnorm": ([_P, _I32, _P, _I32, _I32, _P, _P, ctypes.c_float, _P, _I32, _I64, _I32, _P], _I32),
+    "ssm_bcdt_rmsnorm": ([_P, _I64, _I32, _I32, _I64, ctypes.c_float, _P], _I32),
+    "ssm_stack_prefill_workspace_bytes": ([_P, _I64, _I32, _P], _I32),
+    "ssm_stack_decode_workspace_bytes": ([_P, _I32, _P], _I32),
+    "ssm_stack_prefill": ([_P, _P, _P, _P, _P, _I64, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_stack_decode_step": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_timing_enable": ([_I32, ctypes.c_char_p], _I32),
     "ssm_timing_collect": ([_P, _I32, _P], _I32),
 }
@@ -533,3 +539,103 @@ def ssm_timing_collect(max_kernels: int = 64) -> Dict[str, tuple]:
     n = ctypes.c_int32()
     _check(lib().ssm_timing_collect(buf, max_kernels, ctypes.byref(n)))
     return {buf[i].name.decode(): (int(buf[i].launches), float(buf[i].total_ms)) for i in range(n.value)}
+
+
+# ------------------------------------------------------------------ the layer around the mixer
+class StackDesc(ctypes.Structure):
+    _fields_ = [("layer", Desc), ("n_layers", ctypes.c_int32), ("norm_eps", ctypes.c_float),
+                ("bcdt_eps", ctypes.c_float)]
+
+
+def _dtype_of(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SSM_F32
+    if t.dtype == torch.bfloat16:
+        return SSM_BF16
+    raise ValueError(f"float32 or bfloat16 tensor expected, got {t.dtype}")
+
+
+def _m_ssm_residual_rmsnorm(base, parts, residual, norm_w, eps, normed, stream=None):
+    """residual <- base + sum(parts); normed <- RMSNorm(residual) * norm_w. base, every part,
+    residual and normed are [T][d]; parts is a list (possibly empty) of same-dtype tensors."""
+    T, d = base.shape
+    pdt = _dtype_of(parts[0]) if parts else SSM_F32
+    arr = (ctypes.c_void_p * max(len(parts), 1))(*[p.data_ptr() for p in parts])
+    for p in parts:
+        _ptr(p)
+        if p.shape != base.shape or _dtype_of(p) != pdt:
+            raise ValueError("parts must match base's shape and share one dtype")
+    return (_ptr(base), _dtype_of(base), arr, len(parts), pdt, _ptr(residual), _ptr(norm_w), float(eps),
+            _ptr(normed), _dtype_of(normed), T, d, _stream(stream)), (arr,)
+
+
+def _m_ssm_bcdt_rmsnorm(x_dbl, R, N, eps, stream=None):
+    T, ld = x_dbl.shape
+    if x_dbl.dtype != torch.float32:
+        raise ValueError("x_dbl must be float32")
+    return (_ptr(x_dbl), T, int(R), int(N), ld, float(eps), _stream(stream)), ()
+
+
+def make_stack_desc(shape: LayerShape, n_layers: int, norm_eps: float = 1e-5, bcdt_eps: float = 0.0) -> StackDesc:
+    return StackDesc(make_desc(shape), n_layers, norm_eps, bcdt_eps)
+
+
+class StackWeights:
+    """Host arrays (ctypes) of a stack's per-layer weight structs and device pointers."""
+
+    def __init__(self, layers, norm_w, final_w):
+        self.structs = [_w(w) for w in layers]
+        self.layers = (Weights * len(layers))(*self.structs)
+        self.norm_w = (ctypes.c_void_p * len(norm_w))(*[_ptr(t).value for t in norm_w])
+        self.final_w = _ptr(final_w)
+        self._keep = (layers, norm_w, final_w)
+
+
+class StackPools:
+    def __init__(self, conv, ssm):
+        self.conv = (ctypes.c_void_p * len(conv))(*[_ptr(t).value for t in conv])
+        self.ssm = (ctypes.c_void_p * len(ssm))(*[_ptr(t).value for t in ssm])
+        self.S = conv[0].shape[0]
+        self._keep = (conv, ssm)
+
+
+def stack_prefill_workspace_bytes(sd: StackDesc, max_tokens: int, max_seqs: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_stack_prefill_workspace_bytes(ctypes.byref(sd), max_tokens, max_seqs, ctypes.byref(n)))
+    return n.value
+
+
+def stack_decode_workspace_bytes(sd: StackDesc, max_batch: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_stack_decode_workspace_bytes(ctypes.byref(sd), max_batch, ctypes.byref(n)))
+    return n.value
+
+
+def _m_ssm_stack_prefill(sd, sw: StackWeights, x, meta: SeqMeta, pools: StackPools, out, ws, stream=None):
+    return (ctypes.byref(sd), sw.layers, sw.norm_w, sw.final_w, _ptr(x), meta.T, ctypes.byref(meta.c), pools.conv,
+            pools.ssm, pools.S, _ptr(out), _ptr(ws), ws.numel(), _stream(stream)), (sd, sw, meta, pools)
+
+
+def _m_ssm_stack_decode_step(sd, sw: StackWeights, x_t, cache_slot, pools: StackPools, out, ws, stream=None):
+    return (ctypes.byref(sd), sw.layers, sw.norm_w, sw.final_w, _ptr(x_t), x_t.shape[0], _ptr(cache_slot),
+            pools.conv, pools.ssm, pools.S, _ptr(out), _ptr(ws), ws.numel(), _stream(stream)), (sd, sw, pools)
+
+
+_MARSHAL.update({name[3:]: fn for name, fn in list(globals().items())
+                 if name.startswith(("_m_ssm_residual", "_m_ssm_bcdt", "_m_ssm_stack"))})
+
+
+def ssm_residual_rmsnorm(base, parts, residual, norm_w, eps, normed, stream=None):
+    _call("ssm_residual_rmsnorm", base, parts, residual, norm_w, eps, normed, stream)
+
+
+def ssm_bcdt_rmsnorm(x_dbl, R, N, eps, stream=None):
+    _call("ssm_bcdt_rmsnorm", x_dbl, R, N, eps, stream)
+
+
+def ssm_stack_prefill(sd, sw, x, meta, pools, out, ws, stream=None):
+    _call("ssm_stack_prefill", sd, sw, x, meta, pools, out, ws, stream)
+
+
+def ssm_stack_decode_step(sd, sw, x_t, cache_slot, pools, out, ws, stream=None):
+    _call("ssm_stack_decode_step", sd, sw, x_t, cache_slot, pools, out, ws, stream)

@@ -918,3 +918,204 @@ int ssm2_shard_decode_stage2(const ssm2_shard_desc_t* d, const ssm2_shard_weight
 }
 
 }  // extern "C"
+
+// ================================================================ layer around the mixer
+namespace {
+
+int check_dtype(int32_t t, const char* what) {
+    if (t != SSM_F32 && t != SSM_BF16) return fail(SSM_E_INVAL, "%s dtype %d", what, t);
+    return SSM_OK;
+}
+
+int check_norm_dim(int64_t d) {
+    if (d <= 0 || d % 8 != 0 || d > residual_rmsnorm_max_dim())
+        return fail(SSM_E_INVAL, "row width %lld: a multiple of 8 up to %d", (long long)d, residual_rmsnorm_max_dim());
+    return SSM_OK;
+}
+
+int check_stack(const ssm_stack_desc_t* d, const ssm_shard_weights_t* layers, const float* const* norm_w,
+                const float* final_w) {
+    if (!d) return fail(SSM_E_INVAL, "stack desc is null");
+    SSM_TRY(check_desc(&d->layer));
+    if (d->layer.shard_count != 1)
+        return fail(SSM_E_INVAL, "a stack runs at full width (shard_count 1); split layers go through the layer calls");
+    if (d->n_layers < 1) return fail(SSM_E_INVAL, "n_layers %d", d->n_layers);
+    if (!(d->norm_eps > 0.0f)) return fail(SSM_E_INVAL, "norm_eps must be positive");
+    if (!(d->bcdt_eps >= 0.0f)) return fail(SSM_E_INVAL, "bcdt_eps must be >= 0");
+    SSM_TRY(check_norm_dim(d->layer.d_model));
+    if (!layers || !norm_w) return fail(SSM_E_INVAL, "layer arrays are null");
+    for (int l = 0; l < d->n_layers; ++l) {
+        SSM_TRY(check_weights(&layers[l]));
+        SSM_TRY(check_ptr(norm_w[l], "norm_w[l]"));
+    }
+    return check_ptr(final_w, "final_norm_w");
+}
+
+// the stack's own buffers follow the layer's workspace
+struct StackBufs {
+    float* resid;   // [T][d_model] f32
+    char* normed;   // [T][d_model] act
+    char* y;        // [T][d_model] act
+    size_t total;
+};
+
+StackBufs stack_bufs(const ssm_shard_desc_t* d, int64_t T, size_t layer_total, void* base) {
+    StackBufs S{};
+    char* b = (char*)base;
+    size_t off = layer_total;
+    auto take = [&](size_t bytes) { char* p = b ? b + off : nullptr; off += align256(bytes); return p; };
+    S.resid = (float*)take((size_t)T * d->d_model * 4);
+    S.normed = take((size_t)T * d->d_model * act_bytes(d));
+    S.y = take((size_t)T * d->d_model * act_bytes(d));
+    S.total = off;
+    return S;
+}
+
+NormParts one_part(const void* p) {
+    NormParts q{};
+    q.p[0] = p;
+    q.n = 1;
+    return q;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssm_residual_rmsnorm(const void* base, int32_t base_dtype, const void* const* parts, int32_t n_parts,
+                         int32_t parts_dtype, float* residual, const float* norm_w, float eps, void* normed,
+                         int32_t normed_dtype, int64_t T, int32_t d, hipStream_t s) {
+    SSM_TRY(check_dtype(base_dtype, "base"));
+    SSM_TRY(check_dtype(parts_dtype, "parts"));
+    SSM_TRY(check_dtype(normed_dtype, "normed"));
+    SSM_TRY(check_norm_dim(d));
+    if (T < 0 || T > INT32_MAX) return fail(SSM_E_INVAL, "rows %lld", (long long)T);
+    if (n_parts < 0 || n_parts > kMaxNormParts) return fail(SSM_E_INVAL, "n_parts %d (0..%d)", n_parts, kMaxNormParts);
+    if (!(eps > 0.0f)) return fail(SSM_E_INVAL, "eps must be positive");
+    if (T == 0) return SSM_OK;
+    SSM_TRY(check_ptr(base, "base"));
+    SSM_TRY(check_ptr(residual, "residual"));
+    SSM_TRY(check_ptr(norm_w, "norm_w"));
+    SSM_TRY(check_ptr(normed, "normed"));
+    NormParts q{};
+    q.n = n_parts;
+    if (n_parts > 0 && !parts) return fail(SSM_E_INVAL, "parts is null");
+    for (int k = 0; k < n_parts; ++k) {
+        SSM_TRY(check_ptr(parts[k], "parts[k]"));
+        q.p[k] = parts[k];
+    }
+    if (base != residual && base_dtype == SSM_F32) {
+        // distinct buffers must not overlap partially
+        const char *b0 = (const char*)base, *r0 = (const char*)residual;
+        const size_t n = (size_t)T * d * 4;
+        if (b0 < r0 + n && r0 < b0 + n) return fail(SSM_E_INVAL, "base and residual overlap without being equal");
+    }
+    SSM_TIMED("layer.residual_rmsnorm", s,
+              launch_residual_rmsnorm(base, base_dtype == SSM_BF16, q, parts_dtype == SSM_BF16, residual, norm_w, eps,
+                                      normed, normed_dtype == SSM_BF16, T, d, s));
+    return SSM_OK;
+}
+
+int ssm_bcdt_rmsnorm(float* x_dbl, int64_t T, int32_t R, int32_t N, int64_t ld, float eps, hipStream_t s) {
+    if (T < 0 || R < 1 || N < 1 || ld < (int64_t)R + 2 * N) return fail(SSM_E_INVAL, "bcdt shape");
+    if (!(eps > 0.0f)) return fail(SSM_E_INVAL, "eps must be positive");
+    if (T == 0) return SSM_OK;
+    if (!x_dbl) return fail(SSM_E_INVAL, "x_dbl is null");
+    if (((uintptr_t)x_dbl & 3) != 0) return fail(SSM_E_ALIGN, "x_dbl is not 4-byte aligned");
+    SSM_TIMED("layer.bcdt_rms", s, launch_bcdt_rms(x_dbl, T, R, N, ld, eps, s));
+    return SSM_OK;
+}
+
+int ssm_stack_prefill_workspace_bytes(const ssm_stack_desc_t* desc, int64_t max_tokens, int32_t max_seqs,
+                                      size_t* bytes) {
+    if (!desc) return fail(SSM_E_INVAL, "stack desc is null");
+    SSM_TRY(check_desc(&desc->layer));
+    if (!bytes || max_tokens < 0 || max_tokens > INT32_MAX || max_seqs < 0) return fail(SSM_E_INVAL, "bad size query");
+    const size_t lt = prefill_layout(&desc->layer, max_tokens, max_seqs, nullptr).total;
+    *bytes = stack_bufs(&desc->layer, max_tokens, lt, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm_stack_decode_workspace_bytes(const ssm_stack_desc_t* desc, int32_t max_batch, size_t* bytes) {
+    if (!desc) return fail(SSM_E_INVAL, "stack desc is null");
+    SSM_TRY(check_desc(&desc->layer));
+    if (!bytes || max_batch < 0) return fail(SSM_E_INVAL, "bad size query");
+    const size_t lt = decode_layout(&desc->layer, max_batch, nullptr).total;
+    *bytes = stack_bufs(&desc->layer, max_batch, lt, nullptr).total;
+    return SSM_OK;
+}
+
+int ssm_stack_prefill(const ssm_stack_desc_t* sd, const ssm_shard_weights_t* layers, const float* const* norm_w,
+                      const float* final_w, const void* x, int64_t T, const ssm_seq_meta_t* m,
+                      void* const* conv_pools, float* const* ssm_pools, int32_t S, void* out, void* ws,
+                      size_t ws_bytes, hipStream_t s) {
+    SSM_TRY(check_stack(sd, layers, norm_w, final_w));
+    const ssm_shard_desc_t* d = &sd->layer;
+    PrefillWs L;
+    SSM_TRY(prefill_checks(d, &layers[0], T, m, S, ws, ws_bytes, &L));
+    const StackBufs B = stack_bufs(d, T, L.total, ws);
+    SSM_TRY(check_ws(ws, ws_bytes, B.total));
+    if (!conv_pools || !ssm_pools) return fail(SSM_E_INVAL, "pool arrays are null");
+    for (int l = 0; l < sd->n_layers; ++l) {
+        SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
+        SSM_TRY(check_ptr(ssm_pools[l], "ssm_pools[l]"));
+    }
+    if (T > 0) {
+        SSM_TRY(check_ptr(x, "x"));
+        SSM_TRY(check_ptr(out, "out"));
+    }
+    const bool bf = d->act_dtype == SSM_BF16;
+    const int dm = d->d_model, R = d->dt_rank, N = d->d_state, W = R + 2 * N;
+    const float eps = sd->norm_eps;
+    NormParts none{};
+    SSM_TIMED("layer.residual_rmsnorm", s,
+              launch_residual_rmsnorm(x, bf, none, bf, B.resid, norm_w[0], eps, B.normed, bf, T, dm, s));
+    for (int l = 0; l < sd->n_layers; ++l) {
+        SSM_TRY(prefill1(d, &layers[l], B.normed, T, m, conv_pools[l], S, L.xdbl, L, s));
+        if (sd->bcdt_eps > 0.0f) SSM_TIMED("layer.bcdt_rms", s, launch_bcdt_rms(L.xdbl, T, R, N, W, sd->bcdt_eps, s));
+        SSM_TRY(prefill2(d, &layers[l], L.xdbl, T, m, ssm_pools[l], S, B.y, L, s));
+        const bool last = l + 1 == sd->n_layers;
+        SSM_TIMED("layer.residual_rmsnorm", s,
+                  launch_residual_rmsnorm(B.resid, false, one_part(B.y), bf, B.resid, last ? final_w : norm_w[l + 1],
+                                          eps, last ? out : B.normed, bf, T, dm, s));
+    }
+    return SSM_OK;
+}
+
+int ssm_stack_decode_step(const ssm_stack_desc_t* sd, const ssm_shard_weights_t* layers, const float* const* norm_w,
+                          const float* final_w, const void* x, int32_t Bsz, const int32_t* slot,
+                          void* const* conv_pools, float* const* ssm_pools, int32_t S, void* out, void* ws,
+                          size_t ws_bytes, hipStream_t s) {
+    SSM_TRY(check_stack(sd, layers, norm_w, final_w));
+    const ssm_shard_desc_t* d = &sd->layer;
+    DecodeWs L;
+    SSM_TRY(decode_checks(d, &layers[0], Bsz, slot, S, ws, ws_bytes, &L));
+    const StackBufs B = stack_bufs(d, Bsz, L.total, ws);
+    SSM_TRY(check_ws(ws, ws_bytes, B.total));
+    if (!conv_pools || !ssm_pools) return fail(SSM_E_INVAL, "pool arrays are null");
+    for (int l = 0; l < sd->n_layers; ++l) {
+        SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
+        SSM_TRY(check_ptr(ssm_pools[l], "ssm_pools[l]"));
+    }
+    if (Bsz == 0) return SSM_OK;
+    SSM_TRY(check_ptr(x, "x_t"));
+    SSM_TRY(check_ptr(out, "out"));
+    const bool bf = d->act_dtype == SSM_BF16;
+    const int dm = d->d_model, R = d->dt_rank, N = d->d_state, W = R + 2 * N;
+    const float eps = sd->norm_eps;
+    NormParts none{};
+    SSM_TIMED("layer.residual_rmsnorm", s,
+              launch_residual_rmsnorm(x, bf, none, bf, B.resid, norm_w[0], eps, B.normed, bf, Bsz, dm, s));
+    for (int l = 0; l < sd->n_layers; ++l) {
+        SSM_TRY(decode1(d, &layers[l], B.normed, Bsz, slot, conv_pools[l], S, L.xdbl, L, s));
+        if (sd->bcdt_eps > 0.0f) SSM_TIMED("layer.bcdt_rms", s, launch_bcdt_rms(L.xdbl, Bsz, R, N, W, sd->bcdt_eps, s));
+        SSM_TRY(decode2(d, &layers[l], L.xdbl, Bsz, slot, ssm_pools[l], S, B.y, L, s));
+        const bool last = l + 1 == sd->n_layers;
+        SSM_TIMED("layer.residual_rmsnorm", s,
+                  launch_residual_rmsnorm(B.resid, false, one_part(B.y), bf, B.resid, last ? final_w : norm_w[l + 1],
+                                          eps, last ? out : B.normed, bf, Bsz, dm, s));
+    }
+    return SSM_OK;
+}
+
+}  // extern "C"

@@ -187,4 +187,16 @@ hipError_t launch_reduce_add(float* dst, const float* src, int64_t n, hipStream_
 hipError_t launch_copy_rows(void* dst, int64_t ld_dst, const void* src, int64_t ld_src,
                             int64_t rows, int64_t row_bytes, hipStream_t s);
 
+// ---------------------------------------------------------------- layer (layer.hip)
+constexpr int kMaxNormParts = 8;
+struct NormParts {
+    const void* p[kMaxNormParts];   // partial outputs added to the residual, in this order
+    int n;
+};
+int residual_rmsnorm_max_dim();
+hipError_t launch_residual_rmsnorm(const void* base, bool base_bf16, const NormParts& parts, bool parts_bf16,
+                                   float* resid, const float* w, float eps, void* out, bool out_bf16, int64_t T, int d,
+                                   hipStream_t s);
+hipError_t launch_bcdt_rms(float* x, int64_t T, int R, int N, int64_t ld, float eps, hipStream_t s);
+
 }  // namespace ssm

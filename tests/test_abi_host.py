@@ -145,3 +145,44 @@ def test_exchange_codec_host_checks(B):
     assert L.ssm_exchange_decode_accumulate(3, fake, 100, 4, 8, fake, 8, 0, None) == -3
     assert L.ssm_exchange_decode_accumulate(3, fake, 4096, 4, 8, None, 8, 0, None) == -1
     assert L.ssm_exchange_encode(1, fake, 0, 0, 8, 8, None, 0, None) == 0         # empty: nothing to do
+
+
+def test_layer_and_stack_host_checks(B):
+    """The residual norm, the Falcon-Mamba norms and the stack calls reject bad arguments
+    before any launch; workspace sizes cover the layer's and the stack's buffers."""
+    L = B.lib()
+    fake = 1 << 20   # never dereferenced: every call below fails its host checks first
+    f = ctypes.c_void_p(fake)
+    parts = (ctypes.c_void_p * 2)(fake, fake + (1 << 24))
+    norm = lambda base, bdt, n, pdt, res, d, T=4, eps=1e-5, odt=1: L.ssm_residual_rmsnorm(
+        ctypes.c_void_p(base), bdt, parts, n, pdt, ctypes.c_void_p(res), f, ctypes.c_float(eps), f, odt, T, d, None)
+    assert norm(fake, 0, 1, 1, fake, 12) == -1                 # d not a multiple of 8
+    assert norm(fake, 0, 1, 1, fake, 8200) == -1               # d above 8192
+    assert norm(fake, 0, 9, 1, fake, 16) == -1                 # more than 8 parts
+    assert norm(fake, 3, 1, 1, fake, 16) == -1                 # bad base dtype
+    assert norm(fake, 0, 1, 1, fake, 16, eps=0.0) == -1        # eps must be positive
+    assert norm(fake, 0, 1, 1, fake + 64, 16) == -1            # base overlaps residual partially
+    assert norm(fake + 4, 0, 1, 1, fake + 4096, 16) == -2      # misaligned base
+    assert norm(fake, 0, 1, 1, fake, 16, T=0) == 0             # no rows: nothing to do
+    assert L.ssm_bcdt_rmsnorm(f, 10, 8, 4, 15, ctypes.c_float(1e-6), None) == -1   # ld < R + 2N
+    assert L.ssm_bcdt_rmsnorm(f, 10, 8, 4, 16, ctypes.c_float(0.0), None) == -1    # eps
+    assert L.ssm_bcdt_rmsnorm(None, 10, 8, 4, 16, ctypes.c_float(1e-6), None) == -1
+    d1 = _desc(B, d_inner_shard=5120, shard_count=1)
+    sd = B.StackDesc(d1, 2, 1e-5, 0.0)
+    n1, n2 = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.ssm_stack_prefill_workspace_bytes(ctypes.byref(sd), 1000, 2, ctypes.byref(n1)) == 0
+    assert n1.value >= B.prefill_workspace_bytes(d1, 1000, 2) + 1000 * 2560 * 8
+    assert L.ssm_stack_decode_workspace_bytes(ctypes.byref(sd), 8, ctypes.byref(n2)) == 0
+    w = (B.Weights * 2)(*[B.Weights(*([fake] * 9)) for _ in range(2)])
+    nw = (ctypes.c_void_p * 2)(fake, fake)
+    pools = (ctypes.c_void_p * 2)(fake, fake)
+    meta = B.SeqMetaC(fake, fake, fake, 1)
+    call = lambda sdesc, ws_bytes: L.ssm_stack_prefill(ctypes.byref(sdesc), w, nw, f, f, 100, ctypes.byref(meta),
+                                                       pools, pools, 4, f, f, ws_bytes, None)
+    assert call(B.StackDesc(_desc(B), 2, 1e-5, 0.0), 1 << 40) == -1         # split layers: not a stack
+    assert call(B.StackDesc(d1, 0, 1e-5, 0.0), 1 << 40) == -1               # no layers
+    assert call(B.StackDesc(d1, 2, 0.0, 0.0), 1 << 40) == -1                # norm eps
+    assert call(B.StackDesc(d1, 2, 1e-5, -1.0), 1 << 40) == -1              # bcdt eps
+    need = ctypes.c_size_t()
+    L.ssm_stack_prefill_workspace_bytes(ctypes.byref(sd), 100, 1, ctypes.byref(need))
+    assert call(sd, need.value - 1) == -3                                   # workspace too small
