@@ -293,6 +293,9 @@ def run(args):
     if not args.no_mamba2:
         log("Mamba-2 (SSD) shard on its workload (outside the timed region)")
         result["mamba2"] = mamba2_figures(B, torch, args.steps, args.warmup)
+    if not args.no_ablation:
+        log("cache vs no-cache generation through a 64-layer stack (outside the timed region)")
+        result["ablation"] = ablation_figures(B, torch)
     return result, (sh, full, x_host, xdec_host, slots, S)
 
 
@@ -393,6 +396,101 @@ def mamba2_figures(B, torch, steps, warmup):
             "kernels": kernels}
 
 
+def device_stack_weights(torch, sh, n_layers, seed, dev):
+    """Seeded synthetic weights of a full-width stack drawn on the GPU (torch's Philox
+    generator; drawing ~5 GB of normals on the host would dominate the run). The recipe is
+    the one-layer recipe: matrices and conv ~N(0, 0.02) in bf16, dt0 log-uniform in
+    [1e-3, 0.1] with b_dt = softplus^-1(dt0), A_log[c, n] = log(n + 1), D = 1; norm weights 1."""
+    import math
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    E, dm, N, R, K = sh.d_inner, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv
+
+    def nrm(*size):
+        return (torch.randn(*size, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+
+    a_log = torch.log(torch.arange(1, N + 1, device=dev, dtype=torch.float32)).repeat(E, 1).contiguous()
+    layers = []
+    for _ in range(n_layers):
+        lo, hi = math.log(1e-3), math.log(0.1)
+        dt0 = torch.exp(torch.rand(E, generator=g, device=dev) * (hi - lo) + lo)
+        layers.append({"W_in": nrm(2 * E, dm), "conv_w": nrm(E, K), "conv_b": nrm(E), "W_x": nrm(R + 2 * N, E),
+                       "W_dt": nrm(E, R), "W_out": nrm(dm, E), "b_dt": (dt0 + torch.log(-torch.expm1(-dt0))).float(),
+                       "A_log": a_log.clone(), "D": torch.ones(E, device=dev)})
+    return layers, [torch.ones(dm, device=dev) for _ in range(n_layers)], torch.ones(dm, device=dev), g
+
+
+def ablation_figures(B, torch, n_layers=64, prompt=256, generated=256):
+    """Section V's ablation at kernel level on one GPU: per-token latency of generating
+    `generated` tokens after a `prompt`-token prompt through a Mamba-2.8B-shaped stack at
+    full width, batch 1, with the SSM cache (prefill of the prompt, then one decode step per
+    token) and without it (the prompt, then a prefill of the whole prefix for every token).
+    Inputs are seeded synthetic rows, not fed back (one stack, no LM head)."""
+    import numpy as np
+    from paper_2602_21144_amd import synth
+    dev = "cuda"
+    sh = synth.LayerShape(2560, 5120, 16, 160, 4, 1, "bf16")
+    layers, norm_w, final_w, g = device_stack_weights(torch, sh, n_layers, 21, dev)
+    sd = B.make_stack_desc(sh, n_layers)
+    sw = B.StackWeights(layers, norm_w, final_w)
+    conv = [torch.zeros(1, sh.d_inner, sh.d_conv - 1, dtype=torch.bfloat16, device=dev) for _ in range(n_layers)]
+    ssm = [torch.zeros(1, sh.d_inner, sh.d_state, dtype=torch.float32, device=dev) for _ in range(n_layers)]
+    pools = B.StackPools(conv, ssm)
+    n = prompt + generated
+    x = torch.randn(n, sh.d_model, generator=g, device=dev).to(torch.bfloat16)
+    ws_p = B.workspace(B.stack_prefill_workspace_bytes(sd, n, 1), dev)
+    ws_d = B.workspace(B.stack_decode_workspace_bytes(sd, 1), dev)
+    out_p = torch.empty(n, sh.d_model, dtype=torch.bfloat16, device=dev)
+    out_d = torch.empty(1, sh.d_model, dtype=torch.bfloat16, device=dev)
+    slot = torch.zeros(1, dtype=torch.int32, device=dev)
+    metas = {L: B.SeqMeta([0, L], [0], [0], 1, dev) for L in range(prompt, n + 1)}
+    prefills = {L: B.bind("ssm_stack_prefill", sd, sw, x[:L], metas[L], pools, out_p[:L], ws_p) for L in metas}
+    decodes = [B.bind("ssm_stack_decode_step", sd, sw, x[prompt + t:prompt + t + 1], slot, pools, out_d, ws_d)
+               for t in range(generated)]
+
+    def cached():
+        prefills[prompt]()
+        for c in decodes:
+            c()
+
+    def no_cache():
+        prefills[prompt]()
+        for L in range(prompt + 1, n + 1):
+            prefills[L]()
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    for L in (prompt, n):            # warm up both paths
+        prefills[L]()
+    decodes[0]()
+    t_cache = timed(cached)
+    last_cached = out_d.float().clone()
+    t_pref = timed(lambda: prefills[prompt]())
+    t_nocache = timed(no_cache)
+    last_nocache = out_p[n - 1:n].float()
+    assert B.take_status(ws_p) == 0 and B.take_status(ws_d) == 0
+    diff = float((last_cached - last_nocache).abs().max() / last_nocache.abs().max())
+    del layers, sw, conv, ssm, pools, ws_p, ws_d
+    torch.cuda.empty_cache()
+    return {"workload": f"Mamba-2.8B-shaped stack of {n_layers} layers at full width (d_model 2560, d_inner 5120, "
+                        f"d_state 16, dt_rank 160, d_conv 4; pre-norm RMSNorm, fp32 residual), batch 1, "
+                        f"{prompt}-token prompt then {generated} generated tokens; bf16; seeded synthetic weights "
+                        f"and inputs",
+            "cache_ms_per_token": round(t_cache / generated, 4),
+            "no_cache_ms_per_token": round(t_nocache / generated, 4),
+            "speedup": round(t_nocache / t_cache, 2),
+            "prompt_prefill_ms": round(t_pref, 4),
+            "decode_step_ms": round((t_cache - t_pref) / generated, 4),
+            "last_token_rel_diff_cache_vs_no_cache": round(diff, 5)}
+
+
 def codec_figures(B, torch, tensors):
     """Section IV-D exchange codecs on real partials of the two exchange points: encode and
     decode-accumulate device time (per-dispatch events), algorithmic GB/s, payload bytes,
@@ -490,6 +588,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
     ap.add_argument("--no-mamba2", action="store_true", help="skip the Mamba-2 (SSD) shard figures")
+    ap.add_argument("--no-ablation", action="store_true", help="skip the cache vs no-cache generation figures")
     ap.add_argument("--mamba2-only", action="store_true",
                     help="print only the Mamba-2 (SSD) shard figures (its own kernel profile; the headline step "
                          "shares kernel names with it)")
