@@ -224,6 +224,17 @@ int ssm_exchange_decode_accumulate(int32_t codec, const void* payload, size_t pa
 int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t a_dtype,
                 const void* B, int64_t ldb, int32_t b_dtype, void* C, int64_t ldc, int32_t c_dtype,
                 hipStream_t stream);
+/* The same product on the kernel instance and tile policy of one projection (role: 0
+ * generic, 1 in_proj, 2 x_proj, 3 dt_proj, 4 out_proj), as the prefill runs it. Outputs
+ * with fewer tiles than the GPU has compute units and a long K are computed split-K: the
+ * K-slices' float32 partials go to scratch (device, the caller's; ssm_gemm_splitk_bytes
+ * gives its size, 0 when the shape is not split) and a second kernel adds them in slice
+ * order. With less scratch than that (or none) the product runs unsplit. */
+int ssm_gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int32_t a_dtype, int32_t b_dtype, int32_t role,
+                          size_t* bytes);
+int ssm_gemm_nt_role(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t a_dtype, const void* B,
+                     int64_t ldb, int32_t b_dtype, void* C, int64_t ldc, int32_t c_dtype, int32_t role,
+                     float* scratch, size_t scratch_bytes, hipStream_t stream);
 /* Causal depthwise conv1d + SiLU over a packed batch: reads the SSM half of
  * xz [T][2E] (columns 0..E-1), writes u [T][E] act and the new conv history. */
 int ssm_conv1d_silu(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w, const void* xz,

@@ -86,6 +86,8 @@ _SIGS = {
     "ssm_shard_slice_weights": ([_P, _P, _P, _P], _I32),
     "ssm_reduce_add_f32": ([_P, _P, _I64, _P], _I32),
     "ssm_gemm_nt": ([_I64, _I64, _I64, _P, _I64, _I32, _P, _I64, _I32, _P, _I64, _I32, _P], _I32),
+    "ssm_gemm_splitk_bytes": ([_I64, _I64, _I64, _I32, _I32, _I32, _P], _I32),
+    "ssm_gemm_nt_role": ([_I64, _I64, _I64, _P, _I64, _I32, _P, _I64, _I32, _P, _I64, _I32, _I32, _P, _SZ, _P], _I32),
     "ssm_conv1d_silu": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_selective_scan": ([_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_decode_conv": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
@@ -496,6 +498,29 @@ def ssm_gemm_nt(A, B, C, stream=None):
     _check(lib().ssm_gemm_nt(M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0), _dt(A),
                              ctypes.c_void_p(B.data_ptr()), B.stride(0), _dt(B), ctypes.c_void_p(C.data_ptr()),
                              C.stride(0), _dt(C), _stream(stream)))
+
+
+GEMM_ROLE = {"generic": 0, "in_proj": 1, "x_proj": 2, "dt_proj": 3, "out_proj": 4}
+
+
+def gemm_splitk_bytes(M, N, K, a_dtype, b_dtype, role: str) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().ssm_gemm_splitk_bytes(M, N, K, a_dtype, b_dtype, GEMM_ROLE[role], ctypes.byref(n)))
+    return n.value
+
+
+def ssm_gemm_nt_role(A, B, C, role: str, scratch: Optional[torch.Tensor] = None, stream=None):
+    """ssm_gemm_nt on one projection's kernel path, split-K into scratch when it fits."""
+    M, K = A.shape
+    N = B.shape[0]
+    assert B.shape[1] == K and C.shape == (M, N)
+    for t in (A, B, C):
+        assert t.stride(1) == 1
+    sp = ctypes.c_void_p(scratch.data_ptr()) if scratch is not None else None
+    nb = scratch.numel() * scratch.element_size() if scratch is not None else 0
+    _check(lib().ssm_gemm_nt_role(M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0), _dt(A),
+                                  ctypes.c_void_p(B.data_ptr()), B.stride(0), _dt(B), ctypes.c_void_p(C.data_ptr()),
+                                  C.stride(0), _dt(C), GEMM_ROLE[role], sp, nb, _stream(stream)))
 
 
 def ssm_conv1d_silu(desc, weights, xz, meta: SeqMeta, conv_pool, u, ws, stream=None):

@@ -6,6 +6,7 @@
 //   [first reduction over shards: the caller's]
 //   stage 2: dt_proj GEMM -> dt; selective scan -> g (and the final states); out_proj GEMM -> y
 // Decode: the same with one token per sequence and the single-step kernels.
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -96,12 +97,19 @@ int check_meta(const ssm_seq_meta_t* m, int64_t T) {
 }
 
 // ------------------------------------------------------------------ workspaces
+// fp32 partials of the projections that run split-K (few tokens)
+struct Scratch {
+    float* p = nullptr;
+    size_t bytes = 0;
+};
+
 struct PrefillWs {
     int32_t* status;
     char *xz, *u, *dt, *g;
     char* delta16;  // [T][R] bf16: delta rounded for dt_proj (bf16 activations)
     float* xdbl;
     char* scan;
+    Scratch splitk;  // fp32 partials of the projections that run split-K (few tokens)
     size_t total;
 };
 
@@ -120,6 +128,14 @@ PrefillWs prefill_layout(const ssm_shard_desc_t* d, int64_t T, int nseq, void* b
     L.g = take((size_t)T * E * s);
     L.delta16 = take(d->act_dtype == SSM_BF16 ? (size_t)T * d->dt_rank * 2 : 0);
     L.scan = take(scan_scratch_bytes(T, (int)E, nseq));
+    const int adt = d->act_dtype;
+    const int64_t dm = d->d_model, R = d->dt_rank;
+    size_t sk = gemm_splitk_bytes(T, 2 * E, dm, adt, adt, kGemmInProj);
+    sk = std::max(sk, gemm_splitk_bytes(T, W, E, adt, adt, kGemmXProj));
+    sk = std::max(sk, gemm_splitk_bytes(T, E, R, adt, adt, kGemmDtProj));
+    sk = std::max(sk, gemm_splitk_bytes(T, dm, E, adt, adt, kGemmOutProj));
+    L.splitk.p = (float*)take(sk);
+    L.splitk.bytes = sk;
     L.total = off;
     return L;
 }
@@ -156,9 +172,10 @@ int check_ws(void* ws, size_t have, size_t need) {
 }
 
 int gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int adt, const void* B, int64_t ldb, int bdt,
-         void* C, int64_t ldc, int cdt, hipStream_t s, const char* what, GemmRole role = kGemmGeneric) {
+         void* C, int64_t ldc, int cdt, hipStream_t s, const char* what, GemmRole role = kGemmGeneric,
+         Scratch sk = Scratch{}) {
     KernelTimer kt(what, s);
-    SSM_TRY_HIP(launch_gemm_nt(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, role), what);
+    SSM_TRY_HIP(launch_gemm_nt(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, role, sk.p, sk.bytes), what);
     return SSM_OK;
 }
 
@@ -209,12 +226,12 @@ int prefill1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void
              const ssm_seq_meta_t* m, void* conv_pool, int32_t S, float* xdbl, const PrefillWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    SSM_TRY(gemm(T, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "prefill.in_proj", kGemmInProj));
+    SSM_TRY(gemm(T, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "prefill.in_proj", kGemmInProj, L.splitk));
     ConvArgs ca = conv_args(d, w, L.xz, T, m->cu_seqlens, m->cache_slot, m->has_initial_state, m->nseq, conv_pool,
                             S, L.u, L.status);
     SSM_TIMED("prefill.conv1d", s, launch_conv_prefill(ca, adt == SSM_BF16, s));
     SSM_TIMED("prefill.conv_history", s, launch_conv_state_update(ca, adt == SSM_BF16, s));
-    SSM_TRY(gemm(T, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "prefill.x_proj", kGemmXProj));
+    SSM_TRY(gemm(T, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "prefill.x_proj", kGemmXProj, L.splitk));
     return SSM_OK;
 }
 
@@ -225,14 +242,14 @@ int prefill2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const floa
     if (adt == SSM_BF16 && R % 32 == 0 && T > 64) {
         // delta is rounded to bf16 once, so dt_proj runs on the DMA-fed bf16 tiles
         SSM_TIMED("prefill.dt_round", s, launch_round_bf16_rows(xdbl, W, L.delta16, T, (int)R, s));
-        SSM_TRY(gemm(T, E, R, L.delta16, R, adt, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
+        SSM_TRY(gemm(T, E, R, L.delta16, R, adt, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj, L.splitk));
     } else {
-        SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj));
+        SSM_TRY(gemm(T, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "prefill.dt_proj", kGemmDtProj, L.splitk));
     }
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, T, m->cu_seqlens, m->cache_slot, m->has_initial_state,
                             m->nseq, ssm_pool, S, L.g, L.status, L.scan);
     SSM_TRY_HIP(launch_scan_prefill(sa, adt == SSM_BF16, s), "selective scan");
-    SSM_TRY(gemm(T, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "prefill.out_proj", kGemmOutProj));
+    SSM_TRY(gemm(T, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "prefill.out_proj", kGemmOutProj, L.splitk));
     return SSM_OK;
 }
 
@@ -562,6 +579,36 @@ int ssm_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int
     return gemm(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, "op.gemm");
 }
 
+int ssm_gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int32_t adt, int32_t bdt, int32_t role, size_t* bytes) {
+    if (!bytes || M < 0 || N < 0 || K < 0 || role < kGemmGeneric || role > kGemmOutProj)
+        return fail(SSM_E_INVAL, "bad split-K size query");
+    *bytes = gemm_splitk_bytes(M, N, K, adt, bdt, (GemmRole)role);
+    return SSM_OK;
+}
+
+int ssm_gemm_nt_role(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int32_t adt, const void* B,
+                     int64_t ldb, int32_t bdt, void* C, int64_t ldc, int32_t cdt, int32_t role, float* scratch,
+                     size_t scratch_bytes, hipStream_t s) {
+    if (role < kGemmGeneric || role > kGemmOutProj) return fail(SSM_E_INVAL, "gemm role %d", role);
+    if (scratch_bytes > 0) SSM_TRY(check_ptr(scratch, "scratch"));
+    if (M < 0 || N < 0 || K < 0 || M > INT32_MAX || N > INT32_MAX || K > INT32_MAX)
+        return fail(SSM_E_INVAL, "gemm size %lld x %lld x %lld", (long long)M, (long long)N, (long long)K);
+    for (int32_t dt : {adt, bdt, cdt})
+        if (dt != SSM_F32 && dt != SSM_BF16) return fail(SSM_E_INVAL, "dtype %d", dt);
+    if (bdt == SSM_F32 && (adt != SSM_F32 || cdt != SSM_F32))
+        return fail(SSM_E_INVAL, "float32 B needs float32 A and C");
+    if (M == 0 || N == 0) return SSM_OK;
+    if (K % 8 || lda % 8 || ldb % 8 || ldc % 4) return fail(SSM_E_ALIGN, "K, lda, ldb must be multiples of 8, ldc of 4");
+    if (lda < K || ldb < K || ldc < N) return fail(SSM_E_INVAL, "leading dimension smaller than the row");
+    SSM_TRY(check_ptr(A, "A"));
+    SSM_TRY(check_ptr(B, "B"));
+    SSM_TRY(check_ptr(C, "C"));
+    Scratch sk;
+    sk.p = scratch;
+    sk.bytes = scratch ? scratch_bytes : 0;
+    return gemm(M, N, K, A, lda, adt, B, ldb, bdt, C, ldc, cdt, s, "op.gemm", (GemmRole)role, sk);
+}
+
 int ssm_conv1d_silu(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* xz, int64_t T,
                     const ssm_seq_meta_t* m, void* conv_pool, int32_t S, void* u, void* ws, size_t ws_bytes,
                     hipStream_t s) {
@@ -699,6 +746,7 @@ struct M2Ws {
     int32_t* count;
     float *states, *lsum;
     int win, maxw;
+    Scratch splitk;
     size_t total;
 };
 
@@ -721,6 +769,10 @@ M2Ws m2_layout(const M2& m, int64_t T, int nseq, bool prefill, void* base) {
         L.states = (float*)take(ssd_state_bytes(L.maxw, (int)m.H));
         L.lsum = (float*)take((size_t)L.maxw * m.H * 4);
     }
+    const size_t sk = std::max(gemm_splitk_bytes(T, m.rows, m.dm, SSM_BF16, SSM_BF16, kGemmInProj),
+                               gemm_splitk_bytes(T, m.dm, m.E, SSM_BF16, SSM_BF16, kGemmOutProj));
+    L.splitk.p = (float*)take(sk);
+    L.splitk.bytes = sk;
     L.total = off;
     return L;
 }
@@ -750,7 +802,7 @@ int m2_stage2(const M2& m, const ssm2_shard_weights_t* w, const float* sumsq, in
     SSM_TIMED(norm_name, s, launch_ssd_norm(L.g, sumsq, w->norm_w, L.gn, T, (int)m.E, (int)m.G, m.gsize,
                                             (int)(m.r * m.E), 1e-5f, s));
     return gemm(T, m.dm, m.E, L.gn, m.E, SSM_BF16, w->out_proj_w, m.E, SSM_BF16, y, m.dm, SSM_BF16, s, out_name,
-                kGemmOutProj);
+                kGemmOutProj, L.splitk);
 }
 
 }  // namespace
@@ -841,7 +893,7 @@ int ssm2_shard_prefill_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weigh
         SSM_TRY(check_ptr(x, "x"));
         SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
         SSM_TRY(gemm(T, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
-                     "m2.prefill.in_proj", kGemmInProj));
+                     "m2.prefill.in_proj", kGemmInProj, L.splitk));
     }
     // (the history update also runs for a batch of empty sequences: fresh ones end with zeros)
     ConvArgs ca = m2_conv(m, w, L, T, meta->cu_seqlens, meta->cache_slot, meta->has_initial_state, meta->nseq,
@@ -891,7 +943,7 @@ int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weight
     SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
     SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
     SSM_TRY(gemm(B, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
-                 "m2.decode.in_proj", kGemmInProj));
+                 "m2.decode.in_proj", kGemmInProj, L.splitk));
     ConvArgs ca = m2_conv(m, w, L, B, nullptr, slot, nullptr, B, conv_pool, S);
     SSM_TIMED("m2.decode.conv", s, launch_conv_decode(ca, true, s));
     SsdPublic p = m2_ssd(m, w, L, ssm_pool, S, L.status);

@@ -67,9 +67,13 @@ __host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_
 enum GemmRole { kGemmGeneric = 0, kGemmInProj = 1, kGemmXProj = 2, kGemmDtProj = 3, kGemmOutProj = 4 };
 // o [M][K] bf16 (dense) = a [M][K] fp32 (row stride lda) rounded to nearest even; K % 8 == 0
 hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t M, int K, hipStream_t s);
+// scratch: fp32 partials of a split-K run (outputs with fewer tiles than CUs and a long
+// K); gemm_splitk_bytes gives the size a shape would use (0: it is not split), and with
+// less scratch the GEMM runs unsplit.
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt,
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
-                          hipStream_t s, GemmRole role);
+                          hipStream_t s, GemmRole role, float* scratch = nullptr, size_t scratch_bytes = 0);
+size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role);
 
 // Few-row (decode) GEMM C = A * B^T with a fused epilogue; bf16 weights.
 enum SkinnyEpi { kSkinnyStoreBf16 = 0, kSkinnyStoreF32 = 1, kSkinnyConv = 2, kSkinnyState = 3 };

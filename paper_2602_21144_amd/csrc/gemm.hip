@@ -5,6 +5,8 @@
 // [out_features][in_features]), which is the natural operand layout of MFMA: every
 // lane loads 8 consecutive k of one row. bf16 path: v_mfma_f32_32x32x16_bf16 with
 // fp32 accumulation; fp32 path: v_mfma_f32_16x16x4_f32.
+#include <algorithm>
+
 #include "common.h"
 
 namespace ssm {
@@ -213,12 +215,14 @@ template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
 }
 
 // WM x WN waves; with 8 waves two share each SIMD, so one wave's barrier and LDS waits
-// are covered by the other's MFMAs.
-template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32>
+// are covered by the other's MFMAs. SPLIT: workgroup (tile, blockIdx.y) multiplies the
+// K-slice [blockIdx.y * K, (blockIdx.y + 1) * K) (K is the slice length) and stores its
+// fp32 partial tile at part[blockIdx.y][M][N]; a reduce kernel adds the slices.
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
                                                               int64_t lda, const bf16* __restrict__ B, int64_t ldb,
                                                               void* __restrict__ Cp, int64_t ldc, int tiles_m,
-                                                              int tiles_n) {
+                                                              int tiles_n, float* __restrict__ part) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -237,6 +241,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     const int m0 = tm * BM, n0 = tn * BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
+    if constexpr (SPLIT) {
+        A += (int64_t)blockIdx.y * K;
+        B += (int64_t)blockIdx.y * K;
+    }
 
     const int lr = lane / CPR, lp = lane % CPR;
     const bf16* asrc[AG];
@@ -346,7 +354,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
                 const int n = n0 + wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
                 const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
                 const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-                if constexpr (C_F32) {
+                if constexpr (SPLIT) {
+                    float* p = part + ((int64_t)blockIdx.y * M + m) * N + n;
+                    if (n + 3 < N && (N & 3) == 0) {
+                        *(float4*)p = make_float4(v0, v1, v2, v3);
+                    } else {
+                        if (n < N) p[0] = v0;
+                        if (n + 1 < N) p[1] = v1;
+                        if (n + 2 < N) p[2] = v2;
+                        if (n + 3 < N) p[3] = v3;
+                    }
+                } else if constexpr (C_F32) {
                     float* p = (float*)Cp + (int64_t)m * ldc + n;
                     if (n + 3 < N) {
                         *(float4*)p = make_float4(v0, v1, v2, v3);
@@ -372,28 +390,96 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     }
 }
 
+// C[m][n] = sum over the slices, in slice order, of part[slice][m][n]; 4 outputs per thread
+template <bool C_F32>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int N,
+                                                            void* __restrict__ Cp, int64_t ldc) {
+    const int n4 = (N + 3) / 4;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)M * n4) return;
+    const int m = (int)(i / n4), n = (int)(i % n4) * 4;
+    const int64_t slice = (int64_t)M * N;
+    const float* p = part + (int64_t)m * N + n;
+    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const bool full = n + 3 < N && (N & 3) == 0;
+    for (int sp = 0; sp < splits; ++sp, p += slice) {
+        if (full) {
+            const float4 q = *(const float4*)p;
+            v[0] += q.x; v[1] += q.y; v[2] += q.z; v[3] += q.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (n + e < N) v[e] += p[e];
+        }
+    }
+    if constexpr (C_F32) {
+        float* c = (float*)Cp + (int64_t)m * ldc + n;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (n + e < N) c[e] = v[e];
+    } else {
+        bf16* c = (bf16*)Cp + (int64_t)m * ldc + n;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (n + e < N) c[e] = (bf16)v[e];
+    }
+}
+
 template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF>
 hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
-                   int64_t ldc, hipStream_t s) {
+                   int64_t ldc, hipStream_t s, int splits = 1, float* part = nullptr) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
-    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
-                       (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn);
+    if (splits <= 1) {
+        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
+                   (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, nullptr);
+        return hipGetLastError();
+    }
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, true>), dim3(tm * tn, splits), dim3(64 * WM * WN), 0,
+               s, (int)M, (int)N, (int)(K / splits), (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, part);
+    if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    KernelTimer kt("gemm.splitk_reduce", s);
+    const int64_t n = M * ((N + 3) / 4);
+    SSM_LAUNCH((splitk_reduce_kernel<CF>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const float*)part,
+               splits, (int)M, (int)N, C, ldc);
     return hipGetLastError();
 }
 
 // Tile shape by a wave-quantisation cost model: whole rounds of 256 workgroups (one per
 // CU) times tile area over the shape's measured efficiency (256x256 does the most MFMA
 // work per LDS byte; 128x128 gives more workgroups when the grid is small).
-template <int ROLE, bool CF>
-hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
-                        void* C, int64_t ldc, hipStream_t s) {
+bool dma_big_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, double eff) {
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         return (double)((tiles + 255) / 256) * bm * bn / eff;
     };
-    if (K % 64 == 0 && cost(256, 256, 1.0) <= cost(128, 128, 0.83))
+    return cost(256, 256, 1.0) <= cost(128, 128, 0.83);
+}
+
+// Split-K for outputs of fewer tiles than CUs: K is cut into equal slices of whole
+// 64-wide k-tiles (at least two per slice) so that up to ~384 workgroups run; the slices'
+// fp32 partials are added by a reduce kernel in slice order (deterministic).
+int splitk_slices(int64_t tiles, int64_t K) {
+    if (K % 64 != 0 || tiles >= 256) return 1;
+    const int64_t nk = K / 64, cap = std::max<int64_t>(1, 384 / tiles);
+    int best = 1;
+    for (int64_t d = 2; d <= cap && d <= nk / 2; ++d)
+        if (nk % d == 0) best = (int)d;
+    return best;
+}
+
+int fit_slices(int sp, int64_t M, int64_t N, size_t scratch_bytes) {
+    return (sp > 1 && (size_t)sp * M * N * 4 <= scratch_bytes) ? sp : 1;
+}
+
+template <int ROLE, bool CF>
+hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+                        void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
+    if (K % 64 == 0 && dma_big_tiles(M, N))
         return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (K % 64 == 0) return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (K % 64 == 0) {
+        const int sp = fit_slices(splitk_slices(((M + 127) / 128) * ((N + 127) / 128), K), M, N, scratch_bytes);
+        return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
+    }
     return run_dma<ROLE, 128, 128, 32, 4, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
@@ -496,7 +582,7 @@ __global__ __launch_bounds__(256) void round_bf16_rows_kernel(const float* __res
 
 template <int ROLE, bool AF, bool CF>
 hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
-                         void* C, int64_t ldc, hipStream_t s) {
+                         void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
     // Tile by output size: large outputs use 256x256 (each wave 128x128, the most
     // MFMA work per LDS byte), mid-size ones 128x128 for more workgroups.
     if (M <= 64) {  // few rows: the weight read dominates; stream it with many narrow workgroups
@@ -509,11 +595,14 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
         // x_proj: few output columns (R + 2N), long K; one 64-row tile spans all of N so
         // that every activation row is read once, with a 3-deep ring to cover the latency
         // that four waves per CU leave exposed
-        if (K % 64 == 0 && N <= 192) return run_dma<ROLE, 64, 192, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-        if (K % 64 == 0 && N <= 256) return run_dma<ROLE, 64, 256, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (K % 64 == 0 && N <= 256) {
+            const int sp = fit_slices(splitk_slices((M + 63) / 64, K), M, N, scratch_bytes);
+            if (N <= 192) return run_dma<ROLE, 64, 192, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
+            return run_dma<ROLE, 64, 256, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
+        }
     }
     if constexpr (!AF) {
-        if (K % 32 == 0) return dispatch_dma<ROLE, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (K % 32 == 0) return dispatch_dma<ROLE, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
     }
     // staged path: fp32 A (rounded while staging) or a K tail; short K favours more tiles
     const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
@@ -530,8 +619,20 @@ hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t 
     return hipGetLastError();
 }
 
+size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role) {
+    // mirrors the dispatch below: the DMA paths with bf16 operands and K % 64 == 0
+    if (M <= 64 || N == 0 || b_dt != SSM_BF16 || a_dt != SSM_BF16 || K % 64 != 0) return 0;
+    int64_t tiles;
+    if (role == kGemmXProj && N <= 256) tiles = (M + 63) / 64;
+    else if (dma_big_tiles(M, N)) return 0;
+    else tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    const int sp = splitk_slices(tiles, K);
+    return sp > 1 ? (size_t)sp * M * N * 4 : 0;
+}
+
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, int a_dt, const void* B,
-                          int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s, GemmRole role) {
+                          int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt, hipStream_t s, GemmRole role,
+                          float* scratch, size_t scratch_bytes) {
     if (M == 0 || N == 0) return hipSuccess;
     if (b_dt == SSM_F32) {
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
@@ -554,25 +655,25 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
     // the mixer's projections use one operand combination each
     switch (role) {
         case kGemmInProj:
-            if (!af && !cf) return dispatch_bf16<kGemmInProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            if (!af && !cf) return dispatch_bf16<kGemmInProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
             break;
         case kGemmXProj:
-            if (!af && cf) return dispatch_bf16<kGemmXProj, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            if (!af && cf) return dispatch_bf16<kGemmXProj, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
             break;
         case kGemmDtProj:
-            if (af && !cf) return dispatch_bf16<kGemmDtProj, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
-            if (!af && !cf) return dispatch_bf16<kGemmDtProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            if (af && !cf) return dispatch_bf16<kGemmDtProj, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
+            if (!af && !cf) return dispatch_bf16<kGemmDtProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
             break;
         case kGemmOutProj:
-            if (!af && !cf) return dispatch_bf16<kGemmOutProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+            if (!af && !cf) return dispatch_bf16<kGemmOutProj, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
             break;
         default:
             break;
     }
-    if (af && cf) return dispatch_bf16<kGemmGeneric, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (af) return dispatch_bf16<kGemmGeneric, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    if (cf) return dispatch_bf16<kGemmGeneric, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
-    return dispatch_bf16<kGemmGeneric, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (af && cf) return dispatch_bf16<kGemmGeneric, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
+    if (af) return dispatch_bf16<kGemmGeneric, true, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
+    if (cf) return dispatch_bf16<kGemmGeneric, false, true>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
+    return dispatch_bf16<kGemmGeneric, false, false>(M, N, K, A, lda, B, ldb, C, ldc, s, scratch, scratch_bytes);
 }
 
 }  // namespace ssm

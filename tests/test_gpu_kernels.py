@@ -62,6 +62,37 @@ def test_gemm_nt(B, M, N, K, kind):
     assert_close(got, ref, tol, f"gemm {kind} {M}x{N}x{K}")
 
 
+SPLITK_SHAPES = [("out_proj", 256, 2560, 5120, False), ("in_proj", 256, 10240, 2560, False),
+                 ("x_proj", 300, 192, 5120, True), ("x_proj", 2048, 256, 3584, True), ("in_proj", 100, 5416, 2560, False),
+                 ("out_proj", 333, 3584, 3584, False), ("generic", 129, 130, 1024, False), ("x_proj", 65, 80, 1536, True)]
+
+
+@pytest.mark.parametrize("role,M,N,K,c_f32", SPLITK_SHAPES)
+def test_gemm_split_k(B, role, M, N, K, c_f32):
+    """Few output tiles and a long K: the product is cut into K-slices whose partials a
+    second kernel adds; the result matches the float64 product and the unsplit run."""
+    need = B.gemm_splitk_bytes(M, N, K, B.SSM_BF16, B.SSM_BF16, role)
+    assert need > 0, "this shape is expected to run split-K"
+    rng = np.random.default_rng(M + N + K)
+    A = _rnd_host(rng, (M, K), "bf16")
+    Bm = _rnd_host(rng, (N, K), "bf16", 1.0 / np.sqrt(K))
+    c_dt = torch.float32 if c_f32 else torch.bfloat16
+    Ad, Bd = _dev(A, torch.bfloat16), _dev(Bm, torch.bfloat16)
+    scratch = torch.full((need // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    Np = (N + 3) // 4 * 4   # output rows padded to a multiple of 4 values; C is a view
+    C = torch.full((M, Np), float("nan"), dtype=c_dt, device="cuda")[:, :N]
+    B.ssm_gemm_nt_role(Ad, Bd, C, role, scratch)
+    C1 = torch.full((M, Np), float("nan"), dtype=c_dt, device="cuda")[:, :N]
+    B.ssm_gemm_nt_role(Ad, Bd, C1, role, None)          # no scratch: unsplit
+    torch.cuda.synchronize()
+    ref = A.astype(np.float64) @ Bm.astype(np.float64).T
+    if not c_f32:
+        ref = om.round_bf16(ref)
+    tol = 1e-5 if c_f32 else 8e-3
+    assert_close(C.to(torch.float64).cpu().numpy(), ref, tol, f"split-K {role} {M}x{N}x{K}")
+    assert_close(C1.to(torch.float64).cpu().numpy(), ref, tol, f"unsplit {role} {M}x{N}x{K}")
+
+
 def test_gemm_strided_operands(B):
     """dt_proj reads the first R columns of x_dbl (row stride R+2N) as its A operand."""
     rng = np.random.default_rng(5)
