@@ -387,8 +387,10 @@ typedef struct ssm_kernel_time {
     int64_t launches;    /* launches recorded since the last collection */
     double total_ms;     /* summed kernel execution time, begin to end of each dispatch */
 } ssm_kernel_time_t;
-/* on: 1 to record, 0 to stop. only: NULL to time every kernel, else the one kernel
- * name to time (keeps the event overhead off the other launches). */
+/* on: 0 to stop, 1 to time every launch, k > 1 to time every k-th launch of each kernel
+ * name (the first included), which keeps the per-launch event cost, about 5 us on a
+ * decode-sized kernel, off all but one launch in k; negative: SSM_E_INVAL. only: NULL to
+ * time every kernel, else the one kernel name to time. */
 int ssm_timing_enable(int32_t on, const char* only);
 /* Waits for the recorded events, sums time per kernel name into out[0 .. *count), at
  * most max entries, and forgets the records. SSM_E_HIP if an event could not be read. */

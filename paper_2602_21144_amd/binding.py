@@ -554,8 +554,9 @@ def scan_scratch_workspace_bytes(desc: Desc, T: int, nseq: int) -> int:
     return prefill_workspace_bytes(desc, T, nseq)
 
 
-def ssm_timing_enable(on: bool = True, only: Optional[str] = None):
-    _check(lib().ssm_timing_enable(1 if on else 0, only.encode() if only else None))
+def ssm_timing_enable(on: bool = True, only: Optional[str] = None, every: int = 1):
+    """Per-dispatch kernel timing on (every `every`-th launch of each kernel name) or off."""
+    _check(lib().ssm_timing_enable((max(int(every), 1) if on else 0), only.encode() if only else None))
 
 
 def ssm_timing_collect(max_kernels: int = 64) -> Dict[str, tuple]:

@@ -38,6 +38,29 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
     return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
 }
 
+// Global -> LDS on the DMA path: global_load_lds_dwordx4 writes each lane's 16 bytes at
+// lane slot (lane * 16) of a 1 KB LDS block at lds_addr (M0), with no staging registers.
+// Issued from inline assembly so the compiler does not wait for it before unrelated LDS
+// reads; completion is awaited with wait_vm (the wave's vector-memory counter).
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// wait until at most n of this wave's vector-memory loads are outstanding (n < 64).
+// GFX9 s_waitcnt immediate: vmcnt in bits [3:0] and [15:14]; expcnt [6:4] and
+// lgkmcnt [11:8] at their maxima (no wait on them).
+template <int n> __device__ __forceinline__ void wait_vm() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+// wait until this wave's LDS reads (and other lgkm operations) are complete
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
 // exp2 / log2 on the transcendental unit (v_exp_f32 / v_log_f32).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }

@@ -190,23 +190,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
 // compiler does not serialise the prefetch behind each tile's LDS reads. Rows past M
 // or N are clamped to a valid row (their results are never stored). Fragments of
 // k-substep s+1 are read from LDS while the MFMAs of substep s run.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// wait until at most n of this wave's vector-memory loads are outstanding (n < 64).
-// GFX9 s_waitcnt immediate: vmcnt in bits [3:0] and [15:14]; expcnt [6:4] and
-// lgkmcnt [11:8] at their maxima (no wait on them).
-template <int n> __device__ __forceinline__ void wait_vm() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
 // chunk permutation of an LDS row: 16 lanes reading one chunk column of 16 consecutive
 // rows hit distinct 16-byte bank groups (128-byte rows: key (r>>1)&7; 64-byte: (r>>2)&3)
 template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {

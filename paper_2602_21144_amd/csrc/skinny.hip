@@ -1,8 +1,12 @@
 // Decode-step projections: C[M][N] = A[M][K] * B[N][K]^T for few rows (one token per
-// sequence), where the time is the weight read. Each workgroup owns 16 output columns
-// and up to 64 rows; its waves split K, each streaming its share of the 16 weight rows
-// with 16-byte loads into v_mfma_f32_16x16x32_bf16, and the partial tiles are summed
-// through LDS. Hundreds of workgroups stream disjoint weight rows at once.
+// sequence), where the time is the weight read. Each workgroup owns 16 output columns;
+// its waves split K and the partial tiles are summed through LDS. Hundreds of workgroups
+// stream disjoint weight rows at once. Two ways of moving the operands:
+//   - streamed (up to 16 rows, bf16, K a multiple of 64: in_proj, x_proj, out_proj of a
+//     decode step): whole-line loads into registers, re-laid out through LDS as MFMA
+//     fragments (gemm_gemv_kernel);
+//   - direct (up to 64 rows, any K, fp32 activations): 16-byte fragment loads straight
+//     into v_mfma_f32_16x16x32_bf16 (gemm_skinny_kernel).
 //
 // Epilogues fuse the per-channel work that follows each projection in a decode step
 // (Section IV-A: the cache is read and advanced in place, with no prefix rescan):
@@ -233,6 +237,125 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(SkinnyArgs p) {
     else ein.apply(p, em, en, v);
 }
 
+// Streamed-weight variant for at most 16 rows, bf16 activations and K a multiple of 64
+// (in_proj, x_proj and out_proj of a decode step). Loading MFMA fragments straight from
+// global memory makes every load instruction touch 16 weight rows x 64 bytes (half cache
+// lines of 16 rows), which streams at about half the rate of whole lines. Here every
+// load instruction reads a block of 8 rows x 128 bytes (whole lines): a wave owns a
+// contiguous run of up to NST 64-wide k stages and issues the loads of all of
+// them (16 weight rows and the activation rows of each stage) at once, so its whole
+// share is in flight after a single memory latency; registers hold it, since LDS could
+// not. Each stage is then written to a small wave-private LDS buffer (XOR-swizzled rows)
+// and read back as 16x16x32 MFMA fragments. The waves' partial tiles are summed through
+// LDS at the end and go through the same epilogues.
+constexpr int kGemvBK = 64;
+
+__device__ __forceinline__ int gemv_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+template <int NW, int NST, int XB, int EPI>
+__global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
+    static_assert(NW >= 4, "one epilogue element per thread of the first 256");
+    constexpr int SLOT = (2 + XB) * 1024;  // one stage: 16 weight rows, then 8 * XB activation rows, 128 B each
+    __shared__ __attribute__((aligned(16))) char tr[NW][2][SLOT];
+    __shared__ float red[NW][256];
+    const int n0 = blockIdx.x * 16;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+    const int e = threadIdx.x;
+    const int em = e >> 4, en = n0 + (e & 15);
+    const bool ework = e < 256 && em < p.M && en < p.N;
+    const int emc = em < p.M ? em : p.M - 1, enc = en < p.N ? en : p.N - 1;  // in-range for the fetch
+    EpiIn<EPI> ein;
+    ein.load_slot(p, emc);
+
+    // this wave's stages [sb, sb + nst) of the K / 64 (nst <= NST, checked by the launcher)
+    const int nall = p.K / kGemvBK;
+    const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
+    // lane l loads row l / 8 of a block, 16-byte chunk l % 8; weight rows past N and
+    // activation rows past M lie outside the resources and read as zero
+    const int lr = lane >> 3, lp = lane & 7;
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(min(16, p.N - n0) * p.ldb * 2));
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(p.A, (uint32_t)(p.M * p.lda * 2));
+    const uint32_t k0b = (uint32_t)(sb * kGemvBK + lp * 8) * 2;
+    const uint32_t wo0 = (uint32_t)(lr * p.ldb) * 2 + k0b, wo1 = (uint32_t)((8 + lr) * p.ldb) * 2 + k0b;
+    u32x4 w0[NST], w1[NST], xv[NST][XB];
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+        const bool ok = st < nst;
+        w0[st] = buffer_load16(rb, ok ? wo0 + st * 128 : kOffOutOfRange);
+        w1[st] = buffer_load16(rb, ok ? wo1 + st * 128 : kOffOutOfRange);
+#pragma unroll
+        for (int q = 0; q < XB; ++q)
+            xv[st][q] = buffer_load16(ra, ok ? (uint32_t)((8 * q + lr) * p.lda) * 2 + k0b + st * 128 : kOffOutOfRange);
+    }
+    // the epilogue's slot-addressed operands go out behind the stream
+    __builtin_amdgcn_sched_barrier(0);
+    ein.load(p, emc, enc);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // fragment rows: weights l % 16, activations l % (8 XB); chunk 4 j + l / 16 of substep j
+    const int wr = lane & 15, xr = XB == 2 ? (lane & 15) : (lane & 7), cg = lane >> 4;
+    f32x4 acc = f32x4{};
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+        if (st < nst) {
+            char* t = tr[wave][st & 1];
+            *(u32x4*)(t + lr * 128 + gemv_swz(lr, lp) * 16) = w0[st];
+            *(u32x4*)(t + (8 + lr) * 128 + gemv_swz(8 + lr, lp) * 16) = w1[st];
+#pragma unroll
+            for (int q = 0; q < XB; ++q)
+                *(u32x4*)(t + 2048 + (8 * q + lr) * 128 + gemv_swz(8 * q + lr, lp) * 16) = xv[st][q];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int c = 4 * j + cg;
+                const bf16x8 wf = *(const bf16x8*)(t + wr * 128 + gemv_swz(wr, c) * 16);
+                const bf16x8 xf = *(const bf16x8*)(t + 2048 + xr * 128 + gemv_swz(xr, c) * 16);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, acc, 0, 0, 0);
+            }
+        }
+    }
+    // lane l holds column l % 16 and rows 4 (l / 16) + r of the 16-row tile
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][(4 * (lane >> 4) + r) * 16 + (lane & 15)] = acc[r];
+    __syncthreads();
+    if (!ework) return;
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) v += red[w][e];
+    if constexpr (EPI == kEpiStoreBf16) ((bf16*)p.C)[(int64_t)em * p.ldc + en] = (bf16)v;
+    else if constexpr (EPI == kEpiStoreF32) ((float*)p.C)[(int64_t)em * p.ldc + en] = v;
+    else ein.apply(p, em, en, v);
+}
+
+// waves per workgroup for the streamed variant (0: it does not apply). Grids that fill
+// the CUs take 4 waves of up to 10 stages each (8 waves for longer K); small grids take
+// 16 waves of up to 4 stages, so that the few CUs in use keep many blocks in flight.
+// (Spreading N over exactly one workgroup per CU, ceil(N / 256) rows each, shortened the
+// kernels' span but not a decode step, so the tiles stay 16 columns wide.)
+int gemv_waves(const SkinnyArgs& p) {
+    auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+    if (p.M > 16 || p.a_f32 || p.K % kGemvBK != 0 || p.lda % 8 != 0 || p.ldb % 8 != 0 || !al16(p.A) || !al16(p.B))
+        return 0;
+    if ((int64_t)p.M * p.lda * 2 >= (int64_t)1 << 31 || (int64_t)16 * p.ldb * 2 >= (int64_t)1 << 31) return 0;
+    const int nall = p.K / kGemvBK;
+    if ((p.N + 15) / 16 < 128) return nall <= 16 * 4 ? 16 : 0;
+    if (nall <= 4 * 10) return 4;
+    return nall <= 8 * 10 ? 8 : 0;
+}
+
+template <int EPI>
+hipError_t launch_gemv(const SkinnyArgs& p, int nw, hipStream_t s) {
+    const dim3 grid((unsigned)((p.N + 15) / 16)), block(nw * 64);
+#define SSM_GEMV(NW, NST)                                                                  \
+    if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, EPI>), grid, block, 0, s, p);   \
+    else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, EPI>), grid, block, 0, s, p);
+    if (nw == 4) { SSM_GEMV(4, 10) }
+    else if (nw == 8) { SSM_GEMV(8, 10) }
+    else { SSM_GEMV(16, 4) }
+#undef SSM_GEMV
+    return hipGetLastError();
+}
+
 template <int MB, int NW, int KU, bool AF, int EPI>
 void launch_one(const SkinnyArgs& p, dim3 grid, hipStream_t s) {
     SSM_LAUNCH((gemm_skinny_kernel<MB, NW, KU, AF, EPI>), grid, dim3(NW * 64), 0, s, p);
@@ -284,6 +407,14 @@ hipError_t launch_epi(const SkinnyArgs& p, hipStream_t s) {
 
 hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    if (const int nw = gemv_waves(p)) {
+        switch (epi) {
+            case kSkinnyStoreBf16: return launch_gemv<kEpiStoreBf16>(p, nw, s);
+            case kSkinnyStoreF32: return launch_gemv<kEpiStoreF32>(p, nw, s);
+            case kSkinnyConv: return launch_gemv<kEpiConv>(p, nw, s);
+            default: break;
+        }
+    }
     switch (epi) {
         case kSkinnyStoreBf16: return p.a_f32 ? launch_epi<true, kEpiStoreBf16>(p, s) : launch_epi<false, kEpiStoreBf16>(p, s);
         case kSkinnyStoreF32: return p.a_f32 ? launch_epi<true, kEpiStoreF32>(p, s) : launch_epi<false, kEpiStoreF32>(p, s);

@@ -19,6 +19,17 @@ struct Rec {
 
 thread_local bool g_on = false;
 thread_local std::string g_only;  // when non-empty, only launches with this name are timed
+thread_local int g_stride = 1;    // time every g_stride-th launch of each name
+thread_local std::vector<std::pair<std::string, int64_t>> g_seen;  // launches per name while enabled
+
+// true for the launches of `name` to time: every g_stride-th one (the first included)
+bool sampled(const char* name) {
+    if (g_stride <= 1) return true;
+    for (auto& kv : g_seen)
+        if (kv.first == name) return kv.second++ % g_stride == 0;
+    g_seen.emplace_back(name, 1);
+    return true;
+}
 thread_local std::vector<Rec> g_recs;
 thread_local std::vector<hipEvent_t> g_pool;
 
@@ -41,6 +52,7 @@ KernelTimer::KernelTimer(const char* name, hipStream_t s) : prev_(g_cur) {
     g_cur = nullptr;
     if (!g_on) return;
     if (!g_only.empty() && g_only != name) return;
+    if (!sampled(name)) return;
     // nothing is timed inside graph capture: captured launches carry no timestamps
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
@@ -71,8 +83,11 @@ bool launch_timed_events(hipEvent_t* start, hipEvent_t* stop) {
 extern "C" {
 
 int ssm_timing_enable(int32_t on, const char* only) {
+    if (on < 0) return SSM_E_INVAL;
     ssm::g_on = on != 0;
     ssm::g_only = only ? only : "";
+    ssm::g_stride = on > 1 ? on : 1;
+    ssm::g_seen.clear();
     return SSM_OK;
 }
 

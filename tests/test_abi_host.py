@@ -186,3 +186,13 @@ def test_layer_and_stack_host_checks(B):
     need = ctypes.c_size_t()
     L.ssm_stack_prefill_workspace_bytes(ctypes.byref(sd), 100, 1, ctypes.byref(need))
     assert call(sd, need.value - 1) == -3                                   # workspace too small
+
+
+def test_timing_switch_arguments(B):
+    """Kernel timing: 0 turns it off, k >= 1 samples every k-th launch, negative is rejected;
+    collecting with nothing recorded returns no entries."""
+    L = B.lib()
+    assert L.ssm_timing_enable(-1, None) == -1
+    assert L.ssm_timing_enable(4, b"decode.in_proj_conv") == 0
+    assert L.ssm_timing_enable(0, None) == 0
+    assert B.ssm_timing_collect() == {}

@@ -80,3 +80,26 @@ def test_decode_bad_slot_is_flagged():
     assert B.take_status(g._dws[0]) == 0
     np.testing.assert_array_equal(y_bad[[0, 2]], y_ok)
     assert torch.equal(ssm[0], ssm2[0]) and torch.equal(conv[0], conv2[0])
+
+
+@pytest.mark.parametrize("every", [1, 4])
+def test_kernel_timing_samples_every_kth_launch(every):
+    """Per-dispatch timing of one kernel name records every k-th of its launches (the first
+    included) and nothing for the other kernels."""
+    from paper_2602_21144_amd import binding as B
+    shape = synth.LayerShape(64, 128, 16, 16, 4, 1, "bf16")
+    g = GpuLayer(shape, synth.make_layer(shape, 5))
+    conv, ssm = g.new_pools(4, poison=False)
+    rng = np.random.default_rng(2)
+    sl = torch.tensor([0, 3], dtype=torch.int32, device="cuda")
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True, "decode.in_proj_conv", every=every)
+    for _ in range(8):
+        g.decode(synth.make_tokens(rng, 2, shape.d_model, "bf16"), sl, conv, ssm)
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    got = B.ssm_timing_collect()
+    assert set(got) == {"decode.in_proj_conv"}
+    launches, ms = got["decode.in_proj_conv"]
+    assert launches == 8 // every and ms > 0
+    assert B.take_status(g._dws[0]) == 0
