@@ -23,7 +23,7 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kMinWin = 32, kMaxWin = 2048;
-constexpr int kTargetWaves = 3072;
+constexpr int kTargetWaves = 3072;  // 3 per SIMD: the main pass holds 156 VGPRs per lane
 
 // flags per window, written by pass A
 constexpr int kFlagContIn = 1;    // first token continues a sequence begun earlier
@@ -41,7 +41,7 @@ __device__ __forceinline__ int seq_of(const int32_t* cu, int nseq, int64_t t) {
     return lo;
 }
 
-int64_t target_windows(int E) { return std::max<int64_t>(1, ((int64_t)kTargetWaves * kWave + E - 1) / E); }
+int64_t target_windows(int E) { return std::max<int64_t>(1, (int64_t)kTargetWaves * kWave / E); }
 
 constexpr int kTB = 8;  // tokens per block: loads for block i+1 are in flight while block i computes
 
@@ -182,13 +182,26 @@ __global__ __launch_bounds__(256) void scan_link_kernel(ScanArgs a, int nwin, co
     if (gid >= (int64_t)a.E * kN) return;
     const int c = (int)(gid / kN), n = (int)(gid % kN);
     const float A2 = -__expf(a.A_log[c * kN + n]) * kLog2e;
+    // the windows' local values are fetched kLB at a time, so that only the carry chain
+    // itself is serial (entries of windows without a carry are never written by pass A
+    // and are read but not used)
+    constexpr int kLB = 16;
     float carry = 0.0f;
-    for (int j = 0; j < nwin; ++j) {
-        const int f = wflags[j];
-        if (f & kFlagContIn) a.h_in[((int64_t)j * a.E + c) * kN + n] = carry;
-        if (f & kFlagCarryOut) {
-            const float hl = a.h_local[((int64_t)j * a.E + c) * kN + n];
-            carry = (f & kFlagLastCont) ? fast_exp2(a.sum_delta[(int64_t)j * a.E + c] * A2) * carry + hl : hl;
+    for (int j0 = 0; j0 < nwin; j0 += kLB) {
+        float hl[kLB], sd[kLB];
+#pragma unroll
+        for (int q = 0; q < kLB; ++q) {
+            const int64_t j = min(j0 + q, nwin - 1);
+            hl[q] = a.h_local[(j * a.E + c) * kN + n];
+            sd[q] = a.sum_delta[j * a.E + c];
+        }
+#pragma unroll
+        for (int q = 0; q < kLB; ++q) {
+            const int j = j0 + q;
+            if (j >= nwin) break;
+            const int f = wflags[j];
+            if (f & kFlagContIn) a.h_in[((int64_t)j * a.E + c) * kN + n] = carry;
+            if (f & kFlagCarryOut) carry = (f & kFlagLastCont) ? fast_exp2(sd[q] * A2) * carry + hl[q] : hl[q];
         }
     }
     for (int s = 0; s < a.nseq; ++s) {
@@ -351,12 +364,14 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
 
 }  // namespace
 
+// Window length: about target_windows(E) windows over the T tokens, so that every SIMD
+// runs the same number of waves (the main pass fits 3 per SIMD). Any multiple of the
+// token block works; rounding to a power of two instead left the busiest SIMDs a fifth
+// more work than the average (2560 waves on 1024 SIMDs for the 2.8B half shard).
 int scan_window_len(int64_t T, int E) {
     const int64_t tw = target_windows(E);
-    int64_t want = (T + tw - 1) / tw;
-    int64_t w = kMinWin;
-    while (w < want && w < kMaxWin) w <<= 1;
-    return (int)w;
+    const int64_t want = ((T + tw - 1) / tw + kTB - 1) / kTB * kTB;
+    return (int)std::min<int64_t>(kMaxWin, std::max<int64_t>(kMinWin, want));
 }
 
 static int64_t max_windows(int64_t max_T, int E) {
