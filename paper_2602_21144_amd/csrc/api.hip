@@ -144,8 +144,16 @@ struct DecodeWs {
     int32_t* status;
     char *xz, *u, *dt, *g;
     float* xdbl;
+    Scratch splitk;  // fp32 partials of the projections that run split-K (large batches)
     size_t total;
 };
+
+// Largest decode batch that takes the fused kernels (in_proj with the conv step in its
+// epilogue, dt_proj with the state step in its epilogue): each of their workgroups reads
+// every activation row, which suits a few rows. Larger batches run tiled projections
+// (split-K when the output has few tiles), a conv-step kernel and a state-step kernel
+// with one lane per (sequence, channel).
+constexpr int kFusedDecodeMax = 128;
 
 DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
     const size_t s = act_bytes(d);
@@ -160,6 +168,16 @@ DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
     L.xdbl = (float*)take((size_t)B * W * 4);
     L.dt = take((size_t)B * E * s);
     L.g = take((size_t)B * E * s);
+    const int adt = d->act_dtype;
+    const int64_t dm = d->d_model;
+    size_t sk = 0;
+    if (B > kFusedDecodeMax) {
+        sk = gemm_splitk_bytes(B, 2 * E, dm, adt, adt, kGemmInProj);
+        sk = std::max(sk, gemm_splitk_bytes(B, W, E, adt, adt, kGemmXProj));
+        sk = std::max(sk, gemm_splitk_bytes(B, dm, E, adt, adt, kGemmOutProj));
+    }
+    L.splitk.p = (float*)take(sk);
+    L.splitk.bytes = sk;
     L.total = off;
     return L;
 }
@@ -267,7 +285,7 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
             void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    if (adt == SSM_BF16 && d->d_conv >= 2) {
+    if (adt == SSM_BF16 && d->d_conv >= 2 && B <= kFusedDecodeMax) {
         // in_proj with the conv window shift + SiLU fused into its epilogue; x_proj
         SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, nullptr, 0, B, 2 * E, dm);
         p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
@@ -278,10 +296,12 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
         SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
         return SSM_OK;
     }
-    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj", kGemmInProj));
+    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj", kGemmInProj,
+                 L.splitk));
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
     SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
-    SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj));
+    SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj,
+                 L.splitk));
     return SSM_OK;
 }
 
@@ -289,7 +309,7 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
             const int32_t* slot, float* ssm_pool, int32_t S, void* y, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model, R = d->dt_rank;
-    if (adt == SSM_BF16) {
+    if (adt == SSM_BF16 && B <= kFusedDecodeMax) {
         // dt_proj with the whole recurrence step fused into its epilogue; out_proj
         SkinnyArgs p = skinny(xdbl, W, true, w->dt_proj_w, R, nullptr, 0, B, E, R);
         p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
@@ -305,7 +325,8 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, B, nullptr, slot, nullptr, B, ssm_pool, S, L.g, L.status,
                             nullptr);
     SSM_TIMED("decode.state_update", s, launch_decode_ssm(sa, adt == SSM_BF16, s));
-    SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "decode.out_proj", kGemmOutProj));
+    SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "decode.out_proj", kGemmOutProj,
+                 L.splitk));
     return SSM_OK;
 }
 

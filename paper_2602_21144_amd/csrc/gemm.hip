@@ -466,6 +466,55 @@ hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t 
     return run_dma<ROLE, 128, 128, 32, 4, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
+// fp32 weights and at most 8 activation rows (a decode step of the fp32 configuration),
+// where the time is the weight read: one weight row per wave, streamed in 1 KB runs (64
+// lanes x 4 floats, whole cache lines) and multiplied by the activation rows (M x K floats,
+// shared by every wave and served from cache); the lanes' sums meet by xor shuffles. K,
+// the leading dimensions and the pointers are multiples of 4 floats (checked by the caller).
+template <int ROLE>
+__global__ __launch_bounds__(256) void gemv_f32_kernel(int M, int N, int K, const float* __restrict__ A,
+                                                       int64_t lda, const float* __restrict__ B, int64_t ldb,
+                                                       float* __restrict__ C, int64_t ldc) {
+    constexpr int MR = 8;
+    const int lane = threadIdx.x & 63;
+    const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (n >= N) return;
+    const float* brow = B + (int64_t)n * ldb;
+    float acc[MR];
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[m] = 0.0f;
+    // four 1 KB runs per iteration, so that their loads are in flight together
+    for (int k0 = lane * 4; k0 < K; k0 += 1024) {
+        float4 b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            b[j] = k0 + 256 * j < K ? *(const float4*)(brow + k0 + 256 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+            if (m < M) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (k0 + 256 * j < K) {
+                        const float4 a = *(const float4*)(A + (int64_t)m * lda + k0 + 256 * j);
+                        acc[m] += a.x * b[j].x + a.y * b[j].y + a.z * b[j].z + a.w * b[j].w;
+                    }
+                }
+            }
+        }
+    }
+    float mine = 0.0f;
+#pragma unroll
+    for (int m = 0; m < MR; ++m) {
+        if (m < M) {
+            float v = acc[m];
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+            if (lane == m) mine = v;
+        }
+    }
+    if (lane < M) C[(int64_t)lane * ldc + n] = mine;
+}
+
 // fp32 operands on v_mfma_f32_16x16x4_f32: 64x64 tiles, k 16 per stage, four waves of 32x32.
 constexpr int kFBK = 16;
 constexpr int kFPad = kFBK + 1;
@@ -618,6 +667,24 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
                           float* scratch, size_t scratch_bytes) {
     if (M == 0 || N == 0) return hipSuccess;
     if (b_dt == SSM_F32) {
+        auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+        if (M <= 8 && K % 4 == 0 && lda % 4 == 0 && ldb % 4 == 0 && al16(A) && al16(B)) {
+            const dim3 grid((unsigned)((N + 3) / 4));
+#define SSM_F32_GEMV(R)                                                                                              \
+    case R:                                                                                                          \
+        SSM_LAUNCH(gemv_f32_kernel<R>, grid, dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, lda,         \
+                   (const float*)B, ldb, (float*)C, ldc);                                                            \
+        break;
+            switch (role) {
+                SSM_F32_GEMV(kGemmInProj)
+                SSM_F32_GEMV(kGemmXProj)
+                SSM_F32_GEMV(kGemmDtProj)
+                SSM_F32_GEMV(kGemmOutProj)
+                default: SSM_F32_GEMV(kGemmGeneric)
+            }
+#undef SSM_F32_GEMV
+            return hipGetLastError();
+        }
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
 #define SSM_F32_CASE(R)                                                                                             \
     case R:                                                                                                         \

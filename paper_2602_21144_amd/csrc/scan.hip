@@ -346,15 +346,29 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
     const float u = to_f32(((const T*)a.u)[(int64_t)b * a.E + c]);
     const float dt = to_f32(((const T*)a.dt)[(int64_t)b * a.E + c]);
     const float z = to_f32(((const T*)a.z)[(int64_t)b * a.ld_z + c]);
-    const float* Bt = a.xdbl + (int64_t)b * a.ld_xdbl + a.R;
+    // B_t and C_t of this sequence (the same for all its channels) and the channel's A_log,
+    // as 16-byte loads (ld_xdbl and R are multiples of 4 floats)
+    const float4* bt4 = (const float4*)(a.xdbl + (int64_t)b * a.ld_xdbl + a.R);
+    const float4* al4 = (const float4*)(a.A_log + (int64_t)c * kN);
+    float bc[2 * kN], al[kN];
+#pragma unroll
+    for (int q = 0; q < 2 * kN / 4; ++q) {
+        const float4 v = bt4[q];
+        bc[4 * q] = v.x; bc[4 * q + 1] = v.y; bc[4 * q + 2] = v.z; bc[4 * q + 3] = v.w;
+    }
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) {
+        const float4 v = al4[q];
+        al[4 * q] = v.x; al[4 * q + 1] = v.y; al[4 * q + 2] = v.z; al[4 * q + 3] = v.w;
+    }
     const float delta = softplus_f(dt + a.b_dt[c]);
     const float du = delta * u;
     float y = 0.0f;
 #pragma unroll
     for (int n = 0; n < kN; ++n) {
-        const float A2 = -__expf(a.A_log[c * kN + n]) * kLog2e;
-        h[n] = fast_exp2(delta * A2) * h[n] + du * Bt[n];
-        y += Bt[kN + n] * h[n];
+        const float A2 = -__expf(al[n]) * kLog2e;
+        h[n] = fast_exp2(delta * A2) * h[n] + du * bc[n];
+        y += bc[kN + n] * h[n];
     }
     y += a.D[c] * u;
 #pragma unroll

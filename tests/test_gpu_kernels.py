@@ -33,7 +33,10 @@ def _dev(a, dt):
 
 # ----------------------------------------------------------------------- GEMM
 GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 96, 224), (100, 300, 256), (257, 513, 64),
-               (1000, 520, 768), (2048, 2048, 512), (300, 5120, 2560), (4089, 4091, 256), (200, 300, 96)]
+               (1000, 520, 768), (2048, 2048, 512), (300, 5120, 2560), (4089, 4091, 256), (200, 300, 96),
+               # few rows with K a multiple of 64 (streamed-weight decode kernel: small grid of 16-wave
+               # workgroups, large grid of 4 waves, K long enough for 8 waves, 9..16 rows)
+               (1, 200, 128), (5, 100, 640), (8, 5120, 2560), (16, 192, 2560), (13, 3000, 4096)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
