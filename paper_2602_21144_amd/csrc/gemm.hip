@@ -429,14 +429,21 @@ hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, 
 
 // Tile shape by a wave-quantisation cost model: whole rounds of 256 workgroups (one per
 // CU) times tile area over the shape's measured efficiency (256x256 does the most MFMA
-// work per LDS byte; 128x128 gives more workgroups when the grid is small).
-bool dma_big_tiles(int64_t M, int64_t N) {
+// work per LDS byte; 128x128 gives more workgroups when the grid is small). 256x320 (4x2
+// waves of 64x160) takes an output whose 256-wide tiles leave the last round part-empty
+// but whose N is a multiple of 320: out_proj of the 2.8B half shard (16384 x 2560) runs
+// 512 of them in 2 rounds instead of 640 256x256 tiles in 3.
+enum DmaTiles { kTiles128 = 0, kTiles256 = 1, kTiles256x320 = 2 };
+DmaTiles dma_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, double eff) {
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         return (double)((tiles + 255) / 256) * bm * bn / eff;
     };
-    return cost(256, 256, 1.0) <= cost(128, 128, 0.83);
+    const double c256 = cost(256, 256, 1.0);
+    if (c256 > cost(128, 128, 0.83)) return kTiles128;
+    return (N % 320 == 0 && cost(256, 320, 1.0) < c256) ? kTiles256x320 : kTiles256;
 }
+bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; }
 
 // Split-K for outputs of fewer tiles than CUs: K is cut into equal slices of whole
 // 64-wide k-tiles (at least two per slice) so that up to ~384 workgroups run; the slices'
@@ -457,8 +464,11 @@ int fit_slices(int sp, int64_t M, int64_t N, size_t scratch_bytes) {
 template <int ROLE, bool CF>
 hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                         void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
-    if (K % 64 == 0 && dma_big_tiles(M, N))
-        return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    if (K % 64 == 0) {
+        const DmaTiles t = dma_tiles(M, N);
+        if (t == kTiles256x320) return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (t == kTiles256) return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    }
     if (K % 64 == 0) {
         const int sp = fit_slices(splitk_slices(((M + 127) / 128) * ((N + 127) / 128), K), M, N, scratch_bytes);
         return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);

@@ -65,6 +65,23 @@ def test_gemm_nt(B, M, N, K, kind):
     assert_close(got, ref, tol, f"gemm {kind} {M}x{N}x{K}")
 
 
+@pytest.mark.parametrize("M,N,K", [(16384, 2560, 128), (16140, 2560, 192)])
+def test_gemm_wide_tiles(B, M, N, K):
+    """Outputs whose 256-wide tiles would leave the last round of CUs part-empty take
+    256x320 tiles when N is a multiple of 320 (the 2.8B half shard's out_proj is
+    16384 x 2560); ragged M included. Rows sampled across every tile row."""
+    rng = np.random.default_rng(M + K)
+    A = _rnd_host(rng, (M, K), "bf16")
+    Bm = _rnd_host(rng, (N, K), "bf16", 1.0 / np.sqrt(K))
+    C = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    B.ssm_gemm_nt(_dev(A, torch.bfloat16), _dev(Bm, torch.bfloat16), C)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(0, M, 97), np.arange(M - 40, M)]))
+    ref = om.round_bf16(A[rows].astype(np.float64) @ Bm.astype(np.float64).T)
+    got = C[torch.from_numpy(rows).cuda()].to(torch.float64).cpu().numpy()
+    assert_close(got, ref, 8e-3, f"gemm {M}x{N}x{K}")
+
+
 SPLITK_SHAPES = [("out_proj", 256, 2560, 5120, False), ("in_proj", 256, 10240, 2560, False),
                  ("x_proj", 300, 192, 5120, True), ("x_proj", 2048, 256, 3584, True), ("in_proj", 100, 5416, 2560, False),
                  ("out_proj", 333, 3584, 3584, False), ("generic", 129, 130, 1024, False), ("x_proj", 65, 80, 1536, True)]
