@@ -13,7 +13,7 @@ namespace ssm {
 namespace {
 
 constexpr int kCV = 8;   // channels per thread
-constexpr int kTT = 16;  // tokens per thread (prefill)
+constexpr int kTT = 8;   // tokens per thread (prefill)
 
 template <typename T> struct Vec8;
 template <> struct Vec8<bf16> {
@@ -39,6 +39,12 @@ template <> struct Vec8<float> {
         *(float4*)(p + 4) = make_float4(o[4], o[5], o[6], o[7]);
     }
 };
+
+// bf16 element i (0..7) of 8 packed in a 16-byte register group, as float
+__device__ __forceinline__ float bf16_lane(const u32x4& v, int i) {
+    const uint32_t d = v[i >> 1];
+    return __uint_as_float((i & 1) ? (d & 0xffff0000u) : (d << 16));
+}
 
 // Index of the sequence holding packed token t: the last s with cu[s] <= t (skips
 // empty sequences). cu is monotone when valid; the search stays within [0, nseq-1].
@@ -69,9 +75,32 @@ __global__ __launch_bounds__(256) void conv_prefill_kernel(ConvArgs a) {
     }
     int s = seq_of(a.cu, a.nseq, t0);
     int64_t s_begin = a.cu[s], s_end = a.cu[s + 1];
+    const int64_t t1 = min(t0 + (int64_t)kTT, a.T);
+    if constexpr (sizeof(T) == 2) {
+        // a whole run inside one sequence whose K-1 earlier rows are inside it too (all but
+        // the runs at sequence starts and ends): every input row of the run is requested
+        // at once and kept as raw bf16, instead of one dependent load per token
+        if (t1 - t0 == kTT && s_begin >= 0 && t0 - (K - 1) >= s_begin && t1 <= s_end) {
+            u32x4 raw[kTT + K - 1];
+#pragma unroll
+            for (int r = 0; r < kTT + K - 1; ++r) raw[r] = *(const u32x4*)(xz + (t0 - (K - 1) + r) * a.ld_xz + c0);
+#pragma unroll
+            for (int t = 0; t < kTT; ++t) {
+                float out[kCV];
+#pragma unroll
+                for (int i = 0; i < kCV; ++i) {
+                    float acc = bias[i];
+#pragma unroll
+                    for (int j = 0; j < K; ++j) acc += w[i][j] * bf16_lane(raw[t + j], i);
+                    out[i] = silu_f(acc);
+                }
+                Vec8<T>::store((T*)a.u + (t0 + t) * a.E + c0, out);
+            }
+            return;
+        }
+    }
     float win[K > 1 ? K - 1 : 1][kCV];  // previous K-1 inputs, oldest first
     bool fresh = true;
-    const int64_t t1 = min(t0 + (int64_t)kTT, a.T);
     for (int64_t t = t0; t < t1; ++t) {
         while (t >= s_end && s + 1 < a.nseq) {
             ++s; s_begin = a.cu[s]; s_end = a.cu[s + 1]; fresh = true;

@@ -6,6 +6,7 @@
 // lane loads 8 consecutive k of one row. bf16 path: v_mfma_f32_32x32x16_bf16 with
 // fp32 accumulation; fp32 path: v_mfma_f32_16x16x4_f32.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -215,9 +216,20 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     constexpr int OPS = AG + BG;
     constexpr int SUB = BK / 16;            // MFMA k-substeps per stage
     static_assert(AG >= 1 && BG >= 1 && NS >= 2, "tile");
+    static_assert(BM % (RPB * NW) == 0 && BN % (RPB * NW) == 0, "tile rows split evenly over the waves' DMA blocks");
     static_assert(SUB % 2 == 0, "fragment sets alternate within a tile");
-    __shared__ __attribute__((aligned(1024))) bf16 As[NS][BM * BK];
-    __shared__ __attribute__((aligned(1024))) bf16 Bs[NS][BN * BK];
+    // one LDS block: the operand ring, reused after the k loop to stage the output tile
+    constexpr int RING = NS * (BM + BN) * BK * 2;
+    using OT = typename std::conditional<C_F32 || SPLIT, float, bf16>::type;
+    // stage the output through LDS (in one or two passes of whole wave rows): whole-line
+    // stores instead of the MFMA layout's 16-byte pieces spread over 32 rows
+    constexpr int PASSES = (BM * BN * (int)sizeof(OT) + RING - 1) / RING;
+    constexpr int RB = BM / PASSES;  // tile rows per pass
+    constexpr bool STAGE = !SPLIT && (BN * (int)sizeof(OT)) % 128 == 0 && PASSES <= 2 && BM % PASSES == 0 &&
+                           RB % (BM / WM) == 0;
+    __shared__ __attribute__((aligned(1024))) char smem[RING];
+    bf16 (*As)[BM * BK] = reinterpret_cast<bf16 (*)[BM * BK]>(smem);
+    bf16 (*Bs)[BN * BK] = reinterpret_cast<bf16 (*)[BN * BK]>(smem + NS * BM * BK * 2);
 
     int tm, tn;
     tile_of(tiles_m, tiles_n, tm, tn);
@@ -326,6 +338,53 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         interleave();
     }
 
+    if constexpr (STAGE) {
+        // tile row r is stored as 16-byte chunks, chunk c at position c ^ (r & 7)
+        constexpr int E16 = 16 / (int)sizeof(OT);   // elements per chunk
+        constexpr int CPR_O = BN / E16;             // chunks per tile row
+        OT* st = reinterpret_cast<OT*>(smem);
+        const bool vec = ((uintptr_t)Cp & 15) == 0 && (ldc * (int64_t)sizeof(OT)) % 16 == 0;
+#pragma unroll
+        for (int pass = 0; pass < PASSES; ++pass) {
+            __syncthreads();  // every wave is done with the ring (then with the previous pass)
+            if (wm * WTM >= pass * RB && wm * WTM < (pass + 1) * RB) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const int r = wm * WTM - pass * RB + i * 32 + (lane & 31);
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int col = wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+                            OT* q = st + r * BN + (((col / E16) ^ (r & 7)) * E16) + col % E16;
+                            const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
+                            const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+                            if constexpr (sizeof(OT) == 4) {
+                                *(float4*)q = make_float4(v0, v1, v2, v3);
+                            } else {
+                                bf16x4 o;
+                                o[0] = (bf16)v0; o[1] = (bf16)v1; o[2] = (bf16)v2; o[3] = (bf16)v3;
+                                *(bf16x4*)q = o;
+                            }
+                        }
+                }
+            }
+            __syncthreads();
+            for (int c = tid; c < RB * CPR_O; c += 64 * NW) {
+                const int r = c / CPR_O, cc = c % CPR_O;
+                const int m = m0 + pass * RB + r, n = n0 + cc * E16;
+                if (m >= M || n >= N) continue;
+                const OT* q = st + r * BN + ((cc ^ (r & 7)) * E16);
+                OT* p = (OT*)Cp + (int64_t)m * ldc + n;
+                if (vec && n + E16 <= N) {
+                    *(u32x4*)p = *(const u32x4*)q;
+                } else {
+                    for (int e = 0; e < E16 && n + e < N; ++e) p[e] = q[e];
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         const int m = m0 + wm * WTM + i * 32 + (lane & 31);
