@@ -686,7 +686,10 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
                          void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
     // Tile by output size: large outputs use 256x256 (each wave 128x128, the most
     // MFMA work per LDS byte), mid-size ones 128x128 for more workgroups.
-    if (M <= 64) {  // few rows: the weight read dominates; stream it with many narrow workgroups
+    // few rows: the weight read dominates; stream it with many narrow workgroups. fp32-A
+    // dt_proj of a large decode batch (K = dt_rank) goes the same way: its staged 128x128
+    // tiles would give only a few workgroups (20 for 256 sequences of a 1280-channel shard)
+    if (M <= 64 || (ROLE == kGemmDtProj && AF && M <= 512 && K <= 512)) {
         SkinnyArgs p{};
         p.A = A; p.lda = lda; p.a_f32 = AF; p.B = (const bf16*)B; p.ldb = ldb; p.C = C; p.ldc = ldc;
         p.M = (int)M; p.N = (int)N; p.K = (int)K;

@@ -324,56 +324,53 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
 }
 
 // ---------------------------------------------------------------- decode
-// One lane per (sequence, channel): one recurrence step on the cached state, in place.
+// One recurrence step on the cached states, in place. Four lanes share a (sequence,
+// channel): lane q holds states 4q..4q+3 as one float4, so a wave reads and writes 16
+// channels x 64 bytes = 1 KB contiguous per instruction (a lane per channel would touch
+// 16 bytes of every 64 across 4 KB). The channel's y is summed over the four lanes by
+// two xor shuffles; the first lane of each group applies the D skip and the gate.
 template <typename T>
 __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= (int64_t)a.nseq * a.E) return;
-    const int b = (int)(gid / a.E), c = (int)(gid % a.E);
+    const int64_t item = gid >> 2;  // (sequence, channel)
+    const int q = (int)(gid & 3);
+    // every lane of a quad takes part in the shuffles: items past the end compute on a
+    // clamped item and store nothing
+    const bool live = item < (int64_t)a.nseq * a.E;
+    const int64_t itc = live ? item : 0;
+    const int b = (int)(itc / a.E), c = (int)(itc % a.E);
     const int slot = a.slot[b];
-    if (slot < 0 || slot >= a.S) {
-        atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-        ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(0.0f);
-        return;
-    }
-    float4* hp = (float4*)(a.pool + ((int64_t)slot * a.E + c) * kN);
-    float h[kN];
-#pragma unroll
-    for (int q = 0; q < kN / 4; ++q) {
-        float4 v = hp[q];
-        h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
-    }
+    const bool slot_ok = slot >= 0 && slot < a.S;
+    float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
+    const float4 h = *hp;
+    const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
+    const float* xb = a.xdbl + (int64_t)b * a.ld_xdbl + a.R;  // B at 0, C at kN (16-byte aligned)
+    const float4 Bq = ((const float4*)xb)[q], Cq = ((const float4*)(xb + kN))[q];
     const float u = to_f32(((const T*)a.u)[(int64_t)b * a.E + c]);
     const float dt = to_f32(((const T*)a.dt)[(int64_t)b * a.E + c]);
     const float z = to_f32(((const T*)a.z)[(int64_t)b * a.ld_z + c]);
-    // B_t and C_t of this sequence (the same for all its channels) and the channel's A_log,
-    // as 16-byte loads (ld_xdbl and R are multiples of 4 floats)
-    const float4* bt4 = (const float4*)(a.xdbl + (int64_t)b * a.ld_xdbl + a.R);
-    const float4* al4 = (const float4*)(a.A_log + (int64_t)c * kN);
-    float bc[2 * kN], al[kN];
-#pragma unroll
-    for (int q = 0; q < 2 * kN / 4; ++q) {
-        const float4 v = bt4[q];
-        bc[4 * q] = v.x; bc[4 * q + 1] = v.y; bc[4 * q + 2] = v.z; bc[4 * q + 3] = v.w;
-    }
-#pragma unroll
-    for (int q = 0; q < kN / 4; ++q) {
-        const float4 v = al4[q];
-        al[4 * q] = v.x; al[4 * q + 1] = v.y; al[4 * q + 2] = v.z; al[4 * q + 3] = v.w;
-    }
     const float delta = softplus_f(dt + a.b_dt[c]);
     const float du = delta * u;
-    float y = 0.0f;
+    const float hv[4] = {h.x, h.y, h.z, h.w}, av[4] = {al.x, al.y, al.z, al.w};
+    const float bv[4] = {Bq.x, Bq.y, Bq.z, Bq.w}, cv[4] = {Cq.x, Cq.y, Cq.z, Cq.w};
+    float hn[4], y = 0.0f;
 #pragma unroll
-    for (int n = 0; n < kN; ++n) {
-        const float A2 = -__expf(al[n]) * kLog2e;
-        h[n] = fast_exp2(delta * A2) * h[n] + du * bc[n];
-        y += bc[kN + n] * h[n];
+    for (int i = 0; i < 4; ++i) {
+        hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
+        y += cv[i] * hn[i];
     }
-    y += a.D[c] * u;
-#pragma unroll
-    for (int q = 0; q < kN / 4; ++q) hp[q] = make_float4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
-    ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(y * silu_f(z));
+    y += __shfl_xor(y, 1);
+    y += __shfl_xor(y, 2);
+    if (!live) return;
+    if (!slot_ok) {
+        if (q == 0) {
+            atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+            ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(0.0f);
+        }
+        return;
+    }
+    *hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
+    if (q == 0) ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>((y + a.D[c] * u) * silu_f(z));
 }
 
 }  // namespace
@@ -451,7 +448,7 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
 }
 
 hipError_t launch_decode_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
-    const int64_t lanes = (int64_t)a.nseq * a.E;
+    const int64_t lanes = (int64_t)a.nseq * a.E * 4;
     if (lanes <= 0) return hipSuccess;
     const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
     if (bf) SSM_LAUNCH(decode_ssm_kernel<bf16>, grid, block, 0, s, a);
