@@ -511,6 +511,14 @@ __global__ __launch_bounds__(256) void ssd_decode_kernel(SsdArgs a, int batch) {
     const float dA = __expf(d * -__expf(a.A_log[h]));
     const float x = (float)urow[h * kP + p];
     float* st = a.pool + (((int64_t)(ok ? slot : 0) * a.H + h) * kP + p) * kS + n0;
+    // this thread's 32 entries of B_t and C_t, as 16-byte loads (b_col, c_col and ld_u are
+    // multiples of 8 elements)
+    bf16x8 bv[4], cv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        bv[q] = *(const bf16x8*)(urow + a.b_col + grp * kS + n0 + 8 * q);
+        cv[q] = *(const bf16x8*)(urow + a.c_col + grp * kS + n0 + 8 * q);
+    }
     float acc = 0.0f;
 #pragma unroll
     for (int q = 0; q < 32; q += 4) {
@@ -518,9 +526,9 @@ __global__ __launch_bounds__(256) void ssd_decode_kernel(SsdArgs a, int batch) {
         float sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int n = n0 + q + k;
-            sv[k] = dA * sv[k] + d * x * (float)urow[a.b_col + grp * kS + n];
-            acc += sv[k] * (float)urow[a.c_col + grp * kS + n];
+            const int i = q + k;
+            sv[k] = dA * sv[k] + d * x * (float)bv[i >> 3][i & 7];
+            acc += sv[k] * (float)cv[i >> 3][i & 7];
         }
         if (ok) *(float4*)(st + q) = make_float4(sv[0], sv[1], sv[2], sv[3]);
     }
