@@ -299,6 +299,9 @@ def run(args):
     if not args.no_ablation:
         log("cache vs no-cache generation through a 64-layer stack (outside the timed region)")
         result["ablation"] = ablation_figures(B, torch)
+    if not args.no_decode_heavy:
+        log("decode-heavy step: 256 cached sequences on the 2.8B quarter shard (outside the timed region)")
+        result["decode_heavy"] = decode_heavy_figures(B, torch)
     return result, (sh, full, x_host, xdec_host, slots, S)
 
 
@@ -397,6 +400,85 @@ def mamba2_figures(B, torch, steps, warmup):
             "ssd_main": {"avg_us": round(main_s * 1e6, 3), "TFLOP_per_s": round(flops / main_s / 1e12, 1),
                          "GB_per_s": round(nbytes / main_s / 1e9, 1), "flops": flops, "bytes": nbytes},
             "kernels": kernels}
+
+
+def decode_heavy_figures(B, torch, steps=64):
+    """Decode-heavy serving step on the Mamba-2.8B quarter shard (1280 of 5120 channels,
+    d_model 2560): 256 sequences holding cached states, one single-token step each. Above
+    128 sequences the step runs tiled projections, the conv-step kernel and the state-step
+    kernel, whose traffic is the state cache (read and written once: 2 B E N 4 bytes).
+    Weights are drawn on the GPU with the one-layer recipe; the cache pools hold seeded
+    random values (the timing does not depend on them); the other shards' x_proj partial
+    (their GPUs' work) is precomputed, as in the headline step."""
+    import math
+    import numpy as np
+    from paper_2602_21144_amd import synth
+    cfg = synth.CONFIGS["mamba2.8b_tp4_decode"]
+    sh, Bd = cfg["shape"], cfg["batch"]
+    E, dm, N, R, K, W = sh.d_shard, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv, sh.w_dbl
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(cfg["seed"])
+
+    def nrm(*size, std=0.02):
+        return (torch.randn(*size, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    lo, hi = math.log(1e-3), math.log(0.1)
+    dt0 = torch.exp(torch.rand(E, generator=g, device=dev) * (hi - lo) + lo)
+    w = {"W_in": nrm(2 * E, dm), "conv_w": nrm(E, K), "conv_b": nrm(E), "W_x": nrm(W, E), "W_dt": nrm(E, R),
+         "W_out": nrm(dm, E), "b_dt": (dt0 + torch.log(-torch.expm1(-dt0))).float(),
+         "A_log": torch.log(torch.arange(1, N + 1, device=dev, dtype=torch.float32)).repeat(E, 1).contiguous(),
+         "D": torch.ones(E, device=dev)}
+    ws_ = B.weights_struct(w)
+    d = B.make_desc(sh, 0)
+    S = Bd + 16
+    slots = torch.from_numpy(synth.make_slots(np.random.default_rng(cfg["seed"]), Bd)).to(dev)
+    conv = nrm(S, E, K - 1, std=1.0)
+    ssm = torch.randn(S, E, N, generator=g, device=dev) * 0.5
+    wsd = B.workspace(B.decode_workspace_bytes(d, Bd), dev)
+    xs = [nrm(Bd, dm, std=1.0) for _ in range(steps)]
+    q0 = torch.empty(Bd, W, dtype=torch.float32, device=dev)
+    other = torch.randn(Bd, W, generator=g, device=dev) * 0.1
+    y = torch.empty(Bd, dm, dtype=torch.bfloat16, device=dev)
+    calls = [(B.bind("ssm_shard_decode_stage1", d, ws_, xs[k], slots, conv, q0, wsd),
+              B.bind("ssm_reduce_add_f32", q0, other),
+              B.bind("ssm_shard_decode_stage2", d, ws_, q0, slots, ssm, y, wsd)) for k in range(steps)]
+
+    def run():
+        for cs in calls:
+            for c in cs:
+                c()
+    run()
+    torch.cuda.synchronize()
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True)
+    run()
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    bd = B.ssm_timing_collect()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    run()
+    ev[1].record()
+    torch.cuda.synchronize()
+    assert B.take_status(wsd) == 0
+    step_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
+    state_bytes = 2 * Bd * E * N * 4 + 4 * Bd * E * 2 + Bd * 2 * N * 4 + E * (N + 2) * 4
+    weight_bytes = (2 * E * dm + W * E + E * R + dm * E) * 2
+    step_bytes = weight_bytes + state_bytes + 2 * Bd * E * (K - 1) * 2 + Bd * (dm + 2 * E + W * 4 + dm) * 2
+    st = bd.get("decode.state_update", (1, float("nan")))
+    st_us = 1e3 * st[1] / st[0]
+    return {"workload": "Mamba-2.8B-shaped layer, shard 0 of a 4-way channel split (d_model 2560, 1280 of 5120 "
+                        "channels, d_state 16, dt_rank 160, d_conv 4): 256 sequences with cached states, one "
+                        "single-token decode step each; bf16, fp32 state; seed 3",
+            "decode_us_per_step": round(step_us, 3),
+            "step_bytes": step_bytes, "step_GBps": round(step_bytes / (step_us * 1e-6) / 1e9, 1),
+            "step_frac_hbm": round(step_bytes / (step_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "state_kernel": {"avg_us": round(st_us, 3), "bytes": state_bytes,
+                             "GBps": round(state_bytes / (st_us * 1e-6) / 1e9, 1),
+                             "frac_hbm": round(state_bytes / (st_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
+            "kernels": {k: {"launches": n, "avg_us": round(1e3 * ms / n, 3)}
+                        for k, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][1])}}
 
 
 def device_stack_weights(torch, sh, n_layers, seed, dev):
@@ -592,6 +674,7 @@ def main():
     ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
     ap.add_argument("--no-mamba2", action="store_true", help="skip the Mamba-2 (SSD) shard figures")
     ap.add_argument("--no-ablation", action="store_true", help="skip the cache vs no-cache generation figures")
+    ap.add_argument("--no-decode-heavy", action="store_true", help="skip the 256-sequence decode step figures")
     ap.add_argument("--mamba2-only", action="store_true",
                     help="print only the Mamba-2 (SSD) shard figures (its own kernel profile; the headline step "
                          "shares kernel names with it)")
