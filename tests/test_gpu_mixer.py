@@ -44,8 +44,11 @@ def _slice(a, r, E):
 @pytest.mark.parametrize("act", ["f32", "bf16"])
 @pytest.mark.parametrize("P", [1, 2])
 @pytest.mark.parametrize("init", ["baseline", "stress", "general"])
-def test_prefill_then_decode(act, P, init):
-    shape, full = _case(act, P, init, seed=3)
+# dt rank 16: dt_proj on the staged tiles with fp32 A (rounded on load); dt rank 32 with 192
+# channels per shard: delta rounded once, then DMA-fed tiles over a ragged last 128-column tile
+@pytest.mark.parametrize("dims", [(256, 16), (384, 32)])
+def test_prefill_then_decode(act, P, init, dims):
+    shape, full = _case(act, P, init, seed=3, E_tot=dims[0], R=dims[1])
     E = shape.d_shard
     rng = np.random.default_rng(17)
     lens = [37, 1, 0, 130, 2, 64, 3]
