@@ -287,10 +287,10 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
     if (adt == SSM_BF16 && d->d_conv >= 2 && B <= kFusedDecodeMax) {
         // in_proj with the conv window shift + SiLU fused into its epilogue; x_proj
-        SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, nullptr, 0, B, 2 * E, dm);
+        SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, L.xz, 2 * E, B, 2 * E, dm);
         p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
         p.conv_w = w->conv_w; p.conv_b = w->conv_b; p.conv_pool = conv_pool; p.Kc = d->d_conv;
-        p.u = L.u; p.z = L.xz + E * act_bytes(d); p.ld_z = 2 * E;
+        p.conv_lo = 0; p.conv_n = (int)E; p.u = L.u;
         SkinnyArgs q = skinny(L.u, E, false, w->x_proj_w, E, xdbl, W, B, W, E);
         SSM_SKINNY("decode.in_proj_conv", s, p, kSkinnyConv);
         SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
@@ -963,10 +963,19 @@ int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weight
     SSM_TRY(check_ptr(conv_pool, "conv_pool"));
     SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
     SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
-    SSM_TRY(gemm(B, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
-                 "m2.decode.in_proj", kGemmInProj, L.splitk));
-    ConvArgs ca = m2_conv(m, w, L, B, nullptr, slot, nullptr, B, conv_pool, S);
-    SSM_TIMED("m2.decode.conv", s, launch_conv_decode(ca, true, s));
+    if (B <= kFusedDecodeMax) {
+        // in_proj with the conv window shift + SiLU of the x, B, C columns in its epilogue
+        SkinnyArgs p = skinny(x, m.dm, false, w->in_proj_w, m.dm, L.zx, m.rows, B, m.rows, m.dm);
+        p.slot = slot; p.S = S; p.status = L.status;
+        p.conv_w = w->conv_w; p.conv_b = w->conv_b; p.conv_pool = conv_pool; p.Kc = (int)m.K;
+        p.conv_lo = (int)m.E; p.conv_n = (int)m.Cc; p.u = L.u;
+        SSM_SKINNY("m2.decode.in_proj_conv", s, p, kSkinnyConv);
+    } else {
+        SSM_TRY(gemm(B, m.rows, m.dm, x, m.dm, SSM_BF16, w->in_proj_w, m.dm, SSM_BF16, L.zx, m.rows, SSM_BF16, s,
+                     "m2.decode.in_proj", kGemmInProj, L.splitk));
+        ConvArgs ca = m2_conv(m, w, L, B, nullptr, slot, nullptr, B, conv_pool, S);
+        SSM_TIMED("m2.decode.conv", s, launch_conv_decode(ca, true, s));
+    }
     SsdPublic p = m2_ssd(m, w, L, ssm_pool, S, L.status);
     p.slot = slot;
     SSM_TIMED("m2.decode.state", s, launch_ssd_decode(p, B, s));

@@ -107,9 +107,12 @@ struct SkinnyArgs {
     int M, N, K;
     const int32_t* slot; int S; int32_t* status;  // per-row cache slot (fused epilogues)
     int E;                                        // channels of the shard
-    // kSkinnyConv (in_proj): conv weights, history pool, u out, gate values out
-    const void* conv_w; const void* conv_b; void* conv_pool; int Kc; void* u; void* z; int64_t ld_z;
+    // kSkinnyConv (in_proj): columns [conv_lo, conv_lo + conv_n) go through the cached conv
+    // window (weights [conv_n][Kc], history pool [S][conv_n][Kc - 1]) into u [M][conv_n];
+    // the other columns are stored to C in bf16
+    const void* conv_w; const void* conv_b; void* conv_pool; int Kc; int conv_lo, conv_n; void* u;
     // kSkinnyState (dt_proj): B and C in xdbl, per-channel parameters, state pool, g out (u, z in)
+    void* z; int64_t ld_z;
     const float* xdbl; int64_t ld_xdbl; int R; const float* b_dt; const float* A_log; const float* D;
     float* pool; void* g;
 };

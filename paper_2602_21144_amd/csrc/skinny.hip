@@ -10,8 +10,8 @@
 //
 // Epilogues fuse the per-channel work that follows each projection in a decode step
 // (Section IV-A: the cache is read and advanced in place, with no prefix rescan):
-//   kEpiConv  (in_proj): SSM-path columns go through the cached conv window + SiLU
-//             (window shifted in place), gate-path columns are stored for the gate;
+//   kEpiConv  (in_proj): conv-path columns go through the cached conv window + SiLU
+//             (window shifted in place), the other columns (gate, Mamba-2's dt) are stored;
 //   kEpiState (dt_proj): Delta = softplus(dt + b_dt), one recurrence step on the cached
 //             state in place, D skip and SiLU gate -> g;
 //   kEpiStore: plain store (x_proj in fp32, out_proj in bf16).
@@ -56,7 +56,8 @@ template <int EPI> struct EpiIn {
 
 __device__ __forceinline__ bool slot_ok(int slot, int S) { return slot >= 0 && slot < S; }
 
-// in_proj: column n < E is channel n of the SSM path (conv window), n >= E the gate.
+// in_proj: column n in [conv_lo, conv_lo + conv_n) is channel n - conv_lo of the conv path
+// (Mamba: the SSM half; Mamba-2: x, B and C), every other column is stored as it is.
 // Needs 2 <= d_conv <= 4 (at least one cached tap).
 template <> struct EpiIn<kEpiConv> {
     int slot;
@@ -64,15 +65,16 @@ template <> struct EpiIn<kEpiConv> {
     __device__ __forceinline__ void load_slot(const SkinnyArgs& p, int m) { slot = p.slot[m]; }
     __device__ __forceinline__ void load(const SkinnyArgs& p, int, int n) {
         const int K = p.Kc;
-        const int c = n < p.E ? n : 0;  // gate columns read channel 0 and ignore it
+        const int c = n - p.conv_lo;
+        const int cc = c >= 0 && c < p.conv_n ? c : 0;  // stored columns read channel 0 and ignore it
         const int sc = slot_ok(slot, p.S) ? slot : 0;
-        const bf16* hist = (const bf16*)p.conv_pool + ((int64_t)sc * p.E + c) * (K - 1);
-        const bf16* wr = (const bf16*)p.conv_w + (int64_t)c * K;
+        const bf16* hist = (const bf16*)p.conv_pool + ((int64_t)sc * p.conv_n + cc) * (K - 1);
+        const bf16* wr = (const bf16*)p.conv_w + (int64_t)cc * K;
 #pragma unroll
         for (int j = 0; j < kMaxConv; ++j) w[j] = (float)wr[j < K ? j : K - 1];
 #pragma unroll
         for (int j = 0; j < kMaxConv - 1; ++j) hv[j] = (float)hist[j < K - 1 ? j : K - 2];
-        bias = (float)((const bf16*)p.conv_b)[c];
+        bias = (float)((const bf16*)p.conv_b)[cc];
         wlast = 0.0f;
 #pragma unroll
         for (int j = 0; j < kMaxConv; ++j) {
@@ -83,13 +85,15 @@ template <> struct EpiIn<kEpiConv> {
         for (int j = 0; j < kMaxConv - 1; ++j) hv[j] = j < K - 1 ? hv[j] : 0.0f;
     }
     __device__ __forceinline__ void apply(const SkinnyArgs& p, int m, int n, float v) const {
-        if (n >= p.E) {
-            ((bf16*)p.z)[(int64_t)m * p.ld_z + (n - p.E)] = (bf16)v;
+        const int c = n - p.conv_lo;
+        if (c < 0 || c >= p.conv_n) {
+            ((bf16*)p.C)[(int64_t)m * p.ldc + n] = (bf16)v;
             return;
         }
+        bf16* u = (bf16*)p.u + (int64_t)m * p.conv_n + c;
         if (!slot_ok(slot, p.S)) {
             atomicOr(p.status, SSM_STATUS_BAD_SLOT);
-            ((bf16*)p.u)[(int64_t)m * p.E + n] = (bf16)0.0f;
+            *u = (bf16)0.0f;
             return;
         }
         const int K = p.Kc;
@@ -99,8 +103,8 @@ template <> struct EpiIn<kEpiConv> {
         for (int j = 0; j < kMaxConv - 1; ++j)
             if (j < K - 1) acc += w[j] * hv[j];
         acc += wlast * x;
-        ((bf16*)p.u)[(int64_t)m * p.E + n] = (bf16)silu_f(acc);
-        bf16* hist = (bf16*)p.conv_pool + ((int64_t)slot * p.E + n) * (K - 1);
+        *u = (bf16)silu_f(acc);
+        bf16* hist = (bf16*)p.conv_pool + ((int64_t)slot * p.conv_n + c) * (K - 1);
 #pragma unroll
         for (int j = 0; j < kMaxConv - 2; ++j)
             if (j < K - 2) hist[j] = (bf16)hv[j + 1];

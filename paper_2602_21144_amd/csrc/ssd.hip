@@ -498,58 +498,73 @@ __global__ __launch_bounds__(256) void ssd_head_sumsq_kernel(const bf16* __restr
 }
 
 // ---------------------------------------------------------------- decode
-// one workgroup per (sequence, head): 4 lanes per row p of the state, 32 states each
-__global__ __launch_bounds__(256) void ssd_decode_kernel(SsdArgs a, int batch) {
+// one workgroup per (sequence, head), 8 lanes per row p of the state: lane q holds the
+// float4 groups at n = 32 j + 4 q (j = 0..3), so each load and store instruction of a wave
+// covers 8 whole rows' 128-byte lines. Everything that does not depend on the cache slot
+// (dt, x, z, the head's parameters, B_t, C_t) is fetched before the slot-addressed states.
+__global__ __launch_bounds__(512) void ssd_decode_kernel(SsdArgs a) {
     const int b = blockIdx.x, h = blockIdx.y;
-    const int tid = threadIdx.x, p = tid >> 2, n0 = (tid & 3) * 32;
-    __shared__ float ysq[4];
+    const int tid = threadIdx.x, p = tid >> 3, q = tid & 7;
+    __shared__ float ysq[8];
     const int slot = a.slot[b];
-    const bool ok = slot >= 0 && slot < a.S;
     const bf16* urow = a.u + (int64_t)b * a.ld_u;
+    const bf16* zrow = a.zx + (int64_t)b * a.ld_zx;
     const int grp = (a.h_global0 + h) / a.hpg - a.g_off;
-    const float d = softplus_dev((float)a.zx[(int64_t)b * a.ld_zx + a.dt_col + h] + a.dt_bias[h]);
-    const float dA = __expf(d * -__expf(a.A_log[h]));
+    const float dtv = (float)zrow[a.dt_col + h], zv = (float)zrow[h * kP + p];
     const float x = (float)urow[h * kP + p];
-    float* st = a.pool + (((int64_t)(ok ? slot : 0) * a.H + h) * kP + p) * kS + n0;
-    // this thread's 32 entries of B_t and C_t, as 16-byte loads (b_col, c_col and ld_u are
-    // multiples of 8 elements)
-    bf16x8 bv[4], cv[4];
+    const float dtb = a.dt_bias[h], alog = a.A_log[h], Dh = a.D[h];
+    // B_t and C_t at this lane's n: 8-byte loads (b_col, c_col and ld_u are multiples of 8)
+    bf16x4 bv[4], cv[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        bv[q] = *(const bf16x8*)(urow + a.b_col + grp * kS + n0 + 8 * q);
-        cv[q] = *(const bf16x8*)(urow + a.c_col + grp * kS + n0 + 8 * q);
+    for (int j = 0; j < 4; ++j) {
+        bv[j] = *(const bf16x4*)(urow + a.b_col + grp * kS + 32 * j + 4 * q);
+        cv[j] = *(const bf16x4*)(urow + a.c_col + grp * kS + 32 * j + 4 * q);
     }
+    const bool ok = slot >= 0 && slot < a.S;
+    // a slot outside the pool reads slot 0 (in range) and discards it
+    float4* st = (float4*)(a.pool + (((int64_t)(ok ? slot : 0) * a.H + h) * kP + p) * kS) + q;
+    float4 s4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s4[j] = st[8 * j];
+    const float d = softplus_dev(dtv + dtb);
+    const float dA = __expf(d * -__expf(alog)), dx = d * x;
     float acc = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 32; q += 4) {
-        float4 s4 = ok ? *(const float4*)(st + q) : make_float4(0.f, 0.f, 0.f, 0.f);
-        float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+    for (int j = 0; j < 4; ++j) {
+        float sv[4] = {s4[j].x, s4[j].y, s4[j].z, s4[j].w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int i = q + k;
-            sv[k] = dA * sv[k] + d * x * (float)bv[i >> 3][i & 7];
-            acc += sv[k] * (float)cv[i >> 3][i & 7];
+            sv[k] = dA * sv[k] + dx * (float)bv[j][k];
+            acc += sv[k] * (float)cv[j][k];
         }
-        if (ok) *(float4*)(st + q) = make_float4(sv[0], sv[1], sv[2], sv[3]);
+        s4[j] = make_float4(sv[0], sv[1], sv[2], sv[3]);
+    }
+    if (ok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st[8 * j] = s4[j];
     }
     acc += __shfl_xor(acc, 1, 64);
     acc += __shfl_xor(acc, 2, 64);
-    const float y = acc + a.D[h] * x;
-    const bf16 gv = ok ? (bf16)(y * silu_f((float)a.zx[(int64_t)b * a.ld_zx + h * kP + p])) : (bf16)0.0f;
+    acc += __shfl_xor(acc, 4, 64);
+    const float y = acc + Dh * x;
+    const bf16 gv = ok ? (bf16)(y * silu_f(zv)) : (bf16)0.0f;
     float sq = 0.0f;
-    if ((tid & 3) == 0) {
+    if (q == 0) {
         a.g[(int64_t)b * a.E + h * kP + p] = gv;
         sq = (float)gv * (float)gv;
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) sq += __shfl_xor(sq, off, 64);
+    sq += __shfl_xor(sq, 8, 64);
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
     if ((tid & 63) == 0) ysq[tid >> 6] = sq;
     __syncthreads();
     if (tid == 0) {
-        a.hs[(int64_t)b * a.H + h] = ysq[0] + ysq[1] + ysq[2] + ysq[3];
+        float hsum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) hsum += ysq[w];
+        a.hs[(int64_t)b * a.H + h] = hsum;
         if (!ok) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
     }
-    (void)batch;
 }
 
 // ---------------------------------------------------------------- norm
@@ -561,9 +576,20 @@ __global__ __launch_bounds__(256) void ssd_group_sumsq_kernel(const float* __res
     if (i >= T * G) return;
     const int64_t t = i / G;
     const int k = (int)(i % G);
+    // the shard's heads in group k are the global heads [k hpg, (k + 1) hpg); blocks of 8
+    // loads go out together and are added in ascending head order
+    const int h0 = max(0, k * hpg - h_global0), h1 = min(H, (k + 1) * hpg - h_global0);
+    const float* r = hs + t * H;
     float s = 0.0f;
-    for (int h = 0; h < H; ++h)
-        if ((h_global0 + h) / hpg == k) s += hs[t * H + h];
+    int h = h0;
+    for (; h + 8 <= h1; h += 8) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = r[h + e];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += v[e];
+    }
+    for (; h < h1; ++h) s += r[h];
     out[i] = s;
 }
 
@@ -643,7 +669,7 @@ hipError_t launch_ssd_decode(const SsdPublic& p, int batch, hipStream_t s) {
     a.h_global0 = p.h_global0; a.hpg = p.hpg; a.g_off = p.g_off;
     a.dt_bias = p.dt_bias; a.A_log = p.A_log; a.D = p.D;
     a.g = (bf16*)p.g; a.hs = p.hs; a.pool = p.pool; a.slot = p.slot; a.status = p.status; a.S = p.S;
-    SSM_LAUNCH(ssd_decode_kernel, dim3((unsigned)batch, (unsigned)a.H), dim3(256), 0, s, a, batch);
+    SSM_LAUNCH(ssd_decode_kernel, dim3((unsigned)batch, (unsigned)a.H), dim3(512), 0, s, a);
     return hipGetLastError();
 }
 

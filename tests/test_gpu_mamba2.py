@@ -167,6 +167,41 @@ def test_m2_windows_of_several_chunks():
     _run_case(sh, full, [9000, 333], np.array([1, 0], np.int32), seed=3, decode_steps=2)
 
 
+# decode batches on each in_proj route: up to 16 sequences on the streamed kernel and up to
+# 128 on the fragment kernel, both with the conv window in the in_proj epilogue; above
+# 128 in_proj, then the conv step as its own kernel
+@pytest.mark.parametrize("Bd", [5, 16, 40, 128, 129])
+def test_m2_decode_batches(Bd):
+    """Decode steps straight from random caches (no prefill) for a batch of sequences in
+    scattered slots; outputs, states and the conv history against the oracle each step."""
+    sh = synth.Mamba2Shape(256, 16, 64, 128, 2, 4, 2, "bf16")
+    full = synth.make_mamba2_layer(sh, 40 + Bd)
+    rng = np.random.default_rng(Bd)
+    S = Bd + 7
+    slots = rng.permutation(S)[:Bd].astype(np.int32)
+    cp0, sp0 = _rand_pools(rng, sh, S)
+    g = GpuLayer2(sh, full)
+    conv, ssm = g.new_pools(S)
+    for r in range(sh.shard_count):
+        conv[r].copy_(torch.from_numpy(cp0[r]).cuda().to(torch.bfloat16))
+        ssm[r].copy_(torch.from_numpy(sp0[r]).cuda())
+    f64 = _f64(full)
+    cps = [c.astype(np.float64) for c in cp0]
+    sps = [s.astype(np.float64) for s in sp0]
+    sl = torch.from_numpy(slots).cuda()
+    for step in range(2):
+        xt = synth.make_tokens(rng, Bd, sh.d_model, "bf16")
+        yd = g.decode(xt, sl, conv, ssm)
+        assert g.status_ok(g.dws)
+        d1, ydr = o2.tp_decode_step(f64, sh, xt.astype(np.float64), slots, cps, sps, "bf16")
+        cps = [d["conv_pool"] for d in d1]
+        sps = [d["ssm_pool"] for d in d1]
+        for r in range(sh.shard_count):
+            assert_close(host(yd[r]), ydr[r], TOL["bf16"], f"decode step {step} shard {r}")
+            assert_close(host(conv[r]), cps[r], TOL["bf16"], f"conv history step {step} shard {r}")
+            assert_close(host(ssm[r]), sps[r], STATE_TOL, f"states step {step} shard {r}")
+
+
 def test_m2_empty_batch_and_bad_slot():
     from paper_2602_21144_amd import binding as B
     sh = synth.Mamba2Shape(128, 8, 64, 128, 1, 4, 1, "bf16")
