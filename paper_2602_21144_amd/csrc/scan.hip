@@ -155,15 +155,20 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
             st.load(a, b0 + kTB, w1, tid, kWave * CW);
         }
         const int nt = rows_upto(w1 - b0, kTB);
+        auto step = [&](int i) {
+            const float delta = softplus_f(to_f32(cur.dt[i]) + bdt);
+            const float du = delta * to_f32(cur.u[i]);
+            sum_delta += delta;
 #pragma unroll
-        for (int i = 0; i < kTB; ++i) {
-            if (i < nt) {
-                const float delta = softplus_f(to_f32(cur.dt[i]) + bdt);
-                const float du = delta * to_f32(cur.u[i]);
-                sum_delta += delta;
+            for (int n = 0; n < kN; ++n) h[n] = fast_exp2(delta * A2[n]) * h[n] + du * bc[buf][i][n];
+        };
+        if (nt == kTB) {
 #pragma unroll
-                for (int n = 0; n < kN; ++n) h[n] = fast_exp2(delta * A2[n]) * h[n] + du * bc[buf][i][n];
-            }
+            for (int i = 0; i < kTB; ++i) step(i);
+        } else {
+#pragma unroll
+            for (int i = 0; i < kTB; ++i)
+                if (i < nt) step(i);
         }
         if (more) st.store(bc[buf ^ 1], tid);
         __syncthreads();
@@ -272,11 +277,19 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
         const int nt = rows_upto(w1 - b0, kTB);
         if (ok && s_end >= b0 + nt) {
             // no sequence ends inside this block: straight-line recurrence from registers
+            // (a whole block without per-token guards, so the states stay in place)
+            auto step = [&](int i) {
+                g[(b0 + i) * a.E + c] = from_f32<T>(token_step(h, A2, to_f32(cur.u[i]), to_f32(cur.dt[i]),
+                                                               to_f32(cur.z[i]), bdt, Dc, bc[buf][i]));
+            };
+            if (nt == kTB) {
 #pragma unroll
-            for (int i = 0; i < kTB; ++i)
-                if (i < nt)
-                    g[(b0 + i) * a.E + c] = from_f32<T>(token_step(h, A2, to_f32(cur.u[i]), to_f32(cur.dt[i]),
-                                                                   to_f32(cur.z[i]), bdt, Dc, bc[buf][i]));
+                for (int i = 0; i < kTB; ++i) step(i);
+            } else {
+#pragma unroll
+                for (int i = 0; i < kTB; ++i)
+                    if (i < nt) step(i);
+            }
         } else if (ok) {
             // a sequence ends in this block: store its state, start the next one (empty
             // sequences are left to the link pass); operands are re-read by token index
