@@ -182,7 +182,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
 }
 
 // bf16 operands, K a multiple of BK: tiles move global -> LDS on the DMA path
-// (global_load_lds_dwordx4: each lane writes 16 bytes at its lane slot of a 1 KB LDS
+// (buffer_load_dwordx4 ... lds: each lane writes 16 bytes at its lane slot of a 1 KB LDS
 // block), so there are no staging registers and no ds_write instructions. A lane picks
 // the global chunk that belongs at its slot under the XOR swizzle. The LDS holds a ring
 // of NS stages: tile k+NS-1 is in flight while tile k is multiplied, which covers
@@ -242,17 +242,20 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     }
 
     const int lr = lane / CPR, lp = lane % CPR;
-    const bf16* asrc[AG];
-    const bf16* bsrc[BG];
+    // the tile's row panels as buffer resources; a lane's chunk is a fixed byte offset in
+    // them and the k advance goes in the scalar offset
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A + (int64_t)m0 * lda, (uint32_t)((int64_t)min(BM, M - m0) * lda * 2));
+    const __amdgpu_buffer_rsrc_t rbr = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)((int64_t)min(BN, N - n0) * ldb * 2));
+    uint32_t aoff[AG], boff[BG];
 #pragma unroll
     for (int q = 0; q < AG; ++q) {
         const int r = (wave * AG + q) * RPB + lr;
-        asrc[q] = A + (int64_t)min(m0 + r, M - 1) * lda + swz_k<BK>(r, lp) * 8;
+        aoff[q] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * lda + swz_k<BK>(r, lp) * 8) * 2);
     }
 #pragma unroll
     for (int q = 0; q < BG; ++q) {
         const int r = (wave * BG + q) * RPB + lr;
-        bsrc[q] = B + (int64_t)min(n0 + r, N - 1) * ldb + swz_k<BK>(r, lp) * 8;
+        boff[q] = (uint32_t)(((int64_t)(min(n0 + r, N - 1) - n0) * ldb + swz_k<BK>(r, lp) * 8) * 2);
     }
     const uint32_t a_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&As[0][0];
     const uint32_t b_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&Bs[0][0];
@@ -260,10 +263,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         const int k0 = kt * BK;
 #pragma unroll
         for (int q = 0; q < AG; ++q)
-            dma16(asrc[q] + k0, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + q) * RPB) * BK * 2)));
+            dma16(ra, aoff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + q) * RPB) * BK * 2)));
 #pragma unroll
         for (int q = 0; q < BG; ++q)
-            dma16(bsrc[q] + k0, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + q) * RPB) * BK * 2)));
+            dma16(rbr, boff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + q) * RPB) * BK * 2)));
     };
 
     f32x16 acc[TM][TN];
