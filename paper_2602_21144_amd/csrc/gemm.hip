@@ -225,7 +225,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     // stores instead of the MFMA layout's 16-byte pieces spread over 32 rows
     constexpr int PASSES = (BM * BN * (int)sizeof(OT) + RING - 1) / RING;
     constexpr int RB = BM / PASSES;  // tile rows per pass
-    constexpr bool STAGE = !SPLIT && (BN * (int)sizeof(OT)) % 128 == 0 && PASSES <= 2 && BM % PASSES == 0 &&
+    constexpr bool STAGE = (BN * (int)sizeof(OT)) % 128 == 0 && PASSES <= 2 && BM % PASSES == 0 &&
                            RB % (BM / WM) == 0;
     __shared__ __attribute__((aligned(1024))) char smem[RING];
     bf16 (*As)[BM * BK] = reinterpret_cast<bf16 (*)[BM * BK]>(smem);
@@ -346,7 +346,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         constexpr int E16 = 16 / (int)sizeof(OT);   // elements per chunk
         constexpr int CPR_O = BN / E16;             // chunks per tile row
         OT* st = reinterpret_cast<OT*>(smem);
-        const bool vec = ((uintptr_t)Cp & 15) == 0 && (ldc * (int64_t)sizeof(OT)) % 16 == 0;
+        // a K-slice's fp32 partial goes to part[blockIdx.y] (row stride N), the output to C
+        OT* const out = SPLIT ? reinterpret_cast<OT*>(part + (int64_t)blockIdx.y * M * N) : (OT*)Cp;
+        const int64_t ldo = SPLIT ? (int64_t)N : ldc;
+        const bool vec = ((uintptr_t)out & 15) == 0 && (ldo * (int64_t)sizeof(OT)) % 16 == 0;
 #pragma unroll
         for (int pass = 0; pass < PASSES; ++pass) {
             __syncthreads();  // every wave is done with the ring (then with the previous pass)
@@ -378,7 +381,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
                 const int m = m0 + pass * RB + r, n = n0 + cc * E16;
                 if (m >= M || n >= N) continue;
                 const OT* q = st + r * BN + ((cc ^ (r & 7)) * E16);
-                OT* p = (OT*)Cp + (int64_t)m * ldc + n;
+                OT* p = out + (int64_t)m * ldo + n;
                 if (vec && n + E16 <= N) {
                     *(u32x4*)p = *(const u32x4*)q;
                 } else {

@@ -1,6 +1,6 @@
 """Decode-step parity across batch sizes on both sides of the 16-row tile limit of the
 decode projections (at most 16 sequences take one row tile; more take 32- or 64-row
-tiles) and of the fused-kernel limit (above 128 sequences the projections are tiled and
+tiles) and of the fused-kernel limit (above 64 sequences the projections are tiled and
 the conv and state steps run as kernels of their own), several steps in a row, against
 the oracle on the same inputs, and a bad cache slot reported in the status word while the
 other sequences still advance.
@@ -28,7 +28,7 @@ def _gpu():
 STATE_TOL = 2.0 ** -8
 
 
-@pytest.mark.parametrize("batch", [1, 5, 16, 17, 40, 128, 129, 200])
+@pytest.mark.parametrize("batch", [1, 5, 16, 17, 40, 64, 65, 128, 129, 200])
 @pytest.mark.parametrize("init", ["baseline", "stress"])
 def test_decode_batches_across_tile_limit(batch, init):
     from paper_2602_21144_amd import binding as B

@@ -168,9 +168,9 @@ def test_m2_windows_of_several_chunks():
 
 
 # decode batches on each in_proj route: up to 16 sequences on the streamed kernel and up to
-# 128 on the fragment kernel, both with the conv window in the in_proj epilogue; above
-# 128 in_proj, then the conv step as its own kernel
-@pytest.mark.parametrize("Bd", [5, 16, 40, 128, 129])
+# 64 on the fragment kernel, both with the conv window in the in_proj epilogue; above 64
+# in_proj, then the conv step as its own kernel
+@pytest.mark.parametrize("Bd", [5, 16, 40, 64, 65, 129])
 def test_m2_decode_batches(Bd):
     """Decode steps straight from random caches (no prefill) for a batch of sequences in
     scattered slots; outputs, states and the conv history against the oracle each step."""
