@@ -85,6 +85,15 @@ __device__ __forceinline__ float softplus_f(float v) {
 __device__ __forceinline__ int rows_upto(int64_t rem, int cap) { return rem < cap ? (int)rem : cap; }
 __device__ __forceinline__ float silu_f(float v) { return v * fast_rcp(1.0f + fast_exp2(-v * kLog2e)); }
 
+// Workgroups are dispatched round robin over the 8 XCDs (workgroup b on XCD b % 8). This
+// maps b to a logical index so that each XCD gets one contiguous range of logical indices:
+// neighbouring pieces of work that share input rows then share that XCD's L2. A bijection
+// on [0, n) for any n.
+__device__ __forceinline__ int xcd_contiguous(int b, int n) {
+    const int per = n / 8, rem = n % 8, x = b % 8, i = b / 8;
+    return x * per + (x < rem ? x : rem) + i;
+}
+
 // Workspace header: status word at offset 0; regions start 256-byte aligned.
 constexpr size_t kWsHeader = 256;
 __host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }

@@ -60,7 +60,9 @@ __device__ __forceinline__ int seq_of(const int32_t* cu, int nseq, int64_t t) {
 template <typename T, int K>
 __global__ __launch_bounds__(256) void conv_prefill_kernel(ConvArgs a) {
     const int groups = a.E / kCV;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // consecutive token runs on one XCD: the K-1 rows before a run are the end of the
+    // previous run, fetched once into that XCD's L2
+    const int64_t gid = (int64_t)xcd_contiguous((int)blockIdx.x, (int)gridDim.x) * blockDim.x + threadIdx.x;
     const int cg = (int)(gid % groups);
     const int64_t t0 = (gid / groups) * kTT;
     if (t0 >= a.T) return;
