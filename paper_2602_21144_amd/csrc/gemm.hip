@@ -538,7 +538,10 @@ hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t 
         const int sp = fit_slices(splitk_slices(((M + 127) / 128) * ((N + 127) / 128), K), M, N, scratch_bytes);
         return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
     }
-    return run_dma<ROLE, 128, 128, 32, 4, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    // K a multiple of 32 only (dt_proj: K = dt_rank): a 3-slot ring (48 KB) lets three
+    // workgroups share a CU, which shortens the many short-lived tiles' latency rounds
+    // (dt_proj of 16384 tokens, K = 160: 35 -> 30 us against a 4-slot ring)
+    return run_dma<ROLE, 128, 128, 32, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
 // fp32 weights and at most 8 activation rows (a decode step of the fp32 configuration),
