@@ -405,11 +405,16 @@ def mamba2_figures(B, torch, steps, warmup):
 def decode_heavy_figures(B, torch, steps=64):
     """Decode-heavy serving step on the Mamba-2.8B quarter shard (1280 of 5120 channels,
     d_model 2560): 256 sequences holding cached states, one single-token step each. Above
-    128 sequences the step runs tiled projections, the conv-step kernel and the state-step
+    64 sequences the step runs tiled projections, the conv-step kernel and the state-step
     kernel, whose traffic is the state cache (read and written once: 2 B E N 4 bytes).
     Weights are drawn on the GPU with the one-layer recipe; the cache pools hold seeded
     random values (the timing does not depend on them); the other shards' x_proj partial
-    (their GPUs' work) is precomputed, as in the headline step."""
+    (their GPUs' work) is precomputed, as in the headline step.
+
+    The 256 sequences' states (21 MB) stay in the 256 MB MALL from step to step, so the
+    state kernel's rate is also measured with 16 groups of 256 sequences in a 4112-slot
+    pool (337 MB of states), each step serving the next group: every step's states then
+    come from HBM ("state_beyond_mall")."""
     import math
     import numpy as np
     from paper_2602_21144_amd import synth
@@ -463,11 +468,44 @@ def decode_heavy_figures(B, torch, steps=64):
     torch.cuda.synchronize()
     assert B.take_status(wsd) == 0
     step_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
+
+    # the same steps over 16 groups of sequences whose states together exceed the MALL
+    groups = 16
+    S2 = groups * Bd + 16
+    perm = torch.from_numpy(np.random.default_rng(cfg["seed"] + 1).permutation(Bd).astype(np.int32)).to(dev)
+    gslots = [perm + gi * Bd for gi in range(groups)]
+    conv2 = nrm(S2, E, K - 1, std=1.0)
+    ssm2 = torch.randn(S2, E, N, generator=g, device=dev) * 0.5
+    calls2 = [(B.bind("ssm_shard_decode_stage1", d, ws_, xs[k], gslots[k % groups], conv2, q0, wsd),
+               B.bind("ssm_reduce_add_f32", q0, other),
+               B.bind("ssm_shard_decode_stage2", d, ws_, q0, gslots[k % groups], ssm2, y, wsd)) for k in range(steps)]
+
+    def run2():
+        for cs in calls2:
+            for c in cs:
+                c()
+    run2()
+    torch.cuda.synchronize()
+    ev[0].record()
+    run2()
+    ev[1].record()
+    torch.cuda.synchronize()
+    step2_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True, "decode.state_update")
+    run2()
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    bd2 = B.ssm_timing_collect()
+    assert B.take_status(wsd) == 0
+    del conv2, ssm2
     state_bytes = 2 * Bd * E * N * 4 + 4 * Bd * E * 2 + Bd * 2 * N * 4 + E * (N + 2) * 4
     weight_bytes = (2 * E * dm + W * E + E * R + dm * E) * 2
     step_bytes = weight_bytes + state_bytes + 2 * Bd * E * (K - 1) * 2 + Bd * (dm + 2 * E + W * 4 + dm) * 2
     st = bd.get("decode.state_update", (1, float("nan")))
     st_us = 1e3 * st[1] / st[0]
+    st2 = bd2.get("decode.state_update", (1, float("nan")))
+    st2_us = 1e3 * st2[1] / st2[0]
     return {"workload": "Mamba-2.8B-shaped layer, shard 0 of a 4-way channel split (d_model 2560, 1280 of 5120 "
                         "channels, d_state 16, dt_rank 160, d_conv 4): 256 sequences with cached states, one "
                         "single-token decode step each; bf16, fp32 state; seed 3",
@@ -477,6 +515,10 @@ def decode_heavy_figures(B, torch, steps=64):
             "state_kernel": {"avg_us": round(st_us, 3), "bytes": state_bytes,
                              "GBps": round(state_bytes / (st_us * 1e-6) / 1e9, 1),
                              "frac_hbm": round(state_bytes / (st_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
+            "state_beyond_mall": {"pool_slots": S2, "state_pool_bytes": S2 * E * N * 4,
+                                  "decode_us_per_step": round(step2_us, 3), "state_kernel_avg_us": round(st2_us, 3),
+                                  "GBps": round(state_bytes / (st2_us * 1e-6) / 1e9, 1),
+                                  "frac_hbm": round(state_bytes / (st2_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
             "kernels": {k: {"launches": n, "avg_us": round(1e3 * ms / n, 3)}
                         for k, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][1])}}
 
