@@ -353,16 +353,20 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
     const int64_t itc = live ? item : 0;
     const int b = (int)(itc / a.E), c = (int)(itc % a.E);
     const int slot = a.slot[b];
-    const bool slot_ok = slot >= 0 && slot < a.S;
-    float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
-    const float4 h = *hp;
+    // everything that does not depend on the slot goes out with the slot index, before the
+    // slot-addressed state
     const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
     const float* xb = a.xdbl + (int64_t)b * a.ld_xdbl + a.R;  // B at 0, C at kN (16-byte aligned)
     const float4 Bq = ((const float4*)xb)[q], Cq = ((const float4*)(xb + kN))[q];
     const float u = to_f32(((const T*)a.u)[(int64_t)b * a.E + c]);
     const float dt = to_f32(((const T*)a.dt)[(int64_t)b * a.E + c]);
     const float z = to_f32(((const T*)a.z)[(int64_t)b * a.ld_z + c]);
-    const float delta = softplus_f(dt + a.b_dt[c]);
+    const float bdt = a.b_dt[c], Dc = a.D[c];
+    __builtin_amdgcn_sched_barrier(0);
+    const bool slot_ok = slot >= 0 && slot < a.S;
+    float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
+    const float4 h = *hp;
+    const float delta = softplus_f(dt + bdt);
     const float du = delta * u;
     const float hv[4] = {h.x, h.y, h.z, h.w}, av[4] = {al.x, al.y, al.z, al.w};
     const float bv[4] = {Bq.x, Bq.y, Bq.z, Bq.w}, cv[4] = {Cq.x, Cq.y, Cq.z, Cq.w};
@@ -374,6 +378,9 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
     }
     y += __shfl_xor(y, 1);
     y += __shfl_xor(y, 2);
+    // z and D are used only past the exits below; keeping them live here stops the compiler
+    // from sinking their loads behind the exits (a second memory round trip per wave)
+    asm volatile("" ::"v"(z), "v"(Dc));
     if (!live) return;
     if (!slot_ok) {
         if (q == 0) {
@@ -383,7 +390,7 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
         return;
     }
     *hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
-    if (q == 0) ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>((y + a.D[c] * u) * silu_f(z));
+    if (q == 0) ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>((y + Dc * u) * silu_f(z));
 }
 
 }  // namespace
