@@ -1,6 +1,8 @@
 """End-to-end parity of the C ABI (prefill stages, exchange, decode) against the oracle at
 sizes the oracle finishes in seconds: several GEMM tiles, ragged tails, packed sequences
-of mixed lengths with continuing and fresh states, all shards of a channel split.
+of mixed lengths with continuing and fresh states, all shards of a channel split; and the
+state-cache invariants on the GPU (prefill then decode equals a longer prefill; caches
+copied through the host continue bit-identically).
 """
 import numpy as np
 import pytest
@@ -183,3 +185,83 @@ def test_empty_batch_and_empty_sequences():
     assert torch.count_nonzero(s[0][2]) == 0 and torch.count_nonzero(c[0][2].float()) == 0
     assert torch.equal(c[0][3].view(torch.int16), before3[0].view(torch.int16))
     assert torch.equal(s[0][3].view(torch.int32), before3[1].view(torch.int32))
+
+
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_prefill_then_decode_equals_longer_prefill(act):
+    """Section IV-A: prefill of L tokens followed by k decode steps fed the next k prompt
+    rows gives the last k outputs, and the caches, of a prefill of L + k tokens (two
+    sequences, one of them continuing a cached state; on the GPU within tolerance, since
+    different kernels add in different orders)."""
+    from paper_2602_21144_amd import binding as B
+    shape, full = _case(act, 2, "stress", seed=21, E_tot=256)
+    rng = np.random.default_rng(21)
+    L, k = [150, 67], 5
+    x = [synth.make_tokens(rng, L[i] + k, shape.d_model, act) for i in range(2)]
+    S, slots, hi = 4, np.array([3, 1], np.int32), np.array([0, 1], np.int32)
+    E = shape.d_shard
+    cp0, sp0 = _pools_host(rng, shape, S, act)
+    g = GpuLayer(shape, full)
+
+    def fresh():
+        conv, ssm = g.new_pools(S)
+        for r in range(shape.shard_count):
+            conv[r].copy_(g.to_dev(_slice(cp0, r, E)))
+            ssm[r].copy_(torch.from_numpy(np.ascontiguousarray(_slice(sp0, r, E))).cuda())
+        return conv, ssm
+
+    # whole: prefill of L + k tokens
+    cw, sw = fresh()
+    xl = np.concatenate(x)
+    cu = np.array([0, L[0] + k, L[0] + L[1] + 2 * k], np.int32)
+    yw = g.prefill(xl, B.SeqMeta(cu, slots, hi, S), cw, sw)
+    # split: prefill of L tokens, then k decode steps
+    cs, ss = fresh()
+    xp = np.concatenate([x[0][:L[0]], x[1][:L[1]]])
+    g.prefill(xp, B.SeqMeta([0, L[0], L[0] + L[1]], slots, hi, S), cs, ss)
+    sl = torch.from_numpy(slots).cuda()
+    tol = TOL[act]
+    for j in range(k):
+        xt = np.stack([x[0][L[0] + j], x[1][L[1] + j]])
+        yd = g.decode(xt, sl, cs, ss)
+        for r in range(shape.shard_count):
+            want = np.stack([host(yw[r][L[0] + j]), host(yw[r][L[0] + k + L[1] + j])])
+            assert_close(host(yd[r]), want, tol, f"decode step {j} vs whole prefill, shard {r}")
+    for r in range(shape.shard_count):
+        assert_close(host(ss[r]), host(sw[r]), 1e-4 if act == "bf16" else 2e-5, f"states, shard {r}")
+        assert_close(host(cs[r]), host(cw[r]), tol, f"conv history, shard {r}")
+
+
+def test_cache_round_trip_through_host_is_exact():
+    """The caches are plain arrays: copied to the host, restored into fresh pools (other
+    slots) and continued, they give bit-identical outputs to continuing in place."""
+    from paper_2602_21144_amd import binding as B
+    shape, full = _case("bf16", 1, "stress", seed=23, E_tot=192)
+    rng = np.random.default_rng(23)
+    lens = [90, 33, 7]
+    S = 8
+    slots = np.array([5, 0, 2], np.int32)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    x = synth.make_tokens(rng, int(cu[-1]), shape.d_model, "bf16")
+    xdec = [synth.make_tokens(rng, 3, shape.d_model, "bf16") for _ in range(4)]
+    g = GpuLayer(shape, full)
+    conv, ssm = g.new_pools(S)
+    g.prefill(x, B.SeqMeta(cu, slots, np.zeros(3, np.int32), S), conv, ssm)
+    torch.cuda.synchronize()
+    conv_h, ssm_h = conv[0].cpu().clone(), ssm[0].cpu().clone()
+    # in place
+    sl = torch.from_numpy(slots).cuda()
+    y_in = [g.decode(xt, sl, conv, ssm)[0].clone() for xt in xdec]
+    # restored from the host into other slots of a fresh pool
+    slots2 = np.array([1, 7, 4], np.int32)
+    conv2, ssm2 = g.new_pools(S)
+    for a, b in zip(slots, slots2):
+        conv2[0][int(b)].copy_(conv_h[int(a)].cuda())
+        ssm2[0][int(b)].copy_(ssm_h[int(a)].cuda())
+    sl2 = torch.from_numpy(slots2).cuda()
+    y_re = [g.decode(xt, sl2, conv2, ssm2)[0].clone() for xt in xdec]
+    for j, (p, q) in enumerate(zip(y_in, y_re)):
+        assert torch.equal(p.view(torch.int16), q.view(torch.int16)), f"decode step {j}"
+    for a, b in zip(slots, slots2):
+        assert torch.equal(ssm[0][int(a)].view(torch.int32), ssm2[0][int(b)].view(torch.int32))
+        assert torch.equal(conv[0][int(a)].view(torch.int16), conv2[0][int(b)].view(torch.int16))
