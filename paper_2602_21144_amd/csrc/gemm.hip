@@ -221,8 +221,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     // one LDS block: the operand ring, reused after the k loop to stage the output tile
     constexpr int RING = NS * (BM + BN) * BK * 2;
     using OT = typename std::conditional<C_F32 || SPLIT, float, bf16>::type;
-    // stage the output through LDS (in one or two passes of whole wave rows): whole-line
-    // stores instead of the MFMA layout's 16-byte pieces spread over 32 rows
+    // stage the output tile (or a K-slice's fp32 partial tile) through LDS, in one or two
+    // passes of whole wave rows: whole-line stores instead of the MFMA layout's 16-byte
+    // pieces spread over 32 rows
     constexpr int PASSES = (BM * BN * (int)sizeof(OT) + RING - 1) / RING;
     constexpr int RB = BM / PASSES;  // tile rows per pass
     constexpr bool STAGE = (BN * (int)sizeof(OT)) % 128 == 0 && PASSES <= 2 && BM % PASSES == 0 &&
