@@ -21,12 +21,14 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >>
 
 // Map the linear workgroup id to an output tile. Workgroups are dispatched round robin
 // over the 8 XCDs; regroup so each XCD gets a contiguous run of tiles, and order the
-// tiles in groups of 8 tile-rows so that a run shares A panels and B panels in its L2.
+// tiles in groups of 4 tile-rows so that a run shares A panels and B panels in its L2
+// (groups of 4 took dt_proj's 2560 short tiles from 31 to 28 us; 8 and 16 measured the
+// same or slower on every projection).
 __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
     int nwg = gridDim.x;
     int bid = blockIdx.x;
     if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
-    constexpr int G = 8;
+    constexpr int G = 4;
     int per_group = G * tiles_n;
     int grp = bid / per_group;
     int first = grp * G;
