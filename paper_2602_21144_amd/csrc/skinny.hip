@@ -241,6 +241,105 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(SkinnyArgs p) {
     else ein.apply(p, em, en, v);
 }
 
+// 17 to 64 rows: the fragment kernel with 32 output columns per workgroup. Every
+// workgroup reads all MB activation rows, so halving the number of column tiles halves
+// those re-reads (the 3584-wide in_proj of 64 sequences read ~205 MB of activations from
+// L2 on 16-column tiles). NW waves split K; each k-step loads two weight fragments (rows
+// n0 + 16 j) and the MT activation fragments and issues 2 MT MFMAs. The waves' partial
+// tiles meet in LDS; each thread then finishes EPT output elements. Plain stores and the
+// conv epilogue only (the state epilogue holds a whole state row per element).
+template <int MB, int NW, int KU, int EPI>
+__global__ __launch_bounds__(NW * 64) void gemm_skinny32_kernel(SkinnyArgs p) {
+    constexpr int MT = MB / 16, NB = 32;
+    constexpr int EPT = MB * NB / (NW * 64);
+    static_assert(EPT * NW * 64 == MB * NB, "whole elements per thread");
+    __shared__ float red[NW][MB * NB];
+    const int n0 = blockIdx.x * NB, m0 = blockIdx.y * MB;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+    // epilogue elements of this thread: e = tid + t NW 64, row e / 32, column e % 32
+    EpiIn<EPI> ein[EPT];
+    int em[EPT], en[EPT];
+#pragma unroll
+    for (int t = 0; t < EPT; ++t) {
+        const int e = threadIdx.x + t * NW * 64;
+        em[t] = m0 + e / NB;
+        en[t] = n0 + e % NB;
+        ein[t].load_slot(p, em[t] < p.M ? em[t] : p.M - 1);
+    }
+
+    const int ksteps = (p.K + 31) / 32;
+    const int per = (ksteps + NW - 1) / NW;
+    const int s0 = wave * per, s1 = min(ksteps, s0 + per);
+    const int kl = (lane >> 4) * 8;
+    // weight rows past N and activation rows past M lie outside the resources: zeros
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(min(NB, p.N - n0) * p.ldb * 2));
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc((const bf16*)p.A + (int64_t)m0 * p.lda,
+                                                  (uint32_t)(min(MB, p.M - m0) * p.lda * 2));
+    f32x4 acc[2][MT];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[j][i] = f32x4{};
+    u32x4 bf[KU][2], af[KU][MT];
+    auto load_batch = [&](int s) {
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int k = (s + u) * 32 + kl;
+            const bool kok = (s + u < s1) && k < p.K;
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                bf[u][j] = buffer_load16(rb, kok ? (uint32_t)(((16 * j + (lane & 15)) * p.ldb + k) * 2) : kOffOutOfRange);
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                af[u][i] = buffer_load16(ra, kok ? (uint32_t)(((i * 16 + (lane & 15)) * p.lda + k) * 2) : kOffOutOfRange);
+        }
+    };
+    auto mma_batch = [&]() {
+#pragma unroll
+        for (int u = 0; u < KU; ++u)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[u][i]),
+                                                                        __builtin_bit_cast(bf16x8, bf[u][j]), acc[j][i],
+                                                                        0, 0, 0);
+    };
+    load_batch(s0);
+    // the slot-addressed epilogue operands go out behind the first batch of weights
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < EPT; ++t)
+        ein[t].load(p, em[t] < p.M ? em[t] : p.M - 1, en[t] < p.N ? en[t] : p.N - 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_batch();
+    for (int s = s0 + KU; s < s1; s += KU) {
+        load_batch(s);
+        mma_batch();
+    }
+    // lane l holds column l % 16 of block j and rows 4 (l / 16) + r of each 16-row tile
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                red[wave][(i * 16 + 4 * (lane >> 4) + r) * NB + 16 * j + (lane & 15)] = acc[j][i][r];
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < EPT; ++t) {
+        if (em[t] >= p.M || en[t] >= p.N) continue;
+        const int e = threadIdx.x + t * NW * 64;
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += red[w][e];
+        if constexpr (EPI == kEpiStoreBf16) ((bf16*)p.C)[(int64_t)em[t] * p.ldc + en[t]] = (bf16)v;
+        else if constexpr (EPI == kEpiStoreF32) ((float*)p.C)[(int64_t)em[t] * p.ldc + en[t]] = v;
+        else ein[t].apply(p, em[t], en[t], v);
+    }
+}
+
 // Streamed-weight variant for at most 16 rows, bf16 activations and K a multiple of 64
 // (in_proj, x_proj and out_proj of a decode step). Loading MFMA fragments straight from
 // global memory makes every load instruction touch 16 weight rows x 64 bytes (half cache
@@ -407,10 +506,41 @@ hipError_t launch_epi(const SkinnyArgs& p, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// 32-column tiles for 17..64 bf16 rows when they still give at least 192 workgroups.
+// Measured at 64 rows: the 7168-wide in_proj (224 workgroups) 36.6 -> 24.3 us; with 80 or
+// 112 workgroups (2560 or 3584 columns) the 16-column tiles were faster.
+bool use_skinny32(const SkinnyArgs& p) {
+    return !p.a_f32 && p.M > 16 && p.M <= 64 && (p.N + 31) / 32 >= 192 && p.K % 8 == 0 && p.lda % 8 == 0 &&
+           p.ldb % 8 == 0;
+}
+
+template <int EPI>
+hipError_t launch_skinny32(const SkinnyArgs& p, hipStream_t s) {
+    const int ksteps = (p.K + 31) / 32;
+    if (p.M <= 32) {
+        const dim3 grid((unsigned)((p.N + 31) / 32), 1);
+        if ((ksteps + 15) / 16 <= 2) SSM_LAUNCH((gemm_skinny32_kernel<32, 16, 2, EPI>), grid, dim3(1024), 0, s, p);
+        else SSM_LAUNCH((gemm_skinny32_kernel<32, 16, 4, EPI>), grid, dim3(1024), 0, s, p);
+    } else {
+        const dim3 grid((unsigned)((p.N + 31) / 32), 1);
+        if ((ksteps + 7) / 8 <= 2) SSM_LAUNCH((gemm_skinny32_kernel<64, 8, 2, EPI>), grid, dim3(512), 0, s, p);
+        else SSM_LAUNCH((gemm_skinny32_kernel<64, 8, 4, EPI>), grid, dim3(512), 0, s, p);
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    if (use_skinny32(p)) {
+        switch (epi) {
+            case kSkinnyStoreBf16: return launch_skinny32<kEpiStoreBf16>(p, s);
+            case kSkinnyStoreF32: return launch_skinny32<kEpiStoreF32>(p, s);
+            case kSkinnyConv: return launch_skinny32<kEpiConv>(p, s);
+            default: break;
+        }
+    }
     if (const int nw = gemv_waves(p)) {
         switch (epi) {
             case kSkinnyStoreBf16: return launch_gemv<kEpiStoreBf16>(p, nw, s);
