@@ -820,7 +820,21 @@ ConvArgs m2_conv(const M2& m, const ssm2_shard_weights_t* w, const M2Ws& L, int6
 }
 
 int m2_stage2(const M2& m, const ssm2_shard_weights_t* w, const float* sumsq, int64_t T, void* y, const M2Ws& L,
-              hipStream_t s, const char* norm_name, const char* out_name) {
+              hipStream_t s, const char* norm_name, const char* out_name, const char* fused_name = nullptr) {
+    if (fused_name && T <= 16) {
+        // a few rows (a decode step): the gated norm as the streamed out_proj's operand
+        // transform, one launch instead of two
+        SkinnyArgs p = skinny(L.g, m.E, false, w->out_proj_w, m.E, y, m.dm, T, m.dm, m.E);
+        p.nrm_sumsq = sumsq; p.nrm_w = w->norm_w; p.nrm_G = (int)m.G; p.nrm_gsize = m.gsize;
+        p.nrm_c0 = (int)(m.r * m.E); p.nrm_eps = 1e-5f;
+        hipError_t e;
+        {
+            KernelTimer kt(fused_name, s);
+            e = launch_gemv_norm(p, s);
+        }
+        if (e == hipSuccess) return SSM_OK;
+        if (e != hipErrorNotSupported) return fail(SSM_E_HIP, "%s: %s", fused_name, hipGetErrorString(e));
+    }
     SSM_TIMED(norm_name, s, launch_ssd_norm(L.g, sumsq, w->norm_w, L.gn, T, (int)m.E, (int)m.G, m.gsize,
                                             (int)(m.r * m.E), 1e-5f, s));
     return gemm(T, m.dm, m.E, L.gn, m.E, SSM_BF16, w->out_proj_w, m.E, SSM_BF16, y, m.dm, SSM_BF16, s, out_name,
@@ -1004,7 +1018,7 @@ int ssm2_shard_decode_stage2(const ssm2_shard_desc_t* d, const ssm2_shard_weight
     if (B == 0) return SSM_OK;
     SSM_TRY(check_ptr(sumsq, "sumsq"));
     SSM_TRY(check_ptr(y, "y_partial"));
-    return m2_stage2(m, w, sumsq, B, y, L, s, "m2.decode.norm", "m2.decode.out_proj");
+    return m2_stage2(m, w, sumsq, B, y, L, s, "m2.decode.norm", "m2.decode.out_proj", "m2.decode.norm_out_proj");
 }
 
 }  // extern "C"

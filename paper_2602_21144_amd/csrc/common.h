@@ -129,8 +129,14 @@ struct SkinnyArgs {
     void* z; int64_t ld_z;
     const float* xdbl; int64_t ld_xdbl; int R; const float* b_dt; const float* A_log; const float* D;
     float* pool; void* g;
+    // gated RMSNorm applied to A as it is loaded (Mamba-2 out_proj): column c of row m is
+    // multiplied by 1 / sqrt(sumsq[m][k] / gsize + eps) and norm_w[c], k = (c0 + c) / gsize
+    const float* nrm_sumsq; const float* nrm_w; int nrm_G, nrm_gsize, nrm_c0; float nrm_eps;
 };
 hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s);
+// the streamed kernel with the norm prologue above (plain bf16 stores); hipErrorNotSupported
+// when the shape does not suit it (the caller then runs the norm and the product apart)
+hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s);
 
 struct ConvArgs {
     const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1

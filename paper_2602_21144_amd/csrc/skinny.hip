@@ -355,12 +355,17 @@ constexpr int kGemvBK = 64;
 
 __device__ __forceinline__ int gemv_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int NW, int NST, int XB, int EPI>
+constexpr int kNormMaxK = 8192, kNormMaxMG = 256;  // norm prologue: K columns, rows x groups
+
+template <int NW, int NST, int XB, int EPI, bool NORM = false>
 __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
     static_assert(NW >= 4, "one epilogue element per thread of the first 256");
     constexpr int SLOT = (2 + XB) * 1024;  // one stage: 16 weight rows, then 8 * XB activation rows, 128 B each
     __shared__ __attribute__((aligned(16))) char tr[NW][2][SLOT];
     __shared__ float red[NW][256];
+    // norm prologue: norm_w over K and the per-(row, group) inverse RMS, staged once
+    __shared__ __attribute__((aligned(16))) float nrm_w[NORM ? kNormMaxK : 4];
+    __shared__ float nrm_inv[NORM ? kNormMaxMG : 1];
     const int n0 = blockIdx.x * 16;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
@@ -381,6 +386,19 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
     const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(p.A, (uint32_t)(p.M * p.lda * 2));
     const uint32_t k0b = (uint32_t)(sb * kGemvBK + lp * 8) * 2;
     const uint32_t wo0 = (uint32_t)(lr * p.ldb) * 2 + k0b, wo1 = (uint32_t)((8 + lr) * p.ldb) * 2 + k0b;
+    // norm prologue operands go out first, so that waiting for them waits for nothing else
+    constexpr int NSTG = NORM ? kNormMaxK / 4 / (NW * 64) : 1;
+    float4 nwr[NSTG];
+    float ssq = 0.0f;
+    if constexpr (NORM) {
+#pragma unroll
+        for (int j = 0; j < NSTG; ++j) {
+            const int i = threadIdx.x + j * NW * 64;
+            nwr[j] = i < p.K / 4 ? ((const float4*)p.nrm_w)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (threadIdx.x < p.M * p.nrm_G) ssq = p.nrm_sumsq[threadIdx.x];
+        __builtin_amdgcn_sched_barrier(0);
+    }
     u32x4 w0[NST], w1[NST], xv[NST][XB];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
@@ -395,6 +413,22 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     ein.load(p, emc, enc);
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NORM) {
+        // the same arithmetic as the separate norm kernel: 1 / sqrt(sumsq / gsize + eps),
+        // then (g * inv) * norm_w rounded to bf16
+#pragma unroll
+        for (int j = 0; j < NSTG; ++j) {
+            const int i = threadIdx.x + j * NW * 64;
+            if (i < p.K / 4) *(float4*)&nrm_w[4 * i] = nwr[j];
+        }
+        if (threadIdx.x < p.M * p.nrm_G) nrm_inv[threadIdx.x] = 1.0f / sqrtf(ssq / (float)p.nrm_gsize + p.nrm_eps);
+        __syncthreads();
+    }
+    // the inverse RMS of this lane's activation rows (rows past M: 0) for one group per row
+    auto inv_at = [&](int row, int k) { return row < p.M ? nrm_inv[row * p.nrm_G + (p.nrm_c0 + k) / p.nrm_gsize] : 0.0f; };
+    float inv1[XB];
+#pragma unroll
+    for (int q = 0; q < XB; ++q) inv1[q] = NORM && 8 * q + lr < p.M ? nrm_inv[NORM ? (8 * q + lr) * p.nrm_G : 0] : 0.0f;
 
     // fragment rows: weights l % 16, activations l % (8 XB); chunk 4 j + l / 16 of substep j
     const int wr = lane & 15, xr = XB == 2 ? (lane & 15) : (lane & 7), cg = lane >> 4;
@@ -406,8 +440,22 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
             *(u32x4*)(t + lr * 128 + gemv_swz(lr, lp) * 16) = w0[st];
             *(u32x4*)(t + (8 + lr) * 128 + gemv_swz(8 + lr, lp) * 16) = w1[st];
 #pragma unroll
-            for (int q = 0; q < XB; ++q)
-                *(u32x4*)(t + 2048 + (8 * q + lr) * 128 + gemv_swz(8 * q + lr, lp) * 16) = xv[st][q];
+            for (int q = 0; q < XB; ++q) {
+                u32x4 xq = xv[st][q];
+                if constexpr (NORM) {
+                    const int k = (sb + st) * kGemvBK + lp * 8;
+                    // one group per row (the usual case) needs no group index
+                    const float inv = p.nrm_G == 1 ? inv1[q] : inv_at(8 * q + lr, k);
+                    const float4 w0 = *(const float4*)&nrm_w[k], w1 = *(const float4*)&nrm_w[k + 4];
+                    const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+                    const bf16x8 x8 = __builtin_bit_cast(bf16x8, xq);
+                    bf16x8 o;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[e] = (bf16)((float)x8[e] * inv * wv[e]);
+                    xq = __builtin_bit_cast(u32x4, o);
+                }
+                *(u32x4*)(t + 2048 + (8 * q + lr) * 128 + gemv_swz(8 * q + lr, lp) * 16) = xq;
+            }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int c = 4 * j + cg;
@@ -530,6 +578,24 @@ hipError_t launch_skinny32(const SkinnyArgs& p, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s) {
+    if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    const int nw = gemv_waves(p);
+    // grids that fill the CUs only (4 or 8 waves): the 16-wave small-grid variant has no LDS
+    // left for the staged norm weights
+    if ((nw != 4 && nw != 8) || p.K > kNormMaxK || p.M * p.nrm_G > kNormMaxMG || p.nrm_gsize <= 0 ||
+        p.nrm_gsize % 8 != 0 || ((uintptr_t)p.nrm_w & 15) != 0)
+        return hipErrorNotSupported;
+    const dim3 grid((unsigned)((p.N + 15) / 16)), block(nw * 64);
+#define SSM_GEMV_N(NW, NST)                                                                              \
+    if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, kEpiStoreBf16, true>), grid, block, 0, s, p);   \
+    else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, kEpiStoreBf16, true>), grid, block, 0, s, p);
+    if (nw == 4) { SSM_GEMV_N(4, 10) }
+    else { SSM_GEMV_N(8, 10) }
+#undef SSM_GEMV_N
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
