@@ -32,8 +32,9 @@
  *     workspace status word (SSM_STATUS_*), read with ssm_shard_take_status().
  *     ssm_shard_check_meta_host() validates host copies completely (including
  *     duplicate slots, which the kernels cannot detect; duplicates in one call race).
- *   - Cache layout: conv_pool [num_slots][E][K-1] act dtype, oldest input first;
- *     ssm_pool [num_slots][E][N] float32. Slots not named in a call stay bit-identical.
+ *   - Cache layout: conv_pool [num_slots][E][K-1] act dtype, oldest input first (empty,
+ *     and the pointer may be null, when K = 1); ssm_pool [num_slots][E][N] float32.
+ *     Slots not named in a call stay bit-identical.
  */
 #ifndef SSM_SHARD_H
 #define SSM_SHARD_H

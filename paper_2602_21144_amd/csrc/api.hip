@@ -418,7 +418,7 @@ int ssm_shard_prefill_stage1(const ssm_shard_desc_t* d, const ssm_shard_weights_
                              size_t ws_bytes, hipStream_t s) {
     PrefillWs L;
     SSM_TRY(prefill_checks(d, w, T, m, S, ws, ws_bytes, &L));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     if (T > 0) {
         SSM_TRY(check_ptr(x, "x"));
         SSM_TRY(check_ptr(xdbl, "x_dbl_partial"));
@@ -444,7 +444,7 @@ int ssm_shard_prefill(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, c
                       size_t ws_bytes, hipStream_t s) {
     PrefillWs L;
     SSM_TRY(prefill_checks(d, w, T, m, S, ws, ws_bytes, &L));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
     if (T > 0) {
         SSM_TRY(check_ptr(x, "x"));
@@ -459,7 +459,7 @@ int ssm_shard_decode_stage1(const ssm_shard_desc_t* d, const ssm_shard_weights_t
                             hipStream_t s) {
     DecodeWs L;
     SSM_TRY(decode_checks(d, w, B, slot, S, ws, ws_bytes, &L));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     if (B > 0) {
         SSM_TRY(check_ptr(x, "x_t"));
         SSM_TRY(check_ptr(xdbl, "x_dbl_partial"));
@@ -485,7 +485,7 @@ int ssm_shard_decode_step(const ssm_shard_desc_t* d, const ssm_shard_weights_t* 
                           size_t ws_bytes, hipStream_t s) {
     DecodeWs L;
     SSM_TRY(decode_checks(d, w, B, slot, S, ws, ws_bytes, &L));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
     if (B > 0) {
         SSM_TRY(check_ptr(x, "x_t"));
@@ -637,7 +637,7 @@ int ssm_conv1d_silu(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, con
     SSM_TRY(common_checks(d, w, T, S));
     SSM_TRY(check_meta(m, T));
     SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     if (T > 0) {
         SSM_TRY(check_ptr(xz, "xz"));
         SSM_TRY(check_ptr(u, "u"));
@@ -675,7 +675,7 @@ int ssm_decode_conv(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, con
                     hipStream_t s) {
     SSM_TRY(common_checks(d, w, B, S));
     SSM_TRY(check_ws(ws, ws_bytes, kWsHeader));
-    SSM_TRY(check_ptr(conv_pool, "conv_pool"));
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
     if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
     if (B > 0) {
         if (!slot) return fail(SSM_E_INVAL, "cache_slot is null");
@@ -1161,7 +1161,7 @@ int ssm_stack_prefill(const ssm_stack_desc_t* sd, const ssm_shard_weights_t* lay
     SSM_TRY(check_ws(ws, ws_bytes, B.total));
     if (!conv_pools || !ssm_pools) return fail(SSM_E_INVAL, "pool arrays are null");
     for (int l = 0; l < sd->n_layers; ++l) {
-        SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
+        if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
         SSM_TRY(check_ptr(ssm_pools[l], "ssm_pools[l]"));
     }
     if (T > 0) {
@@ -1198,7 +1198,7 @@ int ssm_stack_decode_step(const ssm_stack_desc_t* sd, const ssm_shard_weights_t*
     SSM_TRY(check_ws(ws, ws_bytes, B.total));
     if (!conv_pools || !ssm_pools) return fail(SSM_E_INVAL, "pool arrays are null");
     for (int l = 0; l < sd->n_layers; ++l) {
-        SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
+        if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pools[l], "conv_pools[l]"));
         SSM_TRY(check_ptr(ssm_pools[l], "ssm_pools[l]"));
     }
     if (Bsz == 0) return SSM_OK;

@@ -265,3 +265,55 @@ def test_cache_round_trip_through_host_is_exact():
     for a, b in zip(slots, slots2):
         assert torch.equal(ssm[0][int(a)].view(torch.int32), ssm2[0][int(b)].view(torch.int32))
         assert torch.equal(conv[0][int(a)].view(torch.int16), conv2[0][int(b)].view(torch.int16))
+
+
+@pytest.mark.parametrize("K", [1, 2, 3])
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_conv_widths_prefill_then_decode(K, act):
+    """Convolution widths below 4, down to 1 (no history: the conv is a per-channel scale
+    plus bias and the conv cache is empty): packed prefill with continuing and fresh
+    sequences, then decode steps, against the oracle."""
+    from paper_2602_21144_amd import binding as B
+    shape = synth.LayerShape(64, 256, 16, 16, K, 2, act)
+    full = synth.make_layer(shape, 40 + K, stress=True)
+    E = shape.d_shard
+    rng = np.random.default_rng(40 + K)
+    lens = [33, 1, 70, 2]
+    S = 6
+    nseq = len(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    slots = np.array([4, 0, 2, 5], np.int32)
+    hi = np.array([1, 0, 1, 0], np.int32)
+    x = synth.make_tokens(rng, int(cu[-1]), shape.d_model, act)
+    cp0, sp0 = _pools_host(rng, shape, S, act)
+    g = GpuLayer(shape, full)
+    conv, ssm = g.new_pools(S)
+    for r in range(shape.shard_count):
+        if K > 1:
+            conv[r].copy_(g.to_dev(_slice(cp0, r, E)))
+        ssm[r].copy_(torch.from_numpy(np.ascontiguousarray(_slice(sp0, r, E))).cuda())
+    ys = g.prefill(x, B.SeqMeta(cu, slots, hi, S), conv, ssm)
+    for r in range(shape.shard_count):
+        assert B.take_status(g.last_ws[r]) == 0
+    w64 = f64(full)
+    shards = [om.shard_weights(w64, r, 2) for r in range(2)]
+    cps = [_slice(cp0, r, E).astype(np.float64) for r in range(2)]
+    sps = [_slice(sp0, r, E).astype(np.float64) for r in range(2)]
+    s1, s2, _ = om.tp_prefill(shards, x.astype(np.float64), cu, slots, hi, cps, sps, act)
+    tol = TOL[act]
+    for r in range(2):
+        assert_close(host(ys[r]), s2[r]["y"], tol, f"prefill y shard {r}")
+        assert_close(host(ssm[r]), s2[r]["ssm_pool"], 1e-4 if act == "bf16" else 2e-5, f"states shard {r}")
+        if K > 1:
+            assert_close(host(conv[r]), s1[r]["conv_pool"], tol, f"conv history shard {r}")
+    sl = torch.from_numpy(slots).cuda()
+    cps = [s["conv_pool"] for s in s1]
+    sps = [s["ssm_pool"] for s in s2]
+    for step in range(2):
+        xt = synth.make_tokens(rng, nseq, shape.d_model, act)
+        yd = g.decode(xt, sl, conv, ssm)
+        d1, d2, _ = om.tp_decode_step(shards, xt.astype(np.float64), slots, cps, sps, act)
+        cps = [d["conv_pool"] for d in d1]
+        sps = [d["ssm_pool"] for d in d2]
+        for r in range(2):
+            assert_close(host(yd[r]), d2[r]["y"], tol, f"decode step {step} shard {r}")
