@@ -45,14 +45,24 @@ def test_decode_wide_shard_batches(batch):
     _decode_batch_case(synth.LayerShape(256, 6144, 16, 32, 4, 2, "bf16"), batch, "baseline", 12)
 
 
+# fp32 activations and weights: at most 8 rows on the one-row-per-wave fp32 kernel, more
+# on 64x64 fp32 MFMA tiles
+@pytest.mark.parametrize("batch", [1, 8, 9, 40, 129])
+def test_decode_f32_batches(batch):
+    _decode_batch_case(synth.LayerShape(96, 256, 16, 32, 4, 2, "f32"), batch, "stress", 14)
+
+
 def _decode_batch_case(shape, batch, init, seed):
     from paper_2602_21144_amd import binding as B
     full = synth.make_layer(shape, seed, stress=(init == "stress"))
     rng = np.random.default_rng(100 + batch)
     E, N, K, P = shape.d_shard, shape.d_state, shape.d_conv, shape.shard_count
+    act = shape.act
     S = batch + 5
     slots = rng.permutation(S)[:batch].astype(np.int32)
-    cp0 = synth.round_bf16_f32(rng.normal(size=(S, shape.d_inner, K - 1)).astype(np.float32))
+    cp0 = rng.normal(size=(S, shape.d_inner, K - 1)).astype(np.float32)
+    if act == "bf16":
+        cp0 = synth.round_bf16_f32(cp0)
     sp0 = (rng.normal(size=(S, shape.d_inner, N)) * 0.5).astype(np.float32)
 
     g = GpuLayer(shape, full)
@@ -66,17 +76,18 @@ def _decode_batch_case(shape, batch, init, seed):
     sps = [sp0[:, r * E:(r + 1) * E].astype(np.float64) for r in range(P)]
     sl = torch.from_numpy(slots).cuda()
     for step in range(3):
-        xt = synth.make_tokens(rng, batch, shape.d_model, "bf16")
+        xt = synth.make_tokens(rng, batch, shape.d_model, act)
         yd = g.decode(xt, sl, conv, ssm)
-        d1, d2, _ = om.tp_decode_step(shards, xt.astype(np.float64), slots, cps, sps, "bf16")
+        d1, d2, _ = om.tp_decode_step(shards, xt.astype(np.float64), slots, cps, sps, act)
         cps = [d["conv_pool"] for d in d1]
         sps = [d["ssm_pool"] for d in d2]
         for r in range(P):
-            assert_close(host(yd[r]), d2[r]["y"], TOL["bf16"], f"step {step} shard {r}")
+            assert_close(host(yd[r]), d2[r]["y"], TOL[act], f"step {step} shard {r}")
     for r in range(P):
         assert B.take_status(g._dws[r]) == 0
-        assert_close(host(ssm[r]), sps[r], STATE_TOL, f"ssm_pool shard {r}")
-        assert_close(host(conv[r]), cps[r], TOL["bf16"], f"conv_pool shard {r}")
+        # fp32: nothing is rounded on the way to the state (2e-5 as after a prefill)
+        assert_close(host(ssm[r]), sps[r], STATE_TOL if act == "bf16" else 2e-5, f"ssm_pool shard {r}")
+        assert_close(host(conv[r]), cps[r], TOL[act], f"conv_pool shard {r}")
 
 
 def test_decode_bad_slot_is_flagged():
