@@ -159,6 +159,15 @@ def test_m2_prefill_then_decode(P, G, stress):
     _run_case(sh, full, lens, hi, seed=7 + P + G)
 
 
+@pytest.mark.parametrize("K", [2, 3])
+def test_m2_conv_widths(K):
+    """Convolution widths 2 and 3 through prefill (continuing and fresh sequences) and the
+    fused decode in_proj's conv window."""
+    sh = synth.Mamba2Shape(128, 16, 64, 128, 2, K, 2, "bf16")
+    full = synth.make_mamba2_layer(sh, 60 + K, stress=True)
+    _run_case(sh, full, [40, 1, 0, 77], np.array([1, 0, 1, 1], np.int32), seed=60 + K)
+
+
 def test_m2_windows_of_several_chunks():
     """Long enough that each (window, head) workgroup walks several chunks, with a second
     sequence after it and a continuing start."""
