@@ -224,8 +224,10 @@ def _scan_inputs(rng, T, E, R, act, stress=False):
 
 @pytest.mark.parametrize("act", ["f32", "bf16"])
 @pytest.mark.parametrize("E", [128, 512])
+# the last case: 200 sequences of 0..4 tokens, so that most 8-token blocks hold several
+# sequence ends (the main pass's per-token path) and windows hold dozens of sequences
 @pytest.mark.parametrize("lens", [[70, 1, 0, 33, 100, 31, 65], [300], [1, 2, 3, 31, 32, 33, 64, 65, 0, 5],
-                                  [7, 0, 0, 9, 1]])
+                                  [7, 0, 0, 9, 1], [int(v) for v in np.random.default_rng(9).integers(0, 5, 200)]])
 def test_selective_scan(B, act, E, lens):
     rng = np.random.default_rng(sum(lens) + len(lens) + E)
     shape = synth.LayerShape(64, E, 16, 16, 4, 1, act)
