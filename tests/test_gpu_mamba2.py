@@ -168,6 +168,17 @@ def test_m2_conv_widths(K):
     _run_case(sh, full, [40, 1, 0, 77], np.array([1, 0, 1, 1], np.int32), seed=60 + K)
 
 
+def test_m2_many_short_sequences():
+    """60 sequences of 0..5 tokens, some continuing: chunks holding many sequence starts and
+    ends, then decode steps."""
+    sh = synth.Mamba2Shape(128, 16, 64, 128, 1, 4, 2, "bf16")
+    full = synth.make_mamba2_layer(sh, 70, stress=True)
+    rng = np.random.default_rng(70)
+    lens = [int(v) for v in rng.integers(0, 6, 60)]
+    hi = (rng.random(60) < 0.4).astype(np.int32)
+    _run_case(sh, full, lens, hi, seed=71, decode_steps=2)
+
+
 def test_m2_windows_of_several_chunks():
     """Long enough that each (window, head) workgroup walks several chunks, with a second
     sequence after it and a continuing start."""
