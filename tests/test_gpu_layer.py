@@ -255,10 +255,11 @@ class GpuStack:
         return out
 
 
-@pytest.mark.parametrize("act,bcdt", [("f32", False), ("bf16", False), ("bf16", True)])
-def test_full_width_stack_calls(act, bcdt):
+# K = 1: no conv history, the stack's conv pools are empty (null pointers)
+@pytest.mark.parametrize("act,bcdt,K", [("f32", False, 4), ("bf16", False, 4), ("bf16", True, 4), ("bf16", False, 1)])
+def test_full_width_stack_calls(act, bcdt, K):
     from paper_2602_21144_amd import binding as B
-    shape = synth.LayerShape(128, 256, 16, 16, 4, 1, act)
+    shape = synth.LayerShape(128, 256, 16, 16, K, 1, act)
     st = synth.make_stack(shape, 4, 40, stress=True)
     S = 4
     g = GpuStack(shape, st, bcdt, S)
