@@ -6,7 +6,11 @@
 //     decode step): whole-line loads into registers, re-laid out through LDS as MFMA
 //     fragments (gemm_gemv_kernel);
 //   - direct (up to 64 rows, any K, fp32 activations): 16-byte fragment loads straight
-//     into v_mfma_f32_16x16x32_bf16 (gemm_skinny_kernel).
+//     into v_mfma_f32_16x16x32_bf16 (gemm_skinny_kernel); for 17..64 bf16 rows over wide
+//     outputs, 32 columns per workgroup (gemm_skinny32_kernel), which halves the
+//     activation re-reads.
+// The streamed kernel can also apply Mamba-2's gated RMSNorm to its activations as they
+// are loaded (out_proj of a Mamba-2 decode step).
 //
 // Epilogues fuse the per-channel work that follows each projection in a decode step
 // (Section IV-A: the cache is read and advanced in place, with no prefix rescan):
