@@ -483,8 +483,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
 }
 
 // waves per workgroup for the streamed variant (0: it does not apply). Grids that fill
-// the CUs take 4 waves of up to 10 stages each (8 waves for longer K); small grids take
-// 16 waves of up to 4 stages, so that the few CUs in use keep many blocks in flight.
+// the CUs take 8 waves of up to 5 stages each (up to 10 for longer K; 4 waves for K up to
+// 1280); small grids take 16 waves of up to 4 stages, so that the few CUs in use keep many
+// blocks in flight. Shorter runs per wave shorten the tail after the loads land: with 8
+// waves instead of 4 at K = 2560, the 2.8B half shard's decode in_proj+conv took 7.6
+// instead of 8.4 us and its step 21.5 instead of 22.5 us (10 waves: 22.1 us).
 // (Spreading N over exactly one workgroup per CU, ceil(N / 256) rows each, shortened the
 // kernels' span but not a decode step, so the tiles stay 16 columns wide.)
 int gemv_waves(const SkinnyArgs& p) {
@@ -494,7 +497,7 @@ int gemv_waves(const SkinnyArgs& p) {
     if ((int64_t)p.M * p.lda * 2 >= (int64_t)1 << 31 || (int64_t)16 * p.ldb * 2 >= (int64_t)1 << 31) return 0;
     const int nall = p.K / kGemvBK;
     if ((p.N + 15) / 16 < 128) return nall <= 16 * 4 ? 16 : 0;
-    if (nall <= 4 * 10) return 4;
+    if (nall <= 4 * 5) return 4;
     return nall <= 8 * 10 ? 8 : 0;
 }
 
@@ -505,7 +508,7 @@ hipError_t launch_gemv(const SkinnyArgs& p, int nw, hipStream_t s) {
     if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, EPI>), grid, block, 0, s, p);   \
     else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, EPI>), grid, block, 0, s, p);
     if (nw == 4) { SSM_GEMV(4, 10) }
-    else if (nw == 8) { SSM_GEMV(8, 10) }
+    else if (nw == 8) { if (p.K / kGemvBK <= 8 * 5) { SSM_GEMV(8, 5) } else { SSM_GEMV(8, 10) } }
     else { SSM_GEMV(16, 4) }
 #undef SSM_GEMV
     return hipGetLastError();
@@ -596,6 +599,7 @@ hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s) {
     if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, kEpiStoreBf16, true>), grid, block, 0, s, p);   \
     else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, kEpiStoreBf16, true>), grid, block, 0, s, p);
     if (nw == 4) { SSM_GEMV_N(4, 10) }
+    else if (p.K / kGemvBK <= 8 * 5) { SSM_GEMV_N(8, 5) }
     else { SSM_GEMV_N(8, 10) }
 #undef SSM_GEMV_N
     return hipGetLastError();
