@@ -556,8 +556,10 @@ template <bool AF, int EPI>
 hipError_t launch_epi(const SkinnyArgs& p, hipStream_t s) {
     // narrow outputs (under 64 column tiles: x_proj) take 16-row tiles at any M, so that the
     // row tiles spread over more workgroups: at 64 rows x_proj 8.8 -> 4.5 us (1280-channel
-    // shard) and 17.5 -> 7.8 us (3584-channel shard, K = 3584)
-    if (p.M <= 16 || (EPI != kEpiState && (p.N + 15) / 16 < 64)) return launch_mb<16, AF, EPI>(p, s);
+    // shard) and 17.5 -> 7.8 us (3584-channel shard, K = 3584). The state step does so up to
+    // 32 rows (32 sequences, 1280 channels: 7.0 -> 5.7 us; at 64 rows 16-row tiles were slower)
+    if (p.M <= 16 || (EPI == kEpiState && p.M <= 32) || (EPI != kEpiState && (p.N + 15) / 16 < 64))
+        return launch_mb<16, AF, EPI>(p, s);
     // the state epilogue holds a whole state row per thread: at most 32-row tiles (8 waves)
     if (p.M <= 32 || EPI == kEpiState) return launch_mb<32, AF, EPI>(p, s);
     if constexpr (EPI != kEpiState) return launch_mb<64, AF, EPI>(p, s);
