@@ -35,8 +35,10 @@ def _dev(a, dt):
 GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 96, 224), (100, 300, 256), (257, 513, 64),
                (1000, 520, 768), (2048, 2048, 512), (300, 5120, 2560), (4089, 4091, 256), (200, 300, 96),
                # few rows with K a multiple of 64 (streamed-weight decode kernel: small grid of 16-wave
-               # workgroups, large grid of 4 waves, K long enough for 8 waves, 9..16 rows)
+               # workgroups; large grids of 8 waves of up to 5 stages, 8 waves of up to 10 stages, and
+               # 4 waves for K up to 1280, including waves left without a stage; 9..16 rows)
                (1, 200, 128), (5, 100, 640), (8, 5120, 2560), (16, 192, 2560), (13, 3000, 4096),
+               (12, 2080, 1344), (9, 2100, 1280), (3, 4096, 64),
                # 17..64 rows over at least 192 tiles of 32 columns (32-column fragment kernel: 32- and
                # 64-row tiles, ragged N, a K tail of 8)
                (17, 6150, 512), (40, 6176, 808), (64, 7168, 1024)]
