@@ -1,7 +1,8 @@
 """Mamba-2 (SSD) shard on the GPU against the float64 oracle on the same seeded inputs:
 packed prefill with fresh and continuing sequences (including empty ones and ones shorter
 than the convolution), the chunked state update across chunk and window boundaries, the
-sum-of-squares exchange of the gated norm with split and with replicated B/C groups,
+sum-of-squares exchange of the gated norm with split and with replicated B/C groups
+(also through the decode out_proj that applies the norm to its operand as it loads it),
 decode steps from the cache, and the Mamba-2 2.7B shard shape at full size (a sampled
 sequence recomputed by the oracle).
 """
@@ -166,6 +167,26 @@ def test_m2_conv_widths(K):
     sh = synth.Mamba2Shape(128, 16, 64, 128, 2, K, 2, "bf16")
     full = synth.make_mamba2_layer(sh, 60 + K, stress=True)
     _run_case(sh, full, [40, 1, 0, 77], np.array([1, 0, 1, 1], np.int32), seed=60 + K)
+
+
+# d_model 2048 gives out_proj 128 tiles of 16 columns, so decode batches of up to 16 take the
+# streamed out_proj with the gated norm applied to its operand as loaded: 4-wave workgroups
+# (K = 512 or 1024 per shard) and 8-wave ones (K = 2048), one norm group per row (G = 1) and
+# several, split over the shards or replicated on each
+@pytest.mark.parametrize("P,G,H", [(2, 1, 32), (2, 2, 16), (1, 4, 16), (1, 2, 32)])
+def test_m2_fused_norm_out_proj(P, G, H):
+    sh = synth.Mamba2Shape(2048, H, 64, 128, G, 4, P, "bf16")
+    full = synth.make_mamba2_layer(sh, 80 + G + H)
+    from paper_2602_21144_amd import binding as B
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True, "m2.decode.norm_out_proj")
+    try:
+        _run_case(sh, full, [20, 1, 0, 9, 33], np.array([1, 0, 1, 0, 1], np.int32), seed=80 + P + G, decode_steps=3)
+        torch.cuda.synchronize()
+    finally:
+        B.ssm_timing_enable(False)
+    # the decode steps took the fused launch (one per shard and step)
+    assert B.ssm_timing_collect()["m2.decode.norm_out_proj"][0] == 3 * P
 
 
 def test_m2_many_short_sequences():
