@@ -507,7 +507,7 @@ hipError_t launch_gemv(const SkinnyArgs& p, int nw, hipStream_t s) {
 #define SSM_GEMV(NW, NST)                                                                  \
     if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, EPI>), grid, block, 0, s, p);   \
     else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, EPI>), grid, block, 0, s, p);
-    if (nw == 4) { SSM_GEMV(4, 10) }
+    if (nw == 4) { SSM_GEMV(4, 5) }
     else if (nw == 8) { if (p.K / kGemvBK <= 8 * 5) { SSM_GEMV(8, 5) } else { SSM_GEMV(8, 10) } }
     else { SSM_GEMV(16, 4) }
 #undef SSM_GEMV
@@ -603,7 +603,7 @@ hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s) {
 #define SSM_GEMV_N(NW, NST)                                                                              \
     if (p.M <= 8) SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 1, kEpiStoreBf16, true>), grid, block, 0, s, p);   \
     else SSM_LAUNCH((gemm_gemv_kernel<NW, NST, 2, kEpiStoreBf16, true>), grid, block, 0, s, p);
-    if (nw == 4) { SSM_GEMV_N(4, 10) }
+    if (nw == 4) { SSM_GEMV_N(4, 5) }
     else if (p.K / kGemvBK <= 8 * 5) { SSM_GEMV_N(8, 5) }
     else { SSM_GEMV_N(8, 10) }
 #undef SSM_GEMV_N
