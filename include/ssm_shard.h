@@ -68,7 +68,8 @@ typedef enum ssm_dtype { SSM_F32 = 0, SSM_BF16 = 1 } ssm_dtype_t;
 /* Shape of one layer and of the shard this rank owns (Section IV-B). The shard owns
  * channels [shard_index * d_inner_shard, (shard_index + 1) * d_inner_shard).
  * Requirements: d_inner_shard * shard_count == d_inner_total; d_state == 16;
- * d_conv in [1, 4]; d_model, d_inner_shard and dt_rank multiples of 16. */
+ * d_conv in [1, 4]; d_model and dt_rank multiples of 16; d_inner_shard a multiple
+ * of 64 (the scan and decode kernels give each 64-lane wave 64 whole channels). */
 typedef struct ssm_shard_desc {
     int32_t d_model;        /* residual width                                   */
     int32_t d_inner_total;  /* E_tot, intermediate channels of the whole layer  */

@@ -46,8 +46,10 @@ def _slice(a, r, E):
 @pytest.mark.parametrize("act", ["f32", "bf16"])
 @pytest.mark.parametrize("P", [1, 2])
 @pytest.mark.parametrize("init", ["baseline", "stress", "general"])
-# dt rank 16: dt_proj on the staged tiles with fp32 A (rounded on load); dt rank 32 with 192
-# channels per shard: delta rounded once, then DMA-fed tiles over a ragged last 128-column tile
+# dt rank 16 at these 237 tokens: dt_proj on the streamed skinny kernel with fp32 A (rounded
+# on load; the staged fp32-A tiles take over above 512 tokens, see test_prefill_staged_dt_proj);
+# dt rank 32 with 192 channels per shard: delta rounded once, then DMA-fed tiles over a
+# ragged last 128-column tile
 @pytest.mark.parametrize("dims", [(256, 16), (384, 32)])
 def test_prefill_then_decode(act, P, init, dims):
     shape, full = _case(act, P, init, seed=3, E_tot=dims[0], R=dims[1])
@@ -104,6 +106,42 @@ def test_prefill_then_decode(act, P, init, dims):
     for r in range(P):
         assert_close(host(ssm[r]), sps[r], 1e-4 if act == "bf16" else 2e-5, f"ssm_pool after decode, shard {r}")
         assert_close(host(conv[r]), cps[r], tol, f"conv_pool after decode, shard {r}")
+
+
+@pytest.mark.parametrize("P", [1, 2])
+def test_prefill_staged_dt_proj(P):
+    """bf16, dt rank 16 (not a multiple of 32) and more than 512 tokens: dt_proj runs on the
+    staged 128x128 tiles that round the fp32 delta to bf16 while staging it. Stress init, so
+    the state path carries y; three sequences, one continuing from a cached state."""
+    shape, full = _case("bf16", P, "stress", seed=9, E_tot=256, R=16)
+    E = shape.d_shard
+    rng = np.random.default_rng(23)
+    lens = [401, 333, 77]
+    S = 5
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    slots = np.array([3, 0, 4], np.int32)
+    hi = np.array([0, 1, 0], np.int32)
+    T = int(cu[-1])
+    x = synth.make_tokens(rng, T, shape.d_model, "bf16")
+    cp0, sp0 = _pools_host(rng, shape, S, "bf16")
+    g = GpuLayer(shape, full)
+    from paper_2602_21144_amd import binding as B
+    meta = B.SeqMeta(cu, slots, hi, S)
+    conv, ssm = g.new_pools(S)
+    for r in range(P):
+        conv[r].copy_(g.to_dev(_slice(cp0, r, E)))
+        ssm[r].copy_(torch.from_numpy(np.ascontiguousarray(_slice(sp0, r, E))).cuda())
+    ys = g.prefill(x, meta, conv, ssm)
+    for r in range(P):
+        assert B.take_status(g.last_ws[r]) == 0
+    shards = [om.shard_weights(f64(full), r, P) for r in range(P)]
+    cps = [_slice(cp0, r, E).astype(np.float64) for r in range(P)]
+    sps = [_slice(sp0, r, E).astype(np.float64) for r in range(P)]
+    s1, s2, _ = om.tp_prefill(shards, x.astype(np.float64), cu, slots, hi, cps, sps, "bf16")
+    for r in range(P):
+        assert_close(host(ys[r]), s2[r]["y"], TOL["bf16"], f"y_partial shard {r}")
+        assert_close(host(ssm[r]), s2[r]["ssm_pool"], 1e-4, f"ssm_pool shard {r}")
+        assert_close(host(conv[r]), s1[r]["conv_pool"], TOL["bf16"], f"conv_pool shard {r}")
 
 
 @pytest.mark.parametrize("act", ["f32", "bf16"])

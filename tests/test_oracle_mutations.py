@@ -26,6 +26,8 @@ def _pins_pass() -> bool:
         pins.test_scan_special_cases,
         pins.test_conv_matches_torch_grouped_conv1d,
         lambda: pins.test_state_cache_invariant_prefill_then_decode("f64"),
+        pins.test_bf16_rounding_points_worked_example,
+        pins.test_bf16_storage_points_are_bf16_values,
     ]
     for c in checks:
         try:
@@ -40,7 +42,8 @@ def test_unmutated_oracle_passes():
 
 
 _orig = {k: getattr(om, k) for k in ("in_proj", "conv1d_silu", "split_x_dbl", "discretize",
-                                      "ssm_recurrence", "gate", "silu", "shard_weights", "x_proj")}
+                                      "ssm_recurrence", "gate", "silu", "shard_weights", "x_proj",
+                                      "dt_proj", "out_proj")}
 
 
 def _swap_xz(w, x, act):
@@ -121,6 +124,41 @@ def _shard_interleaved(full, r, P):
     return s
 
 
+def _delta_unrounded(w, delta, act):
+    # dt_proj fed the fp32 delta instead of its bf16 rounding
+    return om.rnd(np.asarray(delta, np.float64) @ np.asarray(w["W_dt"], np.float64).T, act)
+
+
+def _dt_unrounded(w, delta, act):
+    return om.rnd(delta, act) @ np.asarray(w["W_dt"], np.float64).T
+
+
+def _dt_rounded_after_bias(w, delta, act):
+    # dt_proj's output kept exact; the rounding moved behind the bias add (below)
+    return om.rnd(delta, act) @ np.asarray(w["W_dt"], np.float64).T
+
+
+def _discretize_rounding_sum(dt, b_dt, A_log):
+    v = om.round_bf16(np.asarray(dt, np.float64) + np.asarray(b_dt, np.float64)[None, :])
+    return om.softplus(v), -np.exp(np.asarray(A_log, np.float64))
+
+
+def _gate_unrounded(y, z, act):
+    return np.asarray(y, np.float64) * om.silu(z)
+
+
+def _out_proj_unrounded(w, g, act):
+    return np.asarray(g, np.float64) @ np.asarray(w["W_out"], np.float64).T
+
+
+def _u_unrounded(w, xs, st0, act):
+    return _orig["conv1d_silu"](w, xs, st0, "f64")
+
+
+def _xz_unrounded(w, x, act):
+    return _orig["in_proj"](w, x, "f64")
+
+
 MUTATIONS = {
     "x and z halves swapped": ("in_proj", _swap_xz),
     "convolution taps reversed": ("conv1d_silu", _reversed_taps),
@@ -134,7 +172,20 @@ MUTATIONS = {
     "gate without SiLU": ("gate", _gate_without_silu),
     "SiLU as sigmoid": ("silu", _silu_as_sigmoid),
     "in_proj sliced as one block": ("shard_weights", _shard_interleaved),
+    "delta not rounded before dt_proj": ("dt_proj", _delta_unrounded),
+    "dt not rounded": ("dt_proj", _dt_unrounded),
+    "xz not rounded": ("in_proj", _xz_unrounded),
+    "u not rounded": ("conv1d_silu", _u_unrounded),
+    "g not rounded": ("gate", _gate_unrounded),
+    "y_partial not rounded": ("out_proj", _out_proj_unrounded),
 }
+
+
+def test_pins_catch_rounding_moved_behind_the_bias(monkeypatch):
+    """dt kept exact by dt_proj and rounded only after the bias is added (two coordinated edits)."""
+    monkeypatch.setattr(om, "dt_proj", _dt_rounded_after_bias)
+    monkeypatch.setattr(om, "discretize", _discretize_rounding_sum)
+    assert not _pins_pass()
 
 
 @pytest.mark.parametrize("name", list(MUTATIONS))

@@ -89,6 +89,69 @@ def test_conv_hand_worked_example():
         assert np.array_equal(st[0], newhist)
 
 
+def _bf16_torch(v):
+    """bf16 round trip through torch's conversion (round to nearest even)."""
+    return torch.tensor(np.asarray(v, np.float64), dtype=torch.float64).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def _read_rounding_golden():
+    rows = []
+    for line in open(os.path.join(GOLD, "bf16_rounding_worked_example.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            rows.append([float(v) for v in line.split()])
+    return np.array(rows)
+
+
+def test_bf16_rounding_points_worked_example():
+    """Where a bf16 configuration rounds: delta before dt_proj, dt after it, the bias added
+    to the rounded dt in full precision (tests/golden/bf16_rounding_worked_example.txt),
+    then g and y_partial stored in bf16 (torch's conversion as the reference). The prefill
+    and the decode step must agree on all of it."""
+    rows = _read_rounding_golden()
+    w = {"W_dt": np.ones((1, 3)), "b_dt": np.array([2.0 ** -10]), "A_log": np.zeros((1, 1)),
+         "D": np.zeros(1), "W_out": np.array([[1.0], [3.0]])}
+    z = 3.0
+    silu_z = z / (1.0 + math.exp(-z))
+    x_dbl = np.array([[r[1], r[2], r[3], 1.0, 1.0] for r in rows])      # [delta | B | C]
+    st1 = {"xz": np.array([[0.5, z], [0.5, z]]), "u": np.ones((2, 1))}
+    pre = om.prefill_stage2(w, st1, x_dbl, [0, 1, 2], [0, 1], [0, 0], np.zeros((2, 1, 1)), "bf16")
+    dec = om.decode_stage2(w, st1, x_dbl, [0, 1], np.zeros((2, 1, 1)), "bf16")
+    for out in (pre, dec):
+        for i, r in enumerate(rows):
+            dt_exp, delta_exp = r[4], r[6]
+            assert out["dt"][i, 0] == dt_exp, (i, out["dt"][i, 0], dt_exp)
+            # state = Delta (h0 = 0, B = u = 1), stored as float32
+            assert abs(out["ssm_pool"][i, 0, 0] - delta_exp) <= 2.0 ** -23 * delta_exp, (i, out["ssm_pool"][i])
+            g_exp = _bf16_torch(delta_exp * silu_z)
+            assert out["g"][i, 0] == g_exp, (i, out["g"][i, 0], g_exp)
+            assert out["y"][i, 0] == g_exp and out["y"][i, 1] == _bf16_torch(3.0 * g_exp), (i, out["y"][i])
+
+
+def test_bf16_storage_points_are_bf16_values():
+    """Every tensor a bf16 configuration stores (xz, u, dt, g, y_partial, conv history) holds
+    bf16 values and every state a float32 value, in prefill and decode (torch's conversions
+    as the reference). With the worked example this fixes each rounding point."""
+    shape = synth.tiny_shape(act="bf16")
+    w = _f64(synth.make_general_layer(shape, 4))
+    rng = np.random.default_rng(8)
+    x = synth.round_bf16_f32(rng.normal(size=(11, 8)).astype(np.float32)).astype(np.float64)
+    xt = synth.round_bf16_f32(rng.normal(size=(1, 8)).astype(np.float32)).astype(np.float64)
+    E, N, K = 6, 4, 4
+    pre = om.prefill(w, x, [0, 11], [0], [0], np.zeros((1, E, K - 1)), np.zeros((1, E, N)), "bf16")
+    dec = om.decode_step(w, xt, [0], pre["conv_pool"], pre["ssm_pool"], "bf16")
+    for out in (pre, dec):
+        for k in ("xz", "u", "dt", "g", "y", "conv_pool"):
+            v = np.asarray(out[k], np.float64)
+            assert np.array_equal(v, _bf16_torch(v)), k
+        st = np.asarray(out["ssm_pool"], np.float64)
+        assert np.array_equal(st, st.astype(np.float32).astype(np.float64))
+    # and the rounding is not the identity here: the unrounded pipeline differs
+    exact = om.prefill(w, x, [0, 11], [0], [0], np.zeros((1, E, K - 1)), np.zeros((1, E, N)), "f64")
+    for k in ("xz", "u", "dt", "g", "y"):
+        assert not np.array_equal(pre[k], exact[k]), k
+
+
 def test_softplus_and_silu_values():
     assert om.softplus(0.0) == pytest.approx(math.log(2.0), abs=1e-16)
     assert om.softplus(25.0) == 25.0            # threshold branch
