@@ -180,6 +180,24 @@ int ssm_shard_decode_stage2(const ssm_shard_desc_t* desc, const ssm_shard_weight
                             float* ssm_pool, int32_t num_slots, void* y_partial,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Decode step for callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same computation and kernels as
+ * ssm_shard_decode_step, with its workspace taken from a static device array of
+ * SSM_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on until the
+ * process ends. The call allocates nothing (leave ssm_timing_enable off: timed launches
+ * may create events). A batch whose workspace would exceed the array (the size
+ * ssm_shard_decode_workspace_bytes reports) returns SSM_E_WORKSPACE and enqueues nothing.
+ * The array is shared by every call on one GPU, and calls that overlap in time on one
+ * GPU race; run them on one stream or otherwise in order. Bad device slots still never
+ * cause an out-of-range access, but their status bits are not reported here (validate
+ * slots with ssm_shard_check_meta_host, or use ssm_shard_decode_step to read them).
+ * The stream must belong to the current device. */
+#define SSM_NOALLOC_SCRATCH_BYTES (32u << 20)
+int ssm_shard_decode_step_noalloc(const ssm_shard_desc_t* desc, const ssm_shard_weights_t* w,
+                                  const void* x_t, int32_t batch, const int32_t* cache_slot,
+                                  void* conv_pool, float* ssm_pool, int32_t num_slots,
+                                  void* y_partial, hipStream_t stream);
+
 /* ------------------------------------------------------------------ utilities
  * Channel splitter (Section IV-B): copy this shard's slices of full-width weights
  * (full: same fields at full width, E_tot channels) into caller-allocated shard

@@ -25,6 +25,8 @@ SSM_OK = 0
 ERRORS = {-1: "SSM_E_INVAL", -2: "SSM_E_ALIGN", -3: "SSM_E_WORKSPACE", -4: "SSM_E_SLOT",
           -5: "SSM_E_SEQLENS", -6: "SSM_E_HIP"}
 SSM_STATUS_BAD_SLOT, SSM_STATUS_BAD_SEQLENS = 1, 2
+SSM_E_INVAL, SSM_E_ALIGN, SSM_E_WORKSPACE = -1, -2, -3
+SSM_NOALLOC_SCRATCH_BYTES = 32 << 20   # the static scratch of ssm_shard_decode_step_noalloc
 
 
 class SsmError(RuntimeError):
@@ -81,6 +83,7 @@ _SIGS = {
     "ssm_shard_prefill_stage1": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_shard_prefill_stage2": ([_P, _P, _P, _I64, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_shard_decode_step": ([_P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
+    "ssm_shard_decode_step_noalloc": ([_P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
     "ssm_shard_decode_stage1": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_shard_decode_stage2": ([_P, _P, _P, _I32, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_shard_slice_weights": ([_P, _P, _P, _P], _I32),
@@ -270,6 +273,12 @@ def _m_ssm_shard_decode_step(desc, weights, x_t, cache_slot, conv_pool, ssm_pool
             _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _ptr(ws), ws.numel(), _stream(stream)), (desc, w)
 
 
+def _m_ssm_shard_decode_step_noalloc(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, stream=None):
+    w = _w(weights)
+    return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0], _ptr(cache_slot), _ptr(conv_pool),
+            _ptr(ssm_pool), conv_pool.shape[0], _ptr(y_partial), _stream(stream)), (desc, w)
+
+
 def _m_ssm_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream=None):
     w = _w(weights)
     return (ctypes.byref(desc), ctypes.byref(w), _ptr(x_t), x_t.shape[0], _ptr(cache_slot), _ptr(conv_pool),
@@ -310,6 +319,10 @@ def ssm_shard_prefill_stage2(desc, weights, x_dbl, meta: SeqMeta, ssm_pool, y_pa
 
 def ssm_shard_decode_step(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream=None):
     _call("ssm_shard_decode_step", desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, ws, stream)
+
+
+def ssm_shard_decode_step_noalloc(desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, stream=None):
+    _call("ssm_shard_decode_step_noalloc", desc, weights, x_t, cache_slot, conv_pool, ssm_pool, y_partial, stream)
 
 
 def ssm_shard_decode_stage1(desc, weights, x_t, cache_slot, conv_pool, x_dbl_partial, ws, stream=None):

@@ -7,9 +7,11 @@
 //   stage 2: dt_proj GEMM -> dt; selective scan -> g (and the final states); out_proj GEMM -> y
 // Decode: the same with one token per sequence and the single-step kernels.
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -352,6 +354,44 @@ int decode_checks(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, int32
     return SSM_OK;
 }
 
+// ------------------------------------------------- decode step without allocation
+// The decode workspace (status word, xz, u, x_dbl, dt, g, split-K partials) of
+// ssm_shard_decode_step_noalloc lives in this file-scope device array. Every GPU the
+// library runs on holds its own copy, at its own address, until the process ends. In host
+// code `scratch` names a host-side stand-in, not device memory: its device address comes
+// from hipGetSymbolAddress, once per device, and only that address is handed to kernels.
+static __device__ __align__(256) char scratch[SSM_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_dev[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// device address of `scratch` on the device the launch goes to (looked up on the first
+// call on that device, with that device current)
+int scratch_address(hipStream_t s, void** out) {
+    int dev = 0;
+    SSM_TRY_HIP(hipGetDevice(&dev), "hipGetDevice");
+    if (s) {
+        hipDevice_t sdev = 0;
+        SSM_TRY_HIP(hipStreamGetDevice(s, &sdev), "hipStreamGetDevice");
+        if ((int)sdev != dev)
+            return fail(SSM_E_INVAL, "the stream belongs to device %d but device %d is current", (int)sdev, dev);
+    }
+    if (dev < 0 || dev >= kMaxDevices) return fail(SSM_E_INVAL, "device %d: at most %d devices", dev, kMaxDevices);
+    void* p = g_scratch_dev[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_dev[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            SSM_TRY_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+            if (!p) return fail(SSM_E_HIP, "hipGetSymbolAddress(scratch) returned null");
+            g_scratch_dev[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return SSM_OK;
+}
+
 }  // namespace
 
 // ======================================================================= C ABI
@@ -491,6 +531,31 @@ int ssm_shard_decode_step(const ssm_shard_desc_t* d, const ssm_shard_weights_t* 
         SSM_TRY(check_ptr(x, "x_t"));
         SSM_TRY(check_ptr(y, "y_partial"));
     }
+    SSM_TRY(decode1(d, w, x, B, slot, conv_pool, S, L.xdbl, L, s));
+    return decode2(d, w, L.xdbl, B, slot, ssm_pool, S, y, L, s);
+}
+
+int ssm_shard_decode_step_noalloc(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void* x,
+                                  int32_t B, const int32_t* slot, void* conv_pool, float* ssm_pool, int32_t S,
+                                  void* y, hipStream_t s) {
+    SSM_TRY(common_checks(d, w, B, S));
+    if (B < 0) return fail(SSM_E_INVAL, "batch %d", B);
+    if (B > 0 && !slot) return fail(SSM_E_INVAL, "cache_slot is null");
+    const size_t need = decode_layout(d, B, nullptr).total;
+    if (need > (size_t)SSM_NOALLOC_SCRATCH_BYTES)
+        return fail(SSM_E_WORKSPACE,
+                    "a decode step of %d sequences needs %zu bytes of scratch; the static scratch holds %zu "
+                    "(use ssm_shard_decode_step with a workspace)",
+                    B, need, (size_t)SSM_NOALLOC_SCRATCH_BYTES);
+    if (d->d_conv > 1) SSM_TRY(check_ptr(conv_pool, "conv_pool"));  // K = 1 keeps no history
+    SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
+    if (B > 0) {
+        SSM_TRY(check_ptr(x, "x_t"));
+        SSM_TRY(check_ptr(y, "y_partial"));
+    }
+    void* base = nullptr;
+    SSM_TRY(scratch_address(s, &base));
+    const DecodeWs L = decode_layout(d, B, base);
     SSM_TRY(decode1(d, w, x, B, slot, conv_pool, S, L.xdbl, L, s));
     return decode2(d, w, L.xdbl, B, slot, ssm_pool, S, y, L, s);
 }
