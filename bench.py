@@ -1,21 +1,27 @@
 #!/usr/bin/env python3
 """Benchmark of the selective-SSM mixer shard on one MI355X.
 
-Workload: a Mamba-2.8B-shaped layer (d_model 2560, d_inner 5120 split over 2 ranks, so
-this GPU runs the 2560-channel shard 0; N 16, dt_rank 160, conv 4), bf16 activations
-and weights with fp32 scan state; 8 prompts of 2048 tokens prefilled, then 128 decode
-steps over the 8 sequences. One step = that prefill plus the 128 decode steps.
+Headline workload (the largest of the five): the hybrid-stack-shaped mixer, shard 0 of a
+2-way channel split (d_model 3584, 3584 of 7168 channels, d_state 16, dt_rank 224,
+d_conv 4), serving 64 prompts with lengths uniform in [128, 8192] packed and prefilled in
+2048-token chunks, each chunk followed by one decode step for every sequence already
+prefilled, until each has 64 decode tokens; seed 4. It runs at float32, the paper's
+default precision (activations, weights, accumulation and state), and at bf16 storage
+with fp32 state beside it. One step = the whole schedule.
 
-Per shard, the work of one step is: stage 1 (in_proj, conv1d+SiLU, x_proj), the sum of
-the x_proj partials over ranks (here: shard 1's partial, computed outside the timed
-region because it is the other GPU's work, added by the library's reduce kernel), and
-stage 2 (dt_proj, selective scan, out_proj); the same for every decode step.
+Per shard, a prefill chunk or decode step is stage 1 (in_proj, conv1d + SiLU, x_proj),
+the x_proj exchange (the sum of the shards' partials: a cross-GPU reduction, not this
+shard's work) and stage 2 (dt_proj, selective scan, out_proj). The exchange is excluded:
+an untimed pass runs every shard's stage 1 over the whole schedule and keeps the summed
+x_proj output of each chunk and step on the device; the timed steps run shard 0's stage 1
+and then stage 2 on that sum.
 
-Prints one JSON line: prefill tokens/s (value), decode us/step, ms per step, a roofline
-entry for the kernel that takes the most time in a step (its duration measured during the
-timed region by HIP events bound to every 16th of its dispatches on the launch stream, its HBM
-traffic from the committed rocprofv3 counter summary), a per-kernel breakdown from one
-extra profiled step, and the CPU oracle timed on a bounded sample on the host.
+Prints one JSON line: prefill tokens per second of the whole schedule (value), ms per step,
+prefill-only tokens/s, decode us/step, a roofline entry for the kernel that takes the most
+time (its duration from HIP events bound to its own dispatches during the timed region, its
+HBM traffic from the committed rocprofv3 counter summary), per-kernel figures from one
+extra step with every kernel timed, the four other workloads and the bf16 run of the
+headline schedule as extra objects, and the CPU oracle on a bounded sample.
 """
 from __future__ import annotations
 
@@ -31,57 +37,145 @@ if ROOT not in sys.path:
 
 METRIC = "selective-scan prefill tokens/s + decode µs/step per shard; % HBM/MFMA peak"
 PEAK_HBM_GBS = 8000.0
-PEAK_BF16_TFLOPS = 2500.0
-TIMING_EVERY = 16
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA
+# VALU issue: 256 CUs x 4 SIMDs, one wave64 instruction per SIMD every 4 cycles, 2.4 GHz
+PEAK_VALU_GINSTS = 256 * 4 * 2.4e9 / 4 / 1e9
+
+CONFIG_KEYS = {"c0": "mamba130m_f32", "c1": "mamba2.8b_tp2", "c2": "falcon7b_tp4_long",
+               "c3": "mamba2.8b_tp4_decode", "c4": "hybrid3584_tp2_mixed"}
+WORKLOAD_TEXT = {
+    "c0": "Mamba-130m-shaped mixer layer at full width (d_model 768, d_inner 1536, d_state 16, dt_rank 48, "
+          "d_conv 4): batch 1, prefill 256 then 16 decode steps; seed 0",
+    "c1": "Mamba-2.8B-shaped mixer layer, shard 0 of a 2-way channel split (d_model 2560, 2560 of 5120 channels, "
+          "d_state 16, dt_rank 160, d_conv 4): batch 8, prefill 2048 then 128 decode steps; seed 1",
+    "c2": "Falcon-Mamba-7B-shaped long-context prefill, shard 0 of a 4-way split (d_model 4096, 2048 of 8192 "
+          "channels, d_state 16, dt_rank 256, d_conv 4): batch 4 x prefill 16384, final conv and SSM states "
+          "written to the cache; seed 2",
+    "c3": "Decode-heavy serving, Mamba-2.8B-shaped shard 0 of a 4-way split (d_model 2560, 1280 of 5120 "
+          "channels, d_state 16, dt_rank 160, d_conv 4): 256 sequences prefilled with 512 tokens to fill the "
+          "cache, then 512 single-token decode steps over all 256; seed 3",
+    "c4": "Hybrid-stack-shaped mixer, shard 0 of a 2-way split (d_model 3584, 3584 of 7168 channels, d_state 16, "
+          "dt_rank 224, d_conv 4): 64 prompts with lengths uniform in [128, 8192] packed in index order and "
+          "prefilled in 2048-token chunks (per-sequence state continuation), one decode step after each chunk "
+          "for every fully prefilled sequence, then decode steps until each sequence has 64; seed 4",
+}
+PROFILE_STEM = {"c0": "mamba130m_full_b1x256_dec16", "c1": "mamba2.8b_shard0of2_b8x2048_dec128",
+                "c2": "falcon7b_shard0of4_b4x16384", "c3": "mamba2.8b_shard0of4_b256x512_dec512",
+                "c4": "hybrid3584_shard0of2_64prompts_chunk2048"}
+
+
+def profile_stem(key, act):
+    """Stem of the committed rocprofv3 summaries of a workload (the headline workload runs
+    at two precisions, so its stem names the precision)."""
+    return PROFILE_STEM[key] + (f"_{act}" if key == "c4" else "")
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic(name, sh, T, Bd, nseq):
-    """(roof, amount per launch, unit) of a kernel role: flops for the dense in/out
-    projections in prefill, else bytes each operand must move once (s = act bytes)."""
+# ------------------------------------------------------------------ workloads (host)
+def draw_workload(key, act=None, stress=False):
+    """Seeded host arrays of one workload, in the recipe's draw order (full-width weights,
+    then prompt lengths where they vary, prompts, decode inputs, cache slots), and its
+    schedule: a list of phases, each a prefill call over packed pieces or a decode step over
+    a batch of sequences. The same draws as the parity tests."""
+    import dataclasses
+
+    import numpy as np
+
+    from paper_2602_21144_amd import synth
+    cfg = synth.CONFIGS[CONFIG_KEYS[key]]
+    sh = cfg["shape"] if act is None else dataclasses.replace(cfg["shape"], act=act)
+    full = synth.make_layer(sh, cfg["seed"], stress=stress)
+    rng = full.pop("_rng")
+    phases = []
+    if key == "c4":
+        nseq, steps = cfg["batch"], cfg["decode_steps"]
+        lo, hi = cfg["len_range"]
+        lengths = [int(v) for v in rng.integers(lo, hi, endpoint=True, size=nseq)]
+        x_all = synth.make_tokens(rng, int(sum(lengths)), sh.d_model, sh.act)
+        dec_x = synth.make_tokens(rng, nseq * steps, sh.d_model, sh.act).reshape(nseq, steps, sh.d_model)
+        slots = synth.make_slots(rng, nseq)
+        for kind, what in synth.serving_schedule(lengths, cfg["chunk"], steps):
+            if kind == "prefill":
+                lens = [p[2] for p in what["pieces"]]
+                seqs = [p[0] for p in what["pieces"]]
+                phases.append({"kind": "prefill", "x": x_all[what["start"]:what["stop"]],
+                               "cu": np.concatenate([[0], np.cumsum(lens)]).astype(np.int32),
+                               "slots": slots[seqs].astype(np.int32),
+                               "has_init": np.array([1 if p[1] > 0 else 0 for p in what["pieces"]], np.int32)})
+            else:
+                phases.append({"kind": "decode", "x": np.stack([dec_x[i, k] for i, k in what]),
+                               "slots": slots[[i for i, _ in what]].astype(np.int32)})
+        S = nseq + 16
+        info = {"prompts": nseq, "prompt_tokens": int(sum(lengths)), "chunk": cfg["chunk"],
+                "decode_tokens_per_sequence": steps}
+    else:
+        Bsz, L, nd = cfg["batch"], cfg["prefill_len"], cfg["decode_steps"]
+        x = synth.make_tokens(rng, Bsz * L, sh.d_model, sh.act)
+        xdec = [synth.make_tokens(rng, Bsz, sh.d_model, sh.act) for _ in range(nd)]
+        slots = synth.make_slots(rng, Bsz)
+        S = Bsz + 16
+        phases.append({"kind": "prefill", "x": x, "cu": np.arange(0, Bsz * L + 1, L, dtype=np.int32),
+                       "slots": slots, "has_init": np.zeros(Bsz, np.int32)})
+        for xt in xdec:
+            phases.append({"kind": "decode", "x": xt, "slots": slots})
+        info = {"batch": Bsz, "prefill_len": L, "decode_steps": nd}
+    return sh, full, phases, S, info
+
+
+# ------------------------------------------------------------ algorithmic work per kernel
+def kernel_work(sh, kind, n, nseq):
+    """Kernel roles one prefill call of n tokens (nseq sequences) or one decode step of n
+    sequences launches, as the library dispatches them, each with its roof and the work it
+    must do: flops for the dense in/out projections in prefill, else the bytes each operand
+    and result must move once (s = act bytes). The scan's three passes share one entry."""
     s = 2 if sh.act == "bf16" else 4
     E, dm, N, R, K, W = sh.d_shard, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv, sh.w_dbl
-    M = T if name.startswith("prefill") else Bd
-    table = {
-        "prefill.in_proj": ("mfma", 2.0 * T * 2 * E * dm),
-        "prefill.out_proj": ("mfma", 2.0 * T * dm * E),
-        "prefill.x_proj": ("hbm", T * E * s + W * E * s + T * W * 4),
-        "prefill.dt_round": ("hbm", T * R * 4 + T * R * 2),  # delta rounded to bf16 once
-        "prefill.dt_proj": ("hbm", T * R * s + E * R * s + T * E * s),
-        "prefill.conv1d": ("hbm", 2 * T * E * s + E * (K + 1) * s),
-        "prefill.conv_history": ("hbm", 2 * nseq * E * (K - 1) * s),
-        "prefill.scan_main": ("hbm", 4 * T * E * s + T * 2 * N * 4 + nseq * E * N * 4 + E * (N + 2) * 4),
-        "decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
-        # in_proj with the conv window fused: weights, x_t, u and z out, history read + write
-        "decode.in_proj_conv": ("hbm", 2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
-                                + E * (K + 1) * s),
-        # dt_proj with the state step fused: weights, delta, B and C, u and z, g, state read + write
-        "decode.dt_proj_state": ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4
-                                 + E * (N + 2) * 4),
-        "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
-        "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
-        "decode.dt_proj": ("hbm", E * R * s + M * R * 4 + M * E * s),
-        "decode.state_update": ("hbm", 2 * M * E * N * 4 + 4 * M * E * s + M * 2 * N * 4 + E * (N + 2) * 4),
-        "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s),
-    }
-    if name in table:
-        roof, amt = table[name]
-        return roof, float(amt), ("TFLOP/s" if roof == "mfma" else "GB/s")
-    if name == "exchange.reduce_add":
-        return "hbm", None, "GB/s"
-    return "hbm", None, "GB/s"
+    bf = sh.act == "bf16"
+    if kind == "prefill":
+        T = n
+        out = {"prefill.in_proj": ("mfma", 2.0 * T * 2 * E * dm),
+               "prefill.conv1d": ("hbm", 2 * T * E * s + E * (K + 1) * s),
+               "prefill.conv_history": ("hbm", 2 * nseq * E * (K - 1) * s),
+               "prefill.x_proj": ("hbm", T * E * s + W * E * s + T * W * 4),
+               "prefill.dt_proj": ("hbm", T * R * s + E * R * s + T * E * s),
+               "prefill.scan": ("hbm", 4 * T * E * s + T * 2 * N * 4 + 2 * nseq * E * N * 4 + E * (N + 2) * 4),
+               "prefill.out_proj": ("mfma", 2.0 * T * dm * E)}
+        if bf and R % 32 == 0 and T > 64:
+            out["prefill.dt_round"] = ("hbm", T * R * 4 + T * R * 2)
+        return out
+    M = n
+    if bf and K >= 2 and M <= 64:
+        return {
+            # in_proj with the conv window fused: weights, x_t, u and z out, history read + write
+            "decode.in_proj_conv": ("hbm", 2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
+                                    + E * (K + 1) * s),
+            "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
+            # dt_proj with the state step fused: weights, delta, B and C, u and z, g, state read + write
+            "decode.dt_proj_state": ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4
+                                     + E * (N + 2) * 4),
+            "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
+    return {"decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
+            "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
+            "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
+            "decode.dt_proj": ("hbm", E * R * s + M * R * 4 + M * E * s),
+            "decode.state_update": ("hbm", 2 * M * E * N * 4 + 4 * M * E * s + M * 2 * N * 4 + E * (N + 2) * 4),
+            "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mamba2.8b_shard0of2_b8x2048_dec128.traffic.txt")
+def role_of(name):
+    return "prefill.scan" if name.startswith("prefill.scan_") else name
+
+
 ROLE_SOURCE = {"prefill.in_proj": "gemm.hip", "prefill.out_proj": "gemm.hip", "prefill.x_proj": "gemm.hip",
-               "prefill.dt_proj": "gemm.hip", "prefill.dt_round": "gemm.hip", "prefill.conv1d": "conv.hip", "prefill.conv_history": "conv.hip",
-               "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip", "prefill.scan_main": "scan.hip",
-               "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip", "decode.dt_proj_state": "skinny.hip",
-               "decode.out_proj": "skinny.hip", "exchange.reduce_add": "misc.hip"}
-ROLE_SOURCE.update({f"exchange.{op}_{c}": "codec.hip" for op in ("encode", "decode") for c in ("f16", "bf16", "fp8", "int8")})
+               "prefill.dt_proj": "gemm.hip", "prefill.dt_round": "gemm.hip", "prefill.conv1d": "conv.hip",
+               "prefill.conv_history": "conv.hip", "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip",
+               "prefill.scan_main": "scan.hip", "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip",
+               "decode.dt_proj_state": "skinny.hip", "decode.out_proj": "skinny.hip", "decode.in_proj": "gemm.hip",
+               "decode.dt_proj": "skinny.hip", "decode.conv": "conv.hip", "decode.state_update": "scan.hip",
+               "gemm.splitk_reduce": "gemm.hip", "exchange.reduce_add": "misc.hip"}
 
 
 def source_sha(src):
@@ -93,216 +187,493 @@ def source_sha(src):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(role):
-    """HBM bytes per launch of a kernel role from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE summary (already scaled by the copy calibration), or None when there is
-    no entry or the kernel's source has changed since the counters were taken."""
+def profile_counters(stem, kind, role):
+    """Per-launch counter values of a kernel role from a committed rocprofv3 summary
+    (profiles/<stem>.<kind>.txt), or None when there is no entry or the kernel's source has
+    changed since the counters were taken. kind "traffic": HBM bytes already scaled by the
+    copy calibration ({"fetch", "write"}); kind "util": {"valu", "trans"} instructions."""
+    path = os.path.join(ROOT, "profiles", f"{stem}.{kind}.txt")
     src = ROLE_SOURCE.get(role)
-    if src is None or not os.path.exists(TRAFFIC_FILE):
+    if src is None or not os.path.exists(path):
         return None
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             parts = line.split()
             if line.startswith("#") or len(parts) < 5 or parts[0] != role:
                 continue
-            if parts[4] != source_sha(src):
-                return None
-            return {"fetch": float(parts[2]), "write": float(parts[3])}
+            if kind == "traffic":
+                if parts[4] != source_sha(src):
+                    return None
+                return {"fetch": float(parts[2]), "write": float(parts[3])}
+            if kind == "util" and len(parts) >= 9:
+                if parts[8] != source_sha(src):
+                    return None
+                return {"valu": float(parts[6]), "trans": float(parts[7])}
     return None
 
 
-def achieved(roof, amount, avg_ms):
-    if amount is None or avg_ms <= 0:
-        return None
-    per_s = amount / (avg_ms * 1e-3)
-    return per_s / 1e12 if roof == "mfma" else per_s / 1e9
+# ----------------------------------------------------------------- the GPU runner
+class Workload:
+    """One workload on the GPU: every shard's weights (sliced on the device from the
+    full-width upload), cache pools, the summed x_proj output of every phase (from an
+    untimed pass of all shards' stage 1), and shard 0's calls of a step, marshalled once."""
+
+    def __init__(self, B, torch, key, sh, full, phases, S, info, keep_all=False):
+        import numpy as np
+        self.B, self.torch, self.key, self.sh, self.info = B, torch, key, sh, info
+        dev = "cuda"
+        act = B.torch_act(sh.act)
+        P = sh.shard_count
+        E, N, K, W = sh.d_shard, sh.d_state, sh.d_conv, sh.w_dbl
+        full_dev = B.upload_weights(full, sh.act, dev)
+        self.desc = [B.make_desc(sh, r) for r in range(P)]
+        wdev = []
+        for r in range(P):
+            o = B.empty_shard_weights(sh, dev)
+            B.ssm_shard_slice_weights(self.desc[r], full_dev, o)
+            wdev.append(o)
+        del full_dev
+        self.wdev = wdev
+        self.wst = [B.weights_struct(w) for w in wdev]
+        self.conv = [torch.zeros(S, E, K - 1, dtype=act, device=dev) for _ in range(P)]
+        self.ssm = [torch.zeros(S, E, N, dtype=torch.float32, device=dev) for _ in range(P)]
+        maxT = max([len(p["x"]) for p in phases if p["kind"] == "prefill"] + [1])
+        maxS = max([len(p["slots"]) for p in phases if p["kind"] == "prefill"] + [1])
+        maxB = max([len(p["x"]) for p in phases if p["kind"] == "decode"] + [1])
+        self.wsp = [B.workspace(B.prefill_workspace_bytes(self.desc[r], maxT, maxS), dev) for r in range(P)]
+        self.wsd = [B.workspace(B.decode_workspace_bytes(self.desc[r], maxB), dev) for r in range(P)]
+        self.phases = []
+        for p in phases:
+            q = {"kind": p["kind"], "n": len(p["x"]), "x": torch.from_numpy(np.ascontiguousarray(p["x"])).to(dev, act)}
+            if p["kind"] == "prefill":
+                q["meta"] = B.SeqMeta(p["cu"], p["slots"], p["has_init"], S, dev)
+                q["nseq"] = len(p["slots"])
+            else:
+                q["slots"] = torch.from_numpy(np.ascontiguousarray(p["slots"], np.int32)).to(dev)
+                q["nseq"] = len(p["slots"])
+            self.phases.append(q)
+        self.n_prefill_tokens = sum(q["n"] for q in self.phases if q["kind"] == "prefill")
+        self.n_decode_steps = sum(1 for q in self.phases if q["kind"] == "decode")
+        # the exchange, outside every timed step: all shards' stage 1 over the schedule, summed
+        part = torch.empty(maxT, W, dtype=torch.float32, device=dev)
+        for q in self.phases:
+            n = q["n"]
+            q["xdbl"] = torch.zeros(n, W, dtype=torch.float32, device=dev)
+            for r in range(P):
+                if q["kind"] == "prefill":
+                    B.ssm_shard_prefill_stage1(self.desc[r], self.wst[r], q["x"], q["meta"], self.conv[r], part[:n],
+                                               self.wsp[r])
+                else:
+                    B.ssm_shard_decode_stage1(self.desc[r], self.wst[r], q["x"], q["slots"], self.conv[r], part[:n],
+                                              self.wsd[r])
+                B.ssm_reduce_add_f32(q["xdbl"], part[:n])
+        torch.cuda.synchronize()
+        if not keep_all:               # the other shards' work is done
+            self.wsp, self.wsd = self.wsp[:1], self.wsd[:1]
+            self.conv, self.ssm, self.wst, self.desc = self.conv[:1], self.ssm[:1], self.wst[:1], self.desc[:1]
+            self.wdev = self.wdev[:1]
+            torch.cuda.empty_cache()
+        self.y = torch.empty(max(maxT, maxB), sh.d_model, dtype=act, device=dev)
+        self.p0 = torch.empty(max(maxT, maxB), W, dtype=torch.float32, device=dev)
+        self.stream = torch.cuda.current_stream()
+        self.calls = [self._bind(q) for q in self.phases]
+
+    def _bind(self, q, stream=None):
+        B = self.B
+        d, w, n = self.desc[0], self.wst[0], q["n"]
+        one_shard = self.sh.shard_count == 1   # the exchange is the identity: stage 2 reads stage 1's output
+        xin = self.p0[:n] if one_shard else q["xdbl"]
+        if q["kind"] == "prefill":
+            return (B.bind("ssm_shard_prefill_stage1", d, w, q["x"], q["meta"], self.conv[0], self.p0[:n], self.wsp[0],
+                           stream=stream),
+                    B.bind("ssm_shard_prefill_stage2", d, w, xin, q["meta"], self.ssm[0], self.y[:n], self.wsp[0],
+                           stream=stream))
+        return (B.bind("ssm_shard_decode_stage1", d, w, q["x"], q["slots"], self.conv[0], self.p0[:n], self.wsd[0],
+                       stream=stream),
+                B.bind("ssm_shard_decode_stage2", d, w, xin, q["slots"], self.ssm[0], self.y[:n], self.wsd[0],
+                       stream=stream))
+
+    def step(self, evs=None):
+        for i, cs in enumerate(self.calls):
+            if evs is not None:
+                evs[i].record()
+            for c in cs:
+                c()
+        if evs is not None:
+            evs[-1].record()
+
+    def status_ok(self):
+        return self.B.take_status(self.wsp[0]) == 0 and self.B.take_status(self.wsd[0]) == 0
+
+    def work_by_role(self):
+        """role -> (roof, [work of each launch in schedule order]) over one step."""
+        out = {}
+        for q in self.phases:
+            for role, (roof, amt) in kernel_work(self.sh, q["kind"], q["n"], q["nseq"]).items():
+                out.setdefault(role, (roof, []))[1].append(float(amt))
+        return out
 
 
-def run(args):
+def measure(B, torch, wl, steps, warmup, dominant_every=None):
+    """Warm-up steps, one step with every kernel timed (the per-kernel breakdown; the host
+    waits for each phase), then the
+    timed steps with events at every phase boundary and the dominant kernel's dispatches
+    timed by their own events (every launch if it runs 200 us or more, else every 16th)."""
     import numpy as np
-    import torch
-
-    from paper_2602_21144_amd import binding as B
-    from paper_2602_21144_amd import synth
-
-    cfg = synth.CONFIGS["mamba2.8b_tp2"]
-    sh = cfg["shape"]
-    Bsz, L, steps_dec = cfg["batch"], cfg["prefill_len"], cfg["decode_steps"]
-    T = Bsz * L
-    dev = "cuda"
-    torch.cuda.set_device(0)
-    B.lib()
-
-    log("drawing seeded inputs")
-    full = synth.make_layer(sh, cfg["seed"])
-    rng = full["_rng"]
-    x_host = synth.make_tokens(rng, T, sh.d_model, sh.act)
-    xdec_host = np.stack([synth.make_tokens(rng, Bsz, sh.d_model, sh.act) for _ in range(steps_dec)])
-    S = Bsz + 16
-    slots = synth.make_slots(rng, Bsz)
-
-    log("uploading and slicing weights")
-    full_dev = B.upload_weights(full, sh.act, dev)
-    desc = [B.make_desc(sh, r) for r in range(sh.shard_count)]
-    wdev = []
-    for r in range(sh.shard_count):
-        out = B.empty_shard_weights(sh, dev)
-        B.ssm_shard_slice_weights(desc[r], full_dev, out)
-        wdev.append(out)
-    del full_dev
-    wst = [B.weights_struct(w) for w in wdev]
-    act = B.torch_act(sh.act)
-    x = torch.from_numpy(x_host).to(dev, act)
-    xdec = torch.from_numpy(xdec_host).to(dev, act)
-    cu = np.arange(0, T + 1, L, dtype=np.int32)
-    meta = B.SeqMeta(cu, slots, np.zeros(Bsz, np.int32), S, dev)
-    slots_dev = torch.from_numpy(slots).to(dev)
-    E, N, K, W = sh.d_shard, sh.d_state, sh.d_conv, sh.w_dbl
-    conv = [torch.zeros(S, E, K - 1, dtype=act, device=dev) for _ in range(sh.shard_count)]
-    ssm = [torch.zeros(S, E, N, dtype=torch.float32, device=dev) for _ in range(sh.shard_count)]
-    wsp = [B.workspace(B.prefill_workspace_bytes(desc[r], T, Bsz), dev) for r in range(sh.shard_count)]
-    wsd = [B.workspace(B.decode_workspace_bytes(desc[r], Bsz), dev) for r in range(sh.shard_count)]
-    p0 = torch.empty(T, W, dtype=torch.float32, device=dev)
-    q0 = torch.empty(Bsz, W, dtype=torch.float32, device=dev)
-    y = torch.empty(T, sh.d_model, dtype=act, device=dev)
-    yd = torch.empty(Bsz, sh.d_model, dtype=act, device=dev)
-
-    log("x_proj partials of the other shard (the other GPU's work, outside the timed region)")
-    p1_pref = torch.zeros(T, W, dtype=torch.float32, device=dev)
-    p1_dec = torch.zeros(steps_dec, Bsz, W, dtype=torch.float32, device=dev)
-    pr = torch.empty(T, W, dtype=torch.float32, device=dev)
-    qr = torch.empty(Bsz, W, dtype=torch.float32, device=dev)
-    for r in range(1, sh.shard_count):
-        B.ssm_shard_prefill_stage1(desc[r], wst[r], x, meta, conv[r], pr, wsp[r])
-        B.ssm_reduce_add_f32(p1_pref, pr)
-        for k in range(steps_dec):
-            B.ssm_shard_decode_stage1(desc[r], wst[r], xdec[k], slots_dev, conv[r], qr, wsd[r])
-            B.ssm_reduce_add_f32(p1_dec[k], qr)
+    for _ in range(max(warmup, 1)):
+        wl.step()
     torch.cuda.synchronize()
-
-    # the ABI calls of a step, marshalled once (a serving loop issues the same calls on the
-    # same buffers every step)
-    prefill_calls = (B.bind("ssm_shard_prefill_stage1", desc[0], wst[0], x, meta, conv[0], p0, wsp[0]),
-                     B.bind("ssm_reduce_add_f32", p0, p1_pref),
-                     B.bind("ssm_shard_prefill_stage2", desc[0], wst[0], p0, meta, ssm[0], y, wsp[0]))
-    decode_calls = [(B.bind("ssm_shard_decode_stage1", desc[0], wst[0], xdec[k], slots_dev, conv[0], q0, wsd[0]),
-                     B.bind("ssm_reduce_add_f32", q0, p1_dec[k]),
-                     B.bind("ssm_shard_decode_stage2", desc[0], wst[0], q0, slots_dev, ssm[0], yd, wsd[0]))
-                    for k in range(steps_dec)]
-
-    def prefill():
-        for c in prefill_calls:
-            c()
-
-    def decode(k):
-        for c in decode_calls[k]:
-            c()
-
-    def step(evs=None):
-        if evs:
-            evs[0].record()
-        prefill()
-        if evs:
-            evs[1].record()
-        for k in range(steps_dec):
-            decode(k)
-        if evs:
-            evs[2].record()
-
-    log(f"warmup {args.warmup} step(s)")
-    for _ in range(max(args.warmup, 1)):
-        step()
-    torch.cuda.synchronize()
-
-    log("one profiled step (every kernel bracketed by events) for the breakdown")
+    # the breakdown step waits for each phase before issuing the next: a timed dispatch
+    # queued behind running work can read its wait in the queue as part of its duration
     B.ssm_timing_collect()
     B.ssm_timing_enable(True)
-    step()
-    torch.cuda.synchronize()
+    for cs in wl.calls:
+        for c in cs:
+            c()
+        torch.cuda.synchronize()
     B.ssm_timing_enable(False)
     breakdown = B.ssm_timing_collect()
     dominant = max(breakdown, key=lambda n: breakdown[n][1])
-
-    # every TIMING_EVERY-th launch of the dominant kernel is timed by its own dispatch events
-    # (each timed dispatch costs about 5 us more; timing every launch would slow the step)
-    log(f"timed region: {args.steps} step(s); events bracket every {TIMING_EVERY}th launch of {dominant}")
-    B.ssm_timing_enable(True, dominant, every=TIMING_EVERY)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    dom_avg_ms = breakdown[dominant][1] / breakdown[dominant][0]
+    every = dominant_every or (1 if dom_avg_ms >= 0.2 else 16)
+    B.ssm_timing_enable(True, dominant, every=every)
+    nph = len(wl.phases)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
+    for i in range(steps):
+        wl.step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     B.ssm_timing_enable(False)
     dom_launches, dom_ms = B.ssm_timing_collect()[dominant]
-    pre_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    dec_ms = [e[1].elapsed_time(e[2]) for e in evs]
-    step_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
-    assert B.take_status(wsp[0]) == 0 and B.take_status(wsd[0]) == 0
-    log(f"prefill {np.mean(pre_ms):.3f} ms, decode {1e3 * np.mean(dec_ms) / steps_dec:.2f} us/step, "
-        f"step {step_ms:.3f} ms (host wall {1e3 * wall / args.steps:.3f} ms)")
+    assert wl.status_ok(), "a kernel flagged bad metadata"
+    step_ms = [e[0].elapsed_time(e[-1]) for e in evs]
+    pre_ms, dec_ms = [], []
+    for e in evs:
+        ph = [e[j].elapsed_time(e[j + 1]) for j in range(nph)]
+        pre_ms.append(sum(t for t, q in zip(ph, wl.phases) if q["kind"] == "prefill"))
+        dec_ms.append(sum(t for t, q in zip(ph, wl.phases) if q["kind"] == "decode"))
+    # work of the sampled launches of the dominant kernel (its launches are numbered over
+    # the timed steps; every `every`-th is timed, the first included)
+    work = wl.work_by_role()
+    dom_role = role_of(dominant)
+    sampled_work = None
+    if dom_role in work and not dom_role.startswith("prefill.scan"):
+        amts = work[dom_role][1]
+        n = len(amts)
+        sampled_work = sum(amts[j % n] for j in range(0, steps * n, every))
+    return {"breakdown": breakdown, "dominant": dominant, "every": every, "dom_launches": dom_launches,
+            "dom_ms": dom_ms, "sampled_work": sampled_work, "step_ms": float(np.mean(step_ms)),
+            "prefill_ms": float(np.mean(pre_ms)), "decode_ms": float(np.mean(dec_ms)), "wall_s": wall,
+            "work": work}
 
-    kernels = {}
-    for name, (n, ms) in sorted(breakdown.items(), key=lambda kv: -kv[1][1]):
-        roof, amt, unit = algorithmic(name, sh, T, Bsz, Bsz)
-        avg = ms / n
-        a = achieved(roof, amt, avg)
-        peak = PEAK_BF16_TFLOPS if roof == "mfma" else PEAK_HBM_GBS
-        kernels[name] = {"launches": n, "avg_us": round(1e3 * avg, 3), "share_of_step": round(ms / sum(v[1] for v in breakdown.values()), 4),
-                         "bound": roof, "achieved": None if a is None else round(a, 1), "unit": unit,
-                         "frac": None if a is None else round(a / peak, 4)}
-    roof, amt, unit = algorithmic(dominant, sh, T, Bsz, Bsz)
-    dom_avg = dom_ms / dom_launches
-    ach = achieved(roof, amt, dom_avg)
-    peak = PEAK_BF16_TFLOPS if roof == "mfma" else PEAK_HBM_GBS
-    tr = measured_traffic(dominant)
-    roofline = {"kernel": dominant, "bound": roof, "achieved": None if ach is None else round(ach, 2), "peak": peak,
-                "unit": unit, "frac": None if ach is None else round(ach / peak, 4),
-                "traffic": None if tr is None else round(tr["fetch"] + tr["write"]),
-                "traffic_fetch_write": None if tr is None else [round(tr["fetch"]), round(tr["write"])],
-                "avg_us": round(1e3 * dom_avg, 3), "launches_timed": dom_launches, "timed_every": TIMING_EVERY,
-                "algorithmic_per_launch": amt}
 
-    scan_ms = sum(breakdown[k][1] for k in breakdown if k.startswith("prefill.scan"))
-    result = {
-        "metric": METRIC, "value": round(T / (np.mean(pre_ms) * 1e-3), 1), "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "Mamba-2.8B-shaped mixer layer, shard 0 of a 2-way channel split: d_model 2560, "
-                               "d_inner 2560 of 5120, d_state 16, dt_rank 160, d_conv 4; batch 8 x prefill 2048, "
-                               "then 128 decode steps; bf16 activations/weights, fp32 state; seed 1",
-                   "d_model": sh.d_model, "d_inner_shard": sh.d_shard, "d_inner_total": sh.d_inner,
-                   "d_state": sh.d_state, "dt_rank": sh.dt_rank, "d_conv": sh.d_conv, "batch": Bsz,
-                   "prefill_len": L, "decode_steps": steps_dec, "shard": "0 of 2"},
-        "prefill_ms": round(float(np.mean(pre_ms)), 4),
-        "decode_us_per_step": round(float(1e3 * np.mean(dec_ms) / steps_dec), 3),
-        # device time of the kernels alone (stage 1 + stage 2, exchange excluded), from the breakdown step
-        "prefill_kernels_ms": round(sum(v[1] for k, v in breakdown.items() if k.startswith("prefill.")), 4),
-        "decode_kernels_us_per_step": round(1e3 * sum(v[1] for k, v in breakdown.items() if k.startswith("decode."))
-                                            / steps_dec, 3),
-        "scan_tokens_per_s": round(T / (scan_ms * 1e-3), 1) if scan_ms > 0 else None,
-        "roofline": roofline,
-        "kernels": kernels,
-    }
-    if not args.no_codec:
-        log("quantized exchange codecs on this workload's two exchange tensors (outside the timed region)")
-        xa = torch.empty(T, W, dtype=torch.float32, device=dev)
-        B.ssm_shard_prefill_stage1(desc[0], wst[0], x, meta, conv[0], xa, wsp[0])   # shard 0's x_proj partial
-        y1 = torch.empty(T, sh.d_model, dtype=act, device=dev)
-        ssm1 = torch.zeros(S, E, N, dtype=torch.float32, device=dev)
-        B.ssm_shard_prefill_stage2(desc[1], wst[1], p0, meta, ssm1, y1, wsp[1])      # shard 1's out_proj partial
-        result["codec"] = codec_figures(B, torch, {"x_dbl": [xa, p1_pref], "y_partial": [y, y1]})
-    if not args.no_mamba2:
-        log("Mamba-2 (SSD) shard on its workload (outside the timed region)")
-        result["mamba2"] = mamba2_figures(B, torch, args.steps, args.warmup)
-    if not args.no_ablation:
-        log("cache vs no-cache generation through a 64-layer stack (outside the timed region)")
-        result["ablation"] = ablation_figures(B, torch)
-    if not args.no_decode_heavy:
-        log("decode-heavy step: 256 cached sequences on the 2.8B quarter shard (outside the timed region)")
-        result["decode_heavy"] = decode_heavy_figures(B, torch)
-    return result, (sh, full, x_host, xdec_host, slots, S)
+def kernel_figures(wl, m):
+    """Per-kernel (and per-role) figures from the breakdown step: launches, average time,
+    share of the step, roof, achieved rate and fraction of the roof's peak."""
+    sh = wl.sh
+    bd = m["breakdown"]
+    total = sum(v[1] for v in bd.values())
+    mf_peak = PEAK_TFLOPS[sh.act]
+    out = {}
+    for name, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][1]):
+        e = {"launches": n, "avg_us": round(1e3 * ms / n, 3), "share_of_step": round(ms / total, 4)}
+        role = role_of(name)
+        if role in m["work"] and role == name:
+            roof, amts = m["work"][role]
+            amt = sum(amts)
+            rate = amt / (ms * 1e-3)
+            if roof == "mfma":
+                e.update(bound="mfma", achieved=round(rate / 1e12, 2), unit="TFLOP/s", peak=mf_peak,
+                         frac=round(rate / 1e12 / mf_peak, 4))
+            else:
+                e.update(bound="hbm", achieved=round(rate / 1e9, 1), unit="GB/s", peak=PEAK_HBM_GBS,
+                         frac=round(rate / 1e9 / PEAK_HBM_GBS, 4))
+        out[name] = e
+    # the scan's three passes together: the scan's bytes over their summed time, and the
+    # VALU issue rate from the committed counter summary, when it matches the source
+    scan = [k for k in bd if k.startswith("prefill.scan_")]
+    if scan and "prefill.scan" in m["work"]:
+        ms = sum(bd[k][1] for k in scan)
+        launches = bd.get("prefill.scan_main", (1, 0))[0]
+        amt = sum(m["work"]["prefill.scan"][1])
+        gbs = amt / (ms * 1e-3) / 1e9
+        e = {"passes": sorted(scan), "launches": launches, "avg_us": round(1e3 * ms / launches, 3), "bound": "alu",
+             "hbm": {"achieved": round(gbs, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                     "frac": round(gbs / PEAK_HBM_GBS, 4), "bytes_per_launch": amt / launches}}
+        insts = 0.0
+        for k in scan:
+            c = profile_counters(profile_stem(wl.key, wl.sh.act), "util", k)
+            if c is None:
+                insts = None
+                break
+            insts += c["valu"] + c["trans"]     # a transcendental takes two issue slots
+        if insts is not None:
+            rate = insts / (ms * 1e-3 / launches) / 1e9
+            e["valu_issue"] = {"achieved": round(rate, 1), "unit": "G wave-instructions/s",
+                               "peak": PEAK_VALU_GINSTS, "frac": round(rate / PEAK_VALU_GINSTS, 4),
+                               "insts_per_launch": insts}
+        out["prefill.scan (3 passes)"] = e
+    return out
+
+
+def roofline_entry(wl, m):
+    sh = wl.sh
+    dom = m["dominant"]
+    role = role_of(dom)
+    avg_ms = m["dom_ms"] / m["dom_launches"]
+    roof = m["work"].get(role, ("hbm", None))[0]
+    ach = peak = unit = per_launch = None
+    if m["sampled_work"] is not None:
+        rate = m["sampled_work"] / (m["dom_ms"] * 1e-3)
+        per_launch = m["sampled_work"] / m["dom_launches"]
+        if roof == "mfma":
+            ach, peak, unit = rate / 1e12, PEAK_TFLOPS[sh.act], "TFLOP/s"
+        else:
+            ach, peak, unit = rate / 1e9, PEAK_HBM_GBS, "GB/s"
+    tr = profile_counters(profile_stem(wl.key, sh.act), "traffic", dom)
+    return {"kernel": dom, "bound": roof, "achieved": None if ach is None else round(ach, 2), "peak": peak,
+            "unit": unit, "frac": None if ach is None else round(ach / peak, 4),
+            "traffic": None if tr is None else round(tr["fetch"] + tr["write"]),
+            "traffic_fetch_write": None if tr is None else [round(tr["fetch"]), round(tr["write"])],
+            "avg_us": round(1e3 * avg_ms, 3), "launches_timed": m["dom_launches"], "timed_every": m["every"],
+            "algorithmic_per_launch": per_launch,
+            "dtype": sh.act}
+
+
+def summarize(wl, m):
+    steps_dec = wl.n_decode_steps
+    return {"prefill_tokens": wl.n_prefill_tokens, "decode_steps": steps_dec,
+            "ms_per_step": round(m["step_ms"], 4),
+            "tokens_per_s_whole_step": round(wl.n_prefill_tokens / (m["step_ms"] * 1e-3), 1),
+            "prefill_ms": round(m["prefill_ms"], 4),
+            "prefill_tokens_per_s": round(wl.n_prefill_tokens / (m["prefill_ms"] * 1e-3), 1) if m["prefill_ms"] else None,
+            "decode_us_per_step": round(1e3 * m["decode_ms"] / steps_dec, 3) if steps_dec else None}
+
+
+def graph_decode_us(B, torch, wl, reps=3):
+    """The decode steps of a workload captured once in a HIP graph and replayed: device time
+    per step with launch overhead removed (exchange excluded as in the timed steps)."""
+    s = torch.cuda.Stream()
+    dec = [q for q in wl.phases if q["kind"] == "decode"]
+    if not dec:
+        return None
+    calls = [wl._bind(q, stream=s) for q in dec]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for cs in calls:            # warm on the capture stream
+            for c in cs:
+                c()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for cs in calls:
+            for c in cs:
+                c()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    assert wl.status_ok()
+    del g
+    return e0.elapsed_time(e1) * 1e3 / (reps * len(dec))
+
+
+def to_bf16(drawn):
+    """The bf16 form of a workload drawn at float32: the same draws rounded to bf16 (ties
+    to even), which is what the recipe stores for a bf16 workload."""
+    import dataclasses
+
+    from paper_2602_21144_amd import synth
+    sh, full, phases, S, info = drawn
+    act_keys = ("W_in", "conv_w", "conv_b", "W_x", "W_dt", "W_out")
+    full16 = {k: (synth.round_bf16_f32(v) if k in act_keys else v) for k, v in full.items()}
+    ph16 = [{**q, "x": synth.round_bf16_f32(q["x"])} for q in phases]
+    return dataclasses.replace(sh, act="bf16"), full16, ph16, S, info
+
+
+def run_workload(B, torch, key, act, steps, warmup, graph=False, drawn=None, keep_all=False):
+    if drawn is None:
+        log(f"{key} ({act}): drawing seeded host inputs")
+        drawn = draw_workload(key, act)
+    sh, full, phases, S, info = drawn
+    log(f"{key} ({act}): uploading, slicing weights, precomputing the exchange")
+    wl = Workload(B, torch, key, sh, full, phases, S, info, keep_all=keep_all)
+    log(f"{key} ({act}): {warmup} warm-up and {steps} timed step(s) of {len(wl.phases)} phases")
+    m = measure(B, torch, wl, steps, warmup)
+    res = {"workload": WORKLOAD_TEXT[key], "dtype": act, **info, **summarize(wl, m),
+           "roofline": roofline_entry(wl, m), "kernels": kernel_figures(wl, m)}
+    if graph:
+        res["decode_us_per_step_graph"] = round(graph_decode_us(B, torch, wl), 3)
+    log(f"{key} ({act}): {res['ms_per_step']:.3f} ms/step, prefill {res['prefill_tokens_per_s']} tok/s, "
+        f"decode {res['decode_us_per_step']} us/step")
+    return res, wl, m
+
+
+# ------------------------------------------------------------------- CPU baseline
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(drawn, n_chunks=4, n_decode=4):
+    """The oracle (float64 numpy, untuned) on a bounded sample of the headline workload:
+    shard 0's stage 1 + stage 2 over the first prefill chunks of the schedule (the other
+    shard's x_proj partials precomputed, as on the GPU) and decode steps of 64 sequences;
+    then the smallest workload on one core."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import mixer as om
+    sh, full, phases, S, info = drawn
+    act = sh.act
+    w64 = {k: np.asarray(v, np.float64) for k, v in full.items()}
+    shards = [om.shard_weights(w64, r, sh.shard_count) for r in range(sh.shard_count)]
+    E, N, K = sh.d_shard, sh.d_state, sh.d_conv
+    conv = [np.zeros((S, E, K - 1)) for _ in shards]
+    ssm0 = np.zeros((S, E, N))
+    pre = [q for q in phases if q["kind"] == "prefill"][:n_chunks]
+    t_pre, tokens = 0.0, 0
+    for q in pre:
+        x = q["x"].astype(np.float64)
+        others = []
+        for r in range(1, len(shards)):
+            o = om.prefill_stage1(shards[r], x, q["cu"], q["slots"], q["has_init"], conv[r], sh.act)
+            conv[r] = o["conv_pool"]
+            others.append(o["x_dbl"])
+        t0 = time.perf_counter()
+        s1 = om.prefill_stage1(shards[0], x, q["cu"], q["slots"], q["has_init"], conv[0], sh.act)
+        red = s1["x_dbl"] + sum(others)
+        s2 = om.prefill_stage2(shards[0], s1, red, q["cu"], q["slots"], q["has_init"], ssm0, sh.act)
+        t_pre += time.perf_counter() - t0
+        conv[0], ssm0 = s1["conv_pool"], s2["ssm_pool"]
+        tokens += len(x)
+    rng = np.random.default_rng(0)
+    Bd = 64
+    slots = np.arange(Bd)
+    cp = [rng.normal(size=(Bd, E, K - 1)) for _ in shards]
+    sp = rng.normal(size=(Bd, E, N)) * 0.5
+    t_dec = 0.0
+    for _ in range(n_decode):
+        xt = rng.normal(size=(Bd, sh.d_model))
+        others = []
+        for r in range(1, len(shards)):
+            o = om.decode_stage1(shards[r], xt, slots, cp[r], sh.act)
+            cp[r] = o["conv_pool"]
+            others.append(o["x_dbl"])
+        t0 = time.perf_counter()
+        d1 = om.decode_stage1(shards[0], xt, slots, cp[0], sh.act)
+        d2 = om.decode_stage2(shards[0], d1, d1["x_dbl"] + sum(others), slots, sp, sh.act)
+        t_dec += time.perf_counter() - t0
+        cp[0], sp = d1["conv_pool"], d2["ssm_pool"]
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    # the smallest workload (Mamba-130m shape, full width, fp32) on one core
+    sh0, full0, ph0, S0, _ = draw_workload("c0")
+    w0 = {k: np.asarray(v, np.float64) for k, v in full0.items()}
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        q = ph0[0]
+        E0, K0, N0 = sh0.d_shard, sh0.d_conv, sh0.d_state
+        st = om.prefill(w0, q["x"].astype(np.float64), q["cu"], q["slots"], q["has_init"],
+                        np.zeros((S0, E0, K0 - 1)), np.zeros((S0, E0, N0)), sh0.act)
+        t_c0_pre = time.perf_counter() - t0
+        cpool, spool = st["conv_pool"], st["ssm_pool"]
+        t0 = time.perf_counter()
+        for q in ph0[1:]:
+            d = om.decode_step(w0, q["x"].astype(np.float64), q["slots"], cpool, spool, sh0.act)
+            cpool, spool = d["conv_pool"], d["ssm_pool"]
+        t_c0_dec = time.perf_counter() - t0
+    return {"value": round(tokens / t_pre, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"the first {len(pre)} prefill chunks of the headline schedule ({tokens} tokens, "
+                      f"{sum(len(q['slots']) for q in pre)} sequence pieces) through shard 0's stage 1 + stage 2 "
+                      f"in {act}, and {n_decode} decode steps of {Bd} sequences; float64 numpy, untuned; the other "
+                      f"shard's x_proj partials are precomputed inputs, as on the GPU",
+            "decode_us_per_step": round(1e6 * t_dec / n_decode, 1), "prefill_s": round(t_pre, 2),
+            "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
+            "c0_one_core": {"workload": WORKLOAD_TEXT["c0"], "cores": 1,
+                            "prefill_tokens_per_s": round(256 / t_c0_pre, 1),
+                            "decode_us_per_step": round(1e6 * t_c0_dec / 16, 1)}}
+
+
+# ------------------------------------------------------ the NEXT-row figures (extras)
+def decode_beyond_mall(B, torch, groups=16):
+    """The 2.8B quarter shard's decode step with states that cannot stay in the 256 MB MALL:
+    16 groups of 256 sequences in a 4112-slot pool (337 MB of states), each step serving
+    the next group, so every step's states come from HBM. Weights, states and inputs are
+    seeded device draws (the timing does not depend on their values)."""
+    import math
+    import numpy as np
+    from paper_2602_21144_amd import synth
+    cfg = synth.CONFIGS["mamba2.8b_tp4_decode"]
+    sh, Bd = cfg["shape"], cfg["batch"]
+    E, dm, N, R, K, W = sh.d_shard, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv, sh.w_dbl
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(cfg["seed"])
+
+    def nrm(*size, std=0.02):
+        return (torch.randn(*size, generator=g, device=dev) * std).to(torch.bfloat16)
+    lo, hi = math.log(1e-3), math.log(0.1)
+    dt0 = torch.exp(torch.rand(E, generator=g, device=dev) * (hi - lo) + lo)
+    w = {"W_in": nrm(2 * E, dm), "conv_w": nrm(E, K), "conv_b": nrm(E), "W_x": nrm(W, E), "W_dt": nrm(E, R),
+         "W_out": nrm(dm, E), "b_dt": (dt0 + torch.log(-torch.expm1(-dt0))).float(),
+         "A_log": torch.log(torch.arange(1, N + 1, device=dev, dtype=torch.float32)).repeat(E, 1).contiguous(),
+         "D": torch.ones(E, device=dev)}
+    ws_ = B.weights_struct(w)
+    d = B.make_desc(sh, 0)
+    S2 = groups * Bd + 16
+    perm = torch.from_numpy(np.random.default_rng(cfg["seed"] + 1).permutation(Bd).astype(np.int32)).to(dev)
+    gslots = [perm + gi * Bd for gi in range(groups)]
+    conv2 = nrm(S2, E, K - 1, std=1.0)
+    ssm2 = torch.randn(S2, E, N, generator=g, device=dev) * 0.5
+    wsd = B.workspace(B.decode_workspace_bytes(d, Bd), dev)
+    steps = 64
+    xs = [nrm(Bd, dm, std=1.0) for _ in range(steps)]
+    q0 = torch.empty(Bd, W, dtype=torch.float32, device=dev)
+    xr = torch.randn(Bd, W, generator=g, device=dev) * 0.1
+    y = torch.empty(Bd, dm, dtype=torch.bfloat16, device=dev)
+    calls = [(B.bind("ssm_shard_decode_stage1", d, ws_, xs[k], gslots[k % groups], conv2, q0, wsd),
+              B.bind("ssm_shard_decode_stage2", d, ws_, xr, gslots[k % groups], ssm2, y, wsd)) for k in range(steps)]
+
+    def run():
+        for cs in calls:
+            for c in cs:
+                c()
+    run()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    run()
+    ev[1].record()
+    torch.cuda.synchronize()
+    step_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
+    B.ssm_timing_collect()
+    B.ssm_timing_enable(True, "decode.state_update")
+    run()
+    torch.cuda.synchronize()
+    B.ssm_timing_enable(False)
+    bd = B.ssm_timing_collect()
+    assert B.take_status(wsd) == 0
+    st = bd.get("decode.state_update", (1, float("nan")))
+    st_us = 1e3 * st[1] / st[0]
+    state_bytes = 2 * Bd * E * N * 4 + 4 * Bd * E * 2 + Bd * 2 * N * 4 + E * (N + 2) * 4
+    return {"workload": "the decode-heavy step (2.8B quarter shard, 256 sequences) over 16 groups of 256 sequences "
+                        "in a 4112-slot pool (337 MB of states), each step serving the next group",
+            "state_pool_bytes": S2 * E * N * 4, "decode_us_per_step": round(step_us, 3),
+            "state_kernel_avg_us": round(st_us, 3), "state_kernel_GBps": round(state_bytes / (st_us * 1e-6) / 1e9, 1),
+            "state_kernel_frac_hbm": round(state_bytes / (st_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def mamba2_figures(B, torch, steps, warmup):
@@ -344,16 +715,22 @@ def mamba2_figures(B, torch, steps, warmup):
     q1 = torch.zeros(nd, Bsz, G, dtype=torch.float32, device=dev)
     y = torch.empty(T, sh.d_model, dtype=torch.bfloat16, device=dev)
     yd = torch.empty(Bsz, sh.d_model, dtype=torch.bfloat16, device=dev)
-    # the other shard's partial sums of squares (its GPU's work), outside the timed region
-    B.ssm2_shard_prefill_stage1(desc[1], w[1], x, meta, conv[1], ssm[1], ss1, wsp[1])
+    # the exchange of the sums of squares, outside the timed region: both shards' stage 1
+    # over the step, the partial sums added; the timed steps run shard 0's stage 1 and then
+    # stage 2 on the summed values
+    ssum = torch.zeros(T, G, dtype=torch.float32, device=dev)
+    qsum = torch.zeros(nd, Bsz, G, dtype=torch.float32, device=dev)
+    for r, part in ((0, ss0), (1, ss1)):
+        B.ssm2_shard_prefill_stage1(desc[r], w[r], x, meta, conv[r], ssm[r], part, wsp[r])
+        B.ssm_reduce_add_f32(ssum, part)
     for k in range(nd):
-        B.ssm2_shard_decode_stage1(desc[1], w[1], xdec[k], sl, conv[1], ssm[1], q1[k], wsd[1])
+        for r, part in ((0, q0), (1, q1[k])):
+            B.ssm2_shard_decode_stage1(desc[r], w[r], xdec[k], sl, conv[r], ssm[r], part, wsd[r])
+            B.ssm_reduce_add_f32(qsum[k], part)
     pre = (B.bind("ssm2_shard_prefill_stage1", desc[0], w[0], x, meta, conv[0], ssm[0], ss0, wsp[0]),
-           B.bind("ssm_reduce_add_f32", ss0, ss1),
-           B.bind("ssm2_shard_prefill_stage2", desc[0], w[0], ss0, T, y, wsp[0]))
+           B.bind("ssm2_shard_prefill_stage2", desc[0], w[0], ssum, T, y, wsp[0]))
     dec = [(B.bind("ssm2_shard_decode_stage1", desc[0], w[0], xdec[k], sl, conv[0], ssm[0], q0, wsd[0]),
-            B.bind("ssm_reduce_add_f32", q0, q1[k]),
-            B.bind("ssm2_shard_decode_stage2", desc[0], w[0], q0, Bsz, yd, wsd[0])) for k in range(nd)]
+            B.bind("ssm2_shard_decode_stage2", desc[0], w[0], qsum[k], Bsz, yd, wsd[0])) for k in range(nd)]
 
     def step(evs=None):
         if evs:
@@ -394,133 +771,13 @@ def mamba2_figures(B, torch, steps, warmup):
     main_s = main[1] / main[0] * 1e-3
     return {"workload": "Mamba-2 2.7B-shaped mixer layer, shard 0 of a 2-way head split: d_model 2560, 40 of 80 "
                         "heads of 64, d_state 128, one B/C group (replicated), d_conv 4; batch 8 x prefill 2048, "
-                        "then 128 decode steps; bf16 activations, fp32 state; seed 11",
+                        "then 128 decode steps; bf16 activations, fp32 state; seed 11; the sum-of-squares exchange "
+                        "excluded",
             "prefill_ms": round(pre_ms, 4), "prefill_tokens_per_s": round(T / (pre_ms * 1e-3), 1),
             "decode_us_per_step": round(dec_us, 3),
             "ssd_main": {"avg_us": round(main_s * 1e6, 3), "TFLOP_per_s": round(flops / main_s / 1e12, 1),
                          "GB_per_s": round(nbytes / main_s / 1e9, 1), "flops": flops, "bytes": nbytes},
             "kernels": kernels}
-
-
-def decode_heavy_figures(B, torch, steps=64):
-    """Decode-heavy serving step on the Mamba-2.8B quarter shard (1280 of 5120 channels,
-    d_model 2560): 256 sequences holding cached states, one single-token step each. Above
-    64 sequences the step runs tiled projections, the conv-step kernel and the state-step
-    kernel, whose traffic is the state cache (read and written once: 2 B E N 4 bytes).
-    Weights are drawn on the GPU with the one-layer recipe; the cache pools hold seeded
-    random values (the timing does not depend on them); the other shards' x_proj partial
-    (their GPUs' work) is precomputed, as in the headline step.
-
-    The 256 sequences' states (21 MB) stay in the 256 MB MALL from step to step, so the
-    state kernel's rate is also measured with 16 groups of 256 sequences in a 4112-slot
-    pool (337 MB of states), each step serving the next group: every step's states then
-    come from HBM ("state_beyond_mall")."""
-    import math
-    import numpy as np
-    from paper_2602_21144_amd import synth
-    cfg = synth.CONFIGS["mamba2.8b_tp4_decode"]
-    sh, Bd = cfg["shape"], cfg["batch"]
-    E, dm, N, R, K, W = sh.d_shard, sh.d_model, sh.d_state, sh.dt_rank, sh.d_conv, sh.w_dbl
-    dev = "cuda"
-    g = torch.Generator(device=dev)
-    g.manual_seed(cfg["seed"])
-
-    def nrm(*size, std=0.02):
-        return (torch.randn(*size, generator=g, device=dev) * std).to(torch.bfloat16)
-
-    lo, hi = math.log(1e-3), math.log(0.1)
-    dt0 = torch.exp(torch.rand(E, generator=g, device=dev) * (hi - lo) + lo)
-    w = {"W_in": nrm(2 * E, dm), "conv_w": nrm(E, K), "conv_b": nrm(E), "W_x": nrm(W, E), "W_dt": nrm(E, R),
-         "W_out": nrm(dm, E), "b_dt": (dt0 + torch.log(-torch.expm1(-dt0))).float(),
-         "A_log": torch.log(torch.arange(1, N + 1, device=dev, dtype=torch.float32)).repeat(E, 1).contiguous(),
-         "D": torch.ones(E, device=dev)}
-    ws_ = B.weights_struct(w)
-    d = B.make_desc(sh, 0)
-    S = Bd + 16
-    slots = torch.from_numpy(synth.make_slots(np.random.default_rng(cfg["seed"]), Bd)).to(dev)
-    conv = nrm(S, E, K - 1, std=1.0)
-    ssm = torch.randn(S, E, N, generator=g, device=dev) * 0.5
-    wsd = B.workspace(B.decode_workspace_bytes(d, Bd), dev)
-    xs = [nrm(Bd, dm, std=1.0) for _ in range(steps)]
-    q0 = torch.empty(Bd, W, dtype=torch.float32, device=dev)
-    other = torch.randn(Bd, W, generator=g, device=dev) * 0.1
-    y = torch.empty(Bd, dm, dtype=torch.bfloat16, device=dev)
-    calls = [(B.bind("ssm_shard_decode_stage1", d, ws_, xs[k], slots, conv, q0, wsd),
-              B.bind("ssm_reduce_add_f32", q0, other),
-              B.bind("ssm_shard_decode_stage2", d, ws_, q0, slots, ssm, y, wsd)) for k in range(steps)]
-
-    def run():
-        for cs in calls:
-            for c in cs:
-                c()
-    run()
-    torch.cuda.synchronize()
-    B.ssm_timing_collect()
-    B.ssm_timing_enable(True)
-    run()
-    torch.cuda.synchronize()
-    B.ssm_timing_enable(False)
-    bd = B.ssm_timing_collect()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ev[0].record()
-    run()
-    ev[1].record()
-    torch.cuda.synchronize()
-    assert B.take_status(wsd) == 0
-    step_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
-
-    # the same steps over 16 groups of sequences whose states together exceed the MALL
-    groups = 16
-    S2 = groups * Bd + 16
-    perm = torch.from_numpy(np.random.default_rng(cfg["seed"] + 1).permutation(Bd).astype(np.int32)).to(dev)
-    gslots = [perm + gi * Bd for gi in range(groups)]
-    conv2 = nrm(S2, E, K - 1, std=1.0)
-    ssm2 = torch.randn(S2, E, N, generator=g, device=dev) * 0.5
-    calls2 = [(B.bind("ssm_shard_decode_stage1", d, ws_, xs[k], gslots[k % groups], conv2, q0, wsd),
-               B.bind("ssm_reduce_add_f32", q0, other),
-               B.bind("ssm_shard_decode_stage2", d, ws_, q0, gslots[k % groups], ssm2, y, wsd)) for k in range(steps)]
-
-    def run2():
-        for cs in calls2:
-            for c in cs:
-                c()
-    run2()
-    torch.cuda.synchronize()
-    ev[0].record()
-    run2()
-    ev[1].record()
-    torch.cuda.synchronize()
-    step2_us = ev[0].elapsed_time(ev[1]) * 1e3 / steps
-    B.ssm_timing_collect()
-    B.ssm_timing_enable(True, "decode.state_update")
-    run2()
-    torch.cuda.synchronize()
-    B.ssm_timing_enable(False)
-    bd2 = B.ssm_timing_collect()
-    assert B.take_status(wsd) == 0
-    del conv2, ssm2
-    state_bytes = 2 * Bd * E * N * 4 + 4 * Bd * E * 2 + Bd * 2 * N * 4 + E * (N + 2) * 4
-    weight_bytes = (2 * E * dm + W * E + E * R + dm * E) * 2
-    step_bytes = weight_bytes + state_bytes + 2 * Bd * E * (K - 1) * 2 + Bd * (dm + 2 * E + W * 4 + dm) * 2
-    st = bd.get("decode.state_update", (1, float("nan")))
-    st_us = 1e3 * st[1] / st[0]
-    st2 = bd2.get("decode.state_update", (1, float("nan")))
-    st2_us = 1e3 * st2[1] / st2[0]
-    return {"workload": "Mamba-2.8B-shaped layer, shard 0 of a 4-way channel split (d_model 2560, 1280 of 5120 "
-                        "channels, d_state 16, dt_rank 160, d_conv 4): 256 sequences with cached states, one "
-                        "single-token decode step each; bf16, fp32 state; seed 3",
-            "decode_us_per_step": round(step_us, 3),
-            "step_bytes": step_bytes, "step_GBps": round(step_bytes / (step_us * 1e-6) / 1e9, 1),
-            "step_frac_hbm": round(step_bytes / (step_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
-            "state_kernel": {"avg_us": round(st_us, 3), "bytes": state_bytes,
-                             "GBps": round(state_bytes / (st_us * 1e-6) / 1e9, 1),
-                             "frac_hbm": round(state_bytes / (st_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
-            "state_beyond_mall": {"pool_slots": S2, "state_pool_bytes": S2 * E * N * 4,
-                                  "decode_us_per_step": round(step2_us, 3), "state_kernel_avg_us": round(st2_us, 3),
-                                  "GBps": round(state_bytes / (st2_us * 1e-6) / 1e9, 1),
-                                  "frac_hbm": round(state_bytes / (st2_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
-            "kernels": {k: {"launches": n, "avg_us": round(1e3 * ms / n, 3)}
-                        for k, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][1])}}
 
 
 def device_stack_weights(torch, sh, n_layers, seed, dev):
@@ -553,7 +810,6 @@ def ablation_figures(B, torch, n_layers=64, prompt=256, generated=256):
     full width, batch 1, with the SSM cache (prefill of the prompt, then one decode step per
     token) and without it (the prompt, then a prefill of the whole prefix for every token).
     Inputs are seeded synthetic rows, not fed back (one stack, no LM head)."""
-    import numpy as np
     from paper_2602_21144_amd import synth
     dev = "cuda"
     sh = synth.LayerShape(2560, 5120, 16, 160, 4, 1, "bf16")
@@ -662,91 +918,126 @@ def codec_figures(B, torch, tensors):
     return out
 
 
-def cpu_baseline(ctx):
-    """The oracle (float64 numpy, untuned) on a bounded sample of the same workload."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
-
-    from oracle import mixer as om
-
-    sh, full, x_host, xdec_host, slots, S = ctx
-    w64 = {k: np.asarray(v, np.float64) for k, v in full.items() if not k.startswith("_")}
-    shards = [om.shard_weights(w64, r, sh.shard_count) for r in range(sh.shard_count)]
-    E, N, K = sh.d_shard, sh.d_state, sh.d_conv
-    nb = len(slots)
-    L = x_host.shape[0] // nb
-    cu = np.arange(0, nb * L + 1, L)
-    sl = np.arange(nb)
-    zc = np.zeros((nb, E, K - 1))
-    zs = np.zeros((nb, E, N))
-    xs = x_host.astype(np.float64)
-    # the other rank's x_proj partials are inputs here, as on the GPU (not timed)
-    o1 = om.prefill_stage1(shards[1], xs, cu, sl, np.zeros(nb), zc, sh.act)
-    t0 = time.perf_counter()
-    s1 = om.prefill_stage1(shards[0], xs, cu, sl, np.zeros(nb), zc, sh.act)
-    s2 = om.prefill_stage2(shards[0], s1, s1["x_dbl"] + o1["x_dbl"], cu, sl, np.zeros(nb), zs, sh.act)
-    t_pre = time.perf_counter() - t0
-    cp, sp, cp1 = s1["conv_pool"], s2["ssm_pool"], o1["conv_pool"]
-    nsteps = xdec_host.shape[0]
-    t_dec = 0.0
-    for k in range(nsteps):
-        xd = xdec_host[k].astype(np.float64)
-        d1o = om.decode_stage1(shards[1], xd, sl, cp1, sh.act)
-        cp1 = d1o["conv_pool"]
-        t0 = time.perf_counter()
-        d1 = om.decode_stage1(shards[0], xd, sl, cp, sh.act)
-        d2 = om.decode_stage2(shards[0], d1, d1["x_dbl"] + d1o["x_dbl"], sl, sp, sh.act)
-        t_dec += time.perf_counter() - t0
-        cp, sp = d1["conv_pool"], d2["ssm_pool"]
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": round(nb * L / t_pre, 2), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"the whole step on the host: shard 0 prefill of {nb} x {L} tokens (stage 1 + stage 2, "
-                      f"float64 numpy, untuned) and {nsteps} decode steps of {nb} sequences; the other shard's "
-                      f"x_proj partials are precomputed inputs, as on the GPU",
-            "decode_us_per_step": round(1e6 * t_dec / nsteps, 1), "prefill_s": round(t_pre, 2),
-            "host_cpus": len(os.sched_getaffinity(0))}
+def codec_on_c1(B, torch, wl):
+    """The codecs on the 2.8B half shard's two exchange tensors of its prefill: both shards'
+    x_proj partials and both shards' out_proj partials."""
+    q = wl.phases[0]
+    n = q["n"]
+    act = B.torch_act(wl.sh.act)
+    p = [torch.empty(n, wl.sh.w_dbl, dtype=torch.float32, device="cuda") for _ in range(2)]
+    y = [torch.empty(n, wl.sh.d_model, dtype=act, device="cuda") for _ in range(2)]
+    for r in range(2):
+        B.ssm_shard_prefill_stage1(wl.desc[r], wl.wst[r], q["x"], q["meta"], wl.conv[r], p[r], wl.wsp[r])
+    for r in range(2):
+        B.ssm_shard_prefill_stage2(wl.desc[r], wl.wst[r], q["xdbl"], q["meta"], wl.ssm[r], y[r], wl.wsp[r])
+    return codec_figures(B, torch, {"x_dbl": p, "y_partial": y})
 
 
+# ------------------------------------------------------------------------- main
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", choices=sorted(CONFIG_KEYS), default="c4",
+                    help="workload of the headline line (default c4, the largest)")
+    ap.add_argument("--dtype", choices=["f32", "bf16"], default=None,
+                    help="arithmetic of the headline run (default: f32 for c4, the paper's default precision; "
+                         "the workload's own dtype otherwise)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the headline workload (profiling runs): no other workloads, no NEXT-row figures")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
-    ap.add_argument("--no-codec", action="store_true", help="skip the quantized-exchange codec figures")
-    ap.add_argument("--no-mamba2", action="store_true", help="skip the Mamba-2 (SSD) shard figures")
-    ap.add_argument("--no-ablation", action="store_true", help="skip the cache vs no-cache generation figures")
-    ap.add_argument("--no-decode-heavy", action="store_true", help="skip the 256-sequence decode step figures")
-    ap.add_argument("--mamba2-only", action="store_true",
-                    help="print only the Mamba-2 (SSD) shard figures (its own kernel profile; the headline step "
-                         "shares kernel names with it)")
+    ap.add_argument("--no-next", action="store_true", help="skip the codec, Mamba-2 and ablation figures")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
                          "to scale hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported (this build runs on one GPU)",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU's shard; --gpus {args.gpus} is not supported: this build runs on one GPU, "
+              f"and the cross-GPU exchanges are outside it", file=sys.stderr)
         sys.exit(2)
-    if args.mamba2_only:
-        import torch
-        from paper_2602_21144_amd import binding as B
-        B.lib()
-        torch.cuda.set_device(0)
-        print(json.dumps({"mamba2": mamba2_figures(B, torch, args.steps, args.warmup)}), flush=True)
-        return
-    result, ctx = run(args)
+    import torch
+
+    from paper_2602_21144_amd import binding as B
+    from paper_2602_21144_amd import synth
+    torch.cuda.set_device(0)
+    B.lib()
+    key = args.config
+    act = args.dtype or ("f32" if key == "c4" else synth.CONFIGS[CONFIG_KEYS[key]]["shape"].act)
+    log(f"{key} ({act}): drawing seeded host inputs")
+    drawn = draw_workload(key, "f32" if key == "c4" else act)
+    if act == "bf16" and drawn[0].act == "f32":
+        drawn = to_bf16(drawn)
+    head, wl, m = run_workload(B, torch, key, act, args.steps, args.warmup, graph=(key in ("c1", "c3")),
+                               drawn=drawn)
     if args.copy_calibration:
-        import torch
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
+        del src, dst
         log("copied 1 GiB for counter calibration")
+    sh = wl.sh
+    result = {
+        "metric": METRIC, "value": head["tokens_per_s_whole_step"], "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": act, "data": "synthetic",
+        "config": {"workload": head["workload"] + f"; {act} activations, weights and state"
+                   + ("" if act == "f32" else " (fp32 state)"), "key": key,
+                   "d_model": sh.d_model, "d_inner_shard": sh.d_shard, "d_inner_total": sh.d_inner,
+                   "d_state": sh.d_state, "dt_rank": sh.dt_rank, "d_conv": sh.d_conv,
+                   "shard": f"0 of {sh.shard_count}", **wl.info},
+        "value_is": "prefill tokens of the whole step (schedule) per second of the step, the interleaved decode "
+                    "steps included; the x_proj exchange excluded",
+        "prefill_tokens": head["prefill_tokens"], "decode_steps": head["decode_steps"],
+        "prefill_ms": head["prefill_ms"], "prefill_tokens_per_s": head["prefill_tokens_per_s"],
+        "decode_us_per_step": head["decode_us_per_step"],
+        "roofline": head["roofline"], "kernels": head["kernels"],
+    }
+    if "decode_us_per_step_graph" in head:
+        result["decode_us_per_step_graph"] = head["decode_us_per_step_graph"]
+    del wl, m
+    torch.cuda.empty_cache()
+    sample = None
     if not args.no_cpu_baseline:
+        # the oracle's sample: the first chunks of the headline schedule (kept before the
+        # large arrays are dropped)
+        sh_, full_, phases_, S_, info_ = drawn
+        pre = [q for q in phases_ if q["kind"] == "prefill"][:4]
+        sample = (sh_, full_, pre, S_, info_)
+    if not args.no_extras:
+        others = {}
+        if key == "c4" and act == "f32":
+            r, w2, _ = run_workload(B, torch, "c4", "bf16", max(1, min(args.steps, 3)), 1, drawn=to_bf16(drawn))
+            others["c4_bf16"] = r
+            del w2
+            torch.cuda.empty_cache()
+        drawn = None
+        for k in ("c0", "c1", "c2", "c3", "c4"):
+            if k == key:
+                continue
+            a = synth.CONFIGS[CONFIG_KEYS[k]]["shape"].act
+            r, w2, _ = run_workload(B, torch, k, a, max(1, min(args.steps, 3)), 1, graph=(k in ("c1", "c3")),
+                                    keep_all=(k == "c1"))
+            if k == "c1" and not args.no_next:
+                log("quantized exchange codecs on the 2.8B half shard's exchange tensors")
+                result["codec"] = codec_on_c1(B, torch, w2)
+            others[k] = r
+            del w2
+            torch.cuda.empty_cache()
+        result["workloads"] = others
+        log("decode-heavy step with states beyond the MALL")
+        result["decode_beyond_mall"] = decode_beyond_mall(B, torch)
+        if not args.no_next:
+            log("Mamba-2 (SSD) shard")
+            result["mamba2"] = mamba2_figures(B, torch, max(1, min(args.steps, 3)), 1)
+            log("cache vs no-cache generation through a 64-layer stack")
+            result["ablation"] = ablation_figures(B, torch)
+    drawn = None
+    if sample is not None:
         log("CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(ctx)
+        result["cpu_baseline"] = cpu_baseline(sample)
     print(json.dumps(result), flush=True)
 
 

@@ -30,7 +30,7 @@ import numpy as np
 
 __all__ = [
     "LayerShape", "CONFIGS", "round_bf16_f32", "make_layer", "make_general_layer", "make_tokens",
-    "packed_schedule", "make_slots", "tiny_shape",
+    "packed_schedule", "serving_schedule", "make_slots", "tiny_shape",
 ]
 
 
@@ -85,12 +85,19 @@ def tiny_shape(shard_count: int = 1, act: str = "f32", d_state: int = 4) -> Laye
 def round_bf16_f32(a: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bf16 (ties to even); returns float32 holding them."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16) << 16
-    out = r.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    # add 0x7FFF plus the lowest kept bit, then clear the 16 dropped bits; finite values
+    # never carry out of 32 bits (the largest finite float rounds to infinity's pattern)
+    r = (u >> 16) & 1
+    r += 0x7FFF
+    r += u
+    r &= 0xFFFF0000
+    out = r.view(np.float32)
     # NaN stays NaN (not produced by the draws; kept for completeness)
-    return np.where(np.isnan(a), a, out).astype(np.float32)
+    nan = np.isnan(a)
+    if nan.any():
+        out[nan] = a[nan]
+    return out
 
 
 def _store(a: np.ndarray, act: str) -> np.ndarray:
@@ -278,3 +285,35 @@ def make_mamba2_layer(shape: Mamba2Shape, seed: int, stress: bool = False,
         "D": np.zeros(H, np.float32) if stress else np.ones(H, np.float32),
         "norm_w": np.ones(E, np.float32), "W_out": _store(W_out, act), "_rng": g,
     }
+
+
+def serving_schedule(lengths: List[int], chunk: int, decode_steps: int) -> List[tuple]:
+    """The chunked serving schedule of a mixed batch: prompts concatenated in index order
+    and prefilled in windows of ``chunk`` packed tokens (``packed_schedule``); after each
+    window, one decode step for every sequence whose prompt is complete and that has fewer
+    than ``decode_steps`` decode tokens; after the last window, decode steps until every
+    sequence has ``decode_steps``.
+
+    Returns a list of ("prefill", window) and ("decode", [(sequence, k), ...]) entries, k
+    being that sequence's decode index (which decode input it consumes).
+    """
+    ndec = [0] * len(lengths)
+    ready: List[int] = []
+    out: List[tuple] = []
+
+    def decode_round():
+        batch = [(i, ndec[i]) for i in ready if ndec[i] < decode_steps]
+        if batch:
+            out.append(("decode", batch))
+            for i, _ in batch:
+                ndec[i] += 1
+
+    for w in packed_schedule(lengths, chunk):
+        out.append(("prefill", w))
+        for p in w["pieces"]:
+            if p[1] + p[2] == lengths[p[0]]:
+                ready.append(p[0])
+        decode_round()
+    while any(n < decode_steps for n in ndec):
+        decode_round()
+    return out

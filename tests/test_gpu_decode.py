@@ -35,14 +35,17 @@ def test_decode_batches_across_tile_limit(batch, init):
 
 
 # wide shards: 17..64 sequences take the 32-column fragment kernel for in_proj, with the
-# conv window in its epilogue (3072 channels per shard: 6144 columns). Baseline init: with
-# the stress init at this width some channel's dt lands next to a bf16 rounding boundary
-# where fp32 and fp64 sums round apart, and the state error of that channel (one bf16 step
-# of Delta through a strong decay, 4.8e-3 of the largest state at 40 sequences with either
-# in_proj kernel) exceeds the one-step bound the state tolerance is built on.
+# conv window in its epilogue (3072 channels per shard: 6144 columns). Under the stress init
+# dt reaches a few units, and where the GPU's fp32 sum and the oracle's fp64 sum of a dt
+# round to neighbouring bf16 values, one bf16 step of dt (2^-7 |dt|) moves that channel's
+# state by up to about 2.4 * 2^-7 * sigmoid(v) |dt| / softplus(v) of the largest state
+# (v = dt + b_dt): 4.8e-3 measured at 40 sequences. The state is then held to the bf16
+# tolerance of the outputs, 2e-2.
 @pytest.mark.parametrize("batch", [17, 40, 64])
-def test_decode_wide_shard_batches(batch):
-    _decode_batch_case(synth.LayerShape(256, 6144, 16, 32, 4, 2, "bf16"), batch, "baseline", 12)
+@pytest.mark.parametrize("init", ["baseline", "stress"])
+def test_decode_wide_shard_batches(batch, init):
+    _decode_batch_case(synth.LayerShape(256, 6144, 16, 32, 4, 2, "bf16"), batch, init, 12,
+                       state_tol=TOL["bf16"] if init == "stress" else None)
 
 
 # fp32 activations and weights: at most 8 rows on the one-row-per-wave fp32 kernel, more
@@ -52,7 +55,7 @@ def test_decode_f32_batches(batch):
     _decode_batch_case(synth.LayerShape(96, 256, 16, 32, 4, 2, "f32"), batch, "stress", 14)
 
 
-def _decode_batch_case(shape, batch, init, seed):
+def _decode_batch_case(shape, batch, init, seed, state_tol=None):
     from paper_2602_21144_amd import binding as B
     full = synth.make_layer(shape, seed, stress=(init == "stress"))
     rng = np.random.default_rng(100 + batch)
@@ -86,7 +89,8 @@ def _decode_batch_case(shape, batch, init, seed):
     for r in range(P):
         assert B.take_status(g._dws[r]) == 0
         # fp32: nothing is rounded on the way to the state (2e-5 as after a prefill)
-        assert_close(host(ssm[r]), sps[r], STATE_TOL if act == "bf16" else 2e-5, f"ssm_pool shard {r}")
+        tol_state = state_tol if state_tol is not None else (STATE_TOL if act == "bf16" else 2e-5)
+        assert_close(host(ssm[r]), sps[r], tol_state, f"ssm_pool shard {r}")
         assert_close(host(conv[r]), cps[r], TOL[act], f"conv_pool shard {r}")
 
 
