@@ -137,6 +137,11 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s)
 // the streamed kernel with the norm prologue above (plain bf16 stores); hipErrorNotSupported
 // when the shape does not suit it (the caller then runs the norm and the product apart)
 hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s);
+// Few-row product with float32 operands, C[M][N] = A[M][K] * B[N][K]^T in float32 (the
+// decode projections of a float32 layer); role (GemmRole) only names the kernel instance.
+// hipErrorNotSupported when the shape does not suit it (M > 64, K % 32, unaligned rows).
+hipError_t launch_gemv_f32_stream(int role, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                                  const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t s);
 
 struct ConvArgs {
     const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1

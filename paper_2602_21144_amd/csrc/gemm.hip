@@ -751,6 +751,12 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
                           float* scratch, size_t scratch_bytes) {
     if (M == 0 || N == 0) return hipSuccess;
     if (b_dt == SSM_F32) {
+        // up to 64 rows (a decode step): the weight stream in whole lines
+        if (M <= 64) {
+            const hipError_t e = launch_gemv_f32_stream(role, M, N, K, (const float*)A, lda, (const float*)B, ldb,
+                                                        (float*)C, ldc, s);
+            if (e != hipErrorNotSupported) return e;
+        }
         auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
         if (M <= 8 && K % 4 == 0 && lda % 4 == 0 && ldb % 4 == 0 && al16(A) && al16(B)) {
             const dim3 grid((unsigned)((N + 3) / 4));

@@ -48,11 +48,19 @@ def test_decode_wide_shard_batches(batch, init):
                        state_tol=TOL["bf16"] if init == "stress" else None)
 
 
-# fp32 activations and weights: at most 8 rows on the one-row-per-wave fp32 kernel, more
-# on 64x64 fp32 MFMA tiles
-@pytest.mark.parametrize("batch", [1, 8, 9, 40, 129])
+# fp32 activations and weights: up to 64 rows on the streamed fp32 kernel (16 waves for
+# these narrow outputs; 8, 16, 32 and 64 staged activation rows), more on 64x64 fp32 MFMA
+# tiles
+@pytest.mark.parametrize("batch", [1, 8, 9, 17, 40, 64, 65, 129])
 def test_decode_f32_batches(batch):
     _decode_batch_case(synth.LayerShape(96, 256, 16, 32, 4, 2, "f32"), batch, "stress", 14)
+
+
+# fp32, wide shard (2048 channels: in_proj 4096 columns, 8-wave workgroups on the streamed
+# kernel; x_proj 16 column tiles on 16 waves up to 32 rows, 8 waves for 64 rows)
+@pytest.mark.parametrize("batch", [5, 24, 40, 64])
+def test_decode_f32_wide_shard(batch):
+    _decode_batch_case(synth.LayerShape(256, 4096, 16, 64, 4, 2, "f32"), batch, "stress", 15)
 
 
 def _decode_batch_case(shape, batch, init, seed, state_tol=None):
