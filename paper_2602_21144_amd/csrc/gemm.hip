@@ -672,6 +672,132 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const fl
     }
 }
 
+// fp32 operands at prefill sizes: 128x128 tiles, four waves of 64x64 (4x4 tiles of
+// v_mfma_f32_16x16x4_f32), 32-wide k stages (one 128-byte line of every operand row).
+// Each stage moves global -> registers -> LDS in whole lines (8 threads per row), one
+// stage ahead of the MFMAs, into a double-buffered LDS ring (2 x 32 KB) with one barrier
+// per stage. Fragments are read as float4 along k: lane l takes chunk 4 g + l / 16 of row
+// l % 16 and MFMA u of group g uses component u, the same k for both operands. LDS rows
+// are XOR-swizzled in 16-byte chunks (chunk ^ ((row / 2) % 8)), which keeps both the
+// whole-row writes and the 16-row fragment reads free of bank conflicts. The weight
+// fragment is the MFMA's first operand, so a lane ends up with four consecutive output
+// columns of one row: float4 stores. Rows and columns past M, N read as zero.
+constexpr int kF32BK = 32;
+
+__device__ __forceinline__ int f32_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+template <int ROLE>
+__global__ __launch_bounds__(256) void gemm_f32_big(int M, int N, int K, const float* __restrict__ A, int64_t lda,
+                                                    const float* __restrict__ B, int64_t ldb, float* __restrict__ C,
+                                                    int64_t ldc, int tiles_m, int tiles_n, float* __restrict__ part) {
+    constexpr int BM = 128, BN = 128, TILE = 128 * 128;  // bytes of one operand tile per stage
+    __shared__ __attribute__((aligned(16))) char lds[2][2 * TILE];
+    int tm, tn;
+    tile_of(tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 4));
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 4));
+    // loads of one stage: thread t moves chunk t % 8 of rows t / 8 + 32 i of each operand
+    const int lrow = tid >> 3, lck = tid & 7;
+    u32x4 va[4], vb[4];
+    auto gload = [&](int st) {
+        const uint32_t kb = (uint32_t)(st * kF32BK + lck * 4) * 4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            va[i] = buffer_load16(ra, (uint32_t)((lrow + 32 * i) * lda) * 4 + kb);
+            vb[i] = buffer_load16(rb, (uint32_t)((lrow + 32 * i) * ldb) * 4 + kb);
+        }
+    };
+    auto lstore = [&](int buf) {
+        char* a = lds[buf];
+        char* b = lds[buf] + TILE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = lrow + 32 * i;
+            *(u32x4*)(a + r * 128 + f32_swz(r, lck) * 16) = va[i];
+            *(u32x4*)(b + r * 128 + f32_swz(r, lck) * 16) = vb[i];
+        }
+    };
+    f32x4 acc[4][4];  // [weight tile j][activation tile i]
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{};
+    // split-K: workgroup row blockIdx.y takes K-slice [s0, s0 + nst) of gridDim.y equal slices
+    // and writes its fp32 partial tile to part[blockIdx.y] (row stride N)
+    const int nst = K / kF32BK / gridDim.y, s0 = blockIdx.y * nst;
+    if (part) {
+        C = part + (int64_t)blockIdx.y * M * N;
+        ldc = N;
+    }
+    const int fr = lane & 15, cg = lane >> 4;
+    gload(s0);
+    lstore(0);
+    __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+        const int cur = st & 1;
+        if (st + 1 < nst) gload(s0 + st + 1);
+        const char* a = lds[cur];
+        const char* b = lds[cur] + TILE;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            const int c = 4 * g + cg;
+            f32x4 af[4], bfr[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = wm * 64 + 16 * i + fr;
+                af[i] = *(const f32x4*)(a + r * 128 + f32_swz(r, c) * 16);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = wn * 64 + 16 * j + fr;
+                bfr[j] = *(const f32x4*)(b + r * 128 + f32_swz(r, c) * 16);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(bfr[j][u], af[i][u], acc[j][i], 0, 0, 0);
+        }
+        if (st + 1 < nst) lstore(cur ^ 1);
+        __syncthreads();
+    }
+    // lane l holds activation row l % 16 and weight columns 4 (l / 16) + v of each tile pair
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + wm * 64 + 16 * i + fr;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + wn * 64 + 16 * j + 4 * cg;
+            float* p = C + (int64_t)m * ldc + n;
+            if (n + 3 < N && (ldc & 3) == 0) {
+                *(float4*)p = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (n + v < N) p[v] = acc[j][i][v];
+            }
+        }
+    }
+}
+
+// K-slices for a float32 product with few 128x128 tiles: the most slices (dividing the
+// 32-wide stages, at least 4 stages each) that keep the grid within about two workgroups
+// per CU. 1 = unsplit.
+int f32_slices(int64_t tiles, int64_t K) {
+    if (K % kF32BK != 0 || tiles >= 256) return 1;
+    const int64_t nk = K / kF32BK, cap = std::max<int64_t>(1, 512 / tiles);
+    int best = 1;
+    for (int64_t d = 2; d <= cap && d <= nk / 4; ++d)
+        if (nk % d == 0) best = (int)d;
+    return best;
+}
+
 template <int ROLE, int BM, int BN, int WM, int WN, bool AF, bool CF>
 hipError_t run_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                     void* C, int64_t ldc, hipStream_t s) {
@@ -736,6 +862,12 @@ hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t 
 }
 
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role) {
+    // float32 operands on 128x128 tiles (more than the 64 rows of the streamed kernel)
+    if (a_dt == SSM_F32 && b_dt == SSM_F32) {
+        if (M <= 64 || N == 0) return 0;
+        const int sp = f32_slices(((M + 127) / 128) * ((N + 127) / 128), K);
+        return sp > 1 ? (size_t)sp * M * N * 4 : 0;
+    }
     // mirrors the dispatch below: the DMA paths with bf16 operands and K % 64 == 0
     if (M <= 64 || N == 0 || b_dt != SSM_BF16 || a_dt != SSM_BF16 || K % 64 != 0) return 0;
     int64_t tiles;
@@ -774,6 +906,37 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
             }
 #undef SSM_F32_GEMV
             return hipGetLastError();
+        }
+        // prefill sizes: 128x128 tiles when they give a few rounds of workgroups, or when the
+        // product can be cut into K-slices to get there (x_proj: 32 tiles)
+        {
+            const int64_t tm2 = (M + 127) / 128, tn2 = (N + 127) / 128;
+            const int sp = fit_slices(f32_slices(tm2 * tn2, K), M, N, scratch_bytes);
+            if (K % kF32BK == 0 && (tm2 * tn2 >= 256 || sp > 1) && lda % 4 == 0 && ldb % 4 == 0 && al16(A) &&
+                al16(B) && al16(C) && 128 * lda * 4 < ((int64_t)1 << 31) && 128 * ldb * 4 < ((int64_t)1 << 31)) {
+                const dim3 grid((unsigned)(tm2 * tn2), (unsigned)sp);
+                float* part = sp > 1 ? scratch : nullptr;
+#define SSM_F32_BIG(R)                                                                                          \
+    case R:                                                                                                     \
+        SSM_LAUNCH(gemm_f32_big<R>, grid, dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, lda,       \
+                   (const float*)B, ldb, (float*)C, ldc, (int)tm2, (int)tn2, part);                             \
+        break;
+                switch (role) {
+                    SSM_F32_BIG(kGemmInProj)
+                    SSM_F32_BIG(kGemmXProj)
+                    SSM_F32_BIG(kGemmDtProj)
+                    SSM_F32_BIG(kGemmOutProj)
+                    default: SSM_F32_BIG(kGemmGeneric)
+                }
+#undef SSM_F32_BIG
+                if (sp <= 1) return hipGetLastError();
+                if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+                KernelTimer kt("gemm.splitk_reduce", s);
+                const int64_t n4 = M * ((N + 3) / 4);
+                SSM_LAUNCH((splitk_reduce_kernel<true>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
+                           (const float*)part, sp, (int)M, (int)N, C, ldc);
+                return hipGetLastError();
+            }
         }
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
 #define SSM_F32_CASE(R)                                                                                             \

@@ -41,7 +41,9 @@ GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 9
                (12, 2080, 1344), (9, 2100, 1280), (3, 4096, 64),
                # 17..64 rows over at least 192 tiles of 32 columns (32-column fragment kernel: 32- and
                # 64-row tiles, ragged N, a K tail of 8)
-               (17, 6150, 512), (40, 6176, 808), (64, 7168, 1024)]
+               (17, 6150, 512), (40, 6176, 808), (64, 7168, 1024),
+               # float32 at prefill sizes: 128x128 tiles (ragged M and N, K of 96 to 3584)
+               (2000, 3588, 224), (1500, 4100, 96), (2048, 7168, 3584)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -116,6 +118,33 @@ def test_gemm_split_k(B, role, M, N, K, c_f32):
     tol = 1e-5 if c_f32 else 8e-3
     assert_close(C.to(torch.float64).cpu().numpy(), ref, tol, f"split-K {role} {M}x{N}x{K}")
     assert_close(C1.to(torch.float64).cpu().numpy(), ref, tol, f"unsplit {role} {M}x{N}x{K}")
+
+
+F32_SPLITK_SHAPES = [("x_proj", 2048, 256, 3584), ("x_proj", 2000, 256, 3584), ("in_proj", 256, 3072, 768),
+                     ("out_proj", 300, 770, 1536), ("generic", 129, 130, 1024)]
+
+
+@pytest.mark.parametrize("role,M,N,K", F32_SPLITK_SHAPES)
+def test_gemm_split_k_f32(B, role, M, N, K):
+    """Float32 operands with few 128x128 tiles: K-slices on the tile kernel, their partials
+    added by the reduce kernel (ragged M and N included); matches the float64 product and
+    the unsplit run (64x64 tiles) to float32 accuracy."""
+    need = B.gemm_splitk_bytes(M, N, K, B.SSM_F32, B.SSM_F32, role)
+    assert need > 0, "this shape is expected to run split-K"
+    rng = np.random.default_rng(M + 3 * N + K)
+    A = _rnd_host(rng, (M, K), "f32")
+    Bm = _rnd_host(rng, (N, K), "f32", 1.0 / np.sqrt(K))
+    Ad, Bd = _dev(A, torch.float32), _dev(Bm, torch.float32)
+    scratch = torch.full((need // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    Np = (N + 3) // 4 * 4
+    C = torch.full((M, Np), float("nan"), dtype=torch.float32, device="cuda")[:, :N]
+    B.ssm_gemm_nt_role(Ad, Bd, C, role, scratch)
+    C1 = torch.full((M, Np), float("nan"), dtype=torch.float32, device="cuda")[:, :N]
+    B.ssm_gemm_nt_role(Ad, Bd, C1, role, None)
+    torch.cuda.synchronize()
+    ref = A.astype(np.float64) @ Bm.astype(np.float64).T
+    assert_close(C.to(torch.float64).cpu().numpy(), ref, 1e-5, f"split-K f32 {role} {M}x{N}x{K}")
+    assert_close(C1.to(torch.float64).cpu().numpy(), ref, 1e-5, f"unsplit f32 {role} {M}x{N}x{K}")
 
 
 def test_gemm_strided_operands(B):

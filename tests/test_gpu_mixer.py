@@ -190,7 +190,9 @@ def test_chunked_prefill_equals_whole_on_gpu(act):
         yc.append(host(g.prefill(x[a:b], B.SeqMeta([0, b - a], [0], [1 if a > 0 else 0], 1), cc, sc)[0]))
     assert_close(np.concatenate(yc), yw, TOL[act], "chunked y")
     assert_close(host(sc[0]), host(sw[0]), 1e-4 if act == "bf16" else 2e-5, "state")
-    assert torch.equal(cc[0], cw[0])
+    # the history is a copy of in_proj outputs, and a piece of a few rows runs in_proj on the
+    # few-row kernel while the whole prompt runs it on tiles: equal up to accumulation order
+    assert_close(host(cc[0]), host(cw[0]), TOL[act], "conv history")
 
 
 def test_prefill_is_deterministic():
