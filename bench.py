@@ -169,15 +169,6 @@ def role_of(name):
     return "prefill.scan" if name.startswith("prefill.scan_") else name
 
 
-ROLE_SOURCE = {"prefill.in_proj": "gemm.hip", "prefill.out_proj": "gemm.hip", "prefill.x_proj": "gemm.hip",
-               "prefill.dt_proj": "gemm.hip", "prefill.dt_round": "gemm.hip", "prefill.conv1d": "conv.hip",
-               "prefill.conv_history": "conv.hip", "prefill.scan_local": "scan.hip", "prefill.scan_link": "scan.hip",
-               "prefill.scan_main": "scan.hip", "decode.in_proj_conv": "skinny.hip", "decode.x_proj": "skinny.hip",
-               "decode.dt_proj_state": "skinny.hip", "decode.out_proj": "skinny.hip", "decode.in_proj": "gemm.hip",
-               "decode.dt_proj": "skinny.hip", "decode.conv": "conv.hip", "decode.state_update": "scan.hip",
-               "gemm.splitk_reduce": "gemm.hip", "exchange.reduce_add": "misc.hip"}
-
-
 def source_sha(src):
     import hashlib
     h = hashlib.sha256()
@@ -189,26 +180,29 @@ def source_sha(src):
 
 def profile_counters(stem, kind, role):
     """Per-launch counter values of a kernel role from a committed rocprofv3 summary
-    (profiles/<stem>.<kind>.txt), or None when there is no entry or the kernel's source has
-    changed since the counters were taken. kind "traffic": HBM bytes already scaled by the
-    copy calibration ({"fetch", "write"}); kind "util": {"valu", "trans"} instructions."""
+    (profiles/<stem>.<kind>.txt), or None when there is no entry or the kernel's source file
+    (named on the line) has changed since the counters were taken. kind "traffic": HBM
+    bytes already scaled by the copy calibration ({"fetch", "write"}); kind "util":
+    {"valu", "trans"} wave instructions per dispatch."""
     path = os.path.join(ROOT, "profiles", f"{stem}.{kind}.txt")
-    src = ROLE_SOURCE.get(role)
-    if src is None or not os.path.exists(path):
+    if not os.path.exists(path):
         return None
     with open(path) as f:
         for line in f:
             parts = line.split()
-            if line.startswith("#") or len(parts) < 5 or parts[0] != role:
+            if line.startswith("#") or not parts or parts[0] != role:
                 continue
-            if kind == "traffic":
-                if parts[4] != source_sha(src):
-                    return None
-                return {"fetch": float(parts[2]), "write": float(parts[3])}
-            if kind == "util" and len(parts) >= 9:
-                if parts[8] != source_sha(src):
-                    return None
-                return {"valu": float(parts[6]), "trans": float(parts[7])}
+            try:
+                if kind == "traffic":
+                    if parts[4] != source_sha(parts[5]):
+                        return None
+                    return {"fetch": float(parts[2]), "write": float(parts[3])}
+                if kind == "util":
+                    if parts[8] != source_sha(parts[9]):
+                        return None
+                    return {"valu": float(parts[6]), "trans": float(parts[7])}
+            except (IndexError, ValueError, OSError):
+                return None
     return None
 
 
