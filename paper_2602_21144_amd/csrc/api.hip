@@ -324,10 +324,21 @@ int decode2(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const float
         SSM_SKINNY("decode.out_proj", s, q, kSkinnyStoreBf16);
         return SSM_OK;
     }
-    SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "decode.dt_proj", kGemmDtProj));
     ScanArgs sa = scan_args(d, w, L.u, L.dt, L.xz, xdbl, B, nullptr, slot, nullptr, B, ssm_pool, S, L.g, L.status,
                             nullptr);
-    SSM_TIMED("decode.state_update", s, launch_decode_ssm(sa, adt == SSM_BF16, s));
+    sa.w_dt = w->dt_proj_w;
+    // dt_proj fused into the state step (one launch, no dt round trip) when its rows allow
+    hipError_t fused;
+    {
+        KernelTimer kt("decode.dt_proj_state", s);
+        fused = launch_decode_dt_ssm(sa, adt == SSM_BF16, s);
+    }
+    if (fused != hipErrorNotSupported) {
+        if (fused != hipSuccess) return hip_fail(fused, "decode.dt_proj_state");
+    } else {
+        SSM_TRY(gemm(B, E, R, xdbl, W, SSM_F32, w->dt_proj_w, R, adt, L.dt, E, adt, s, "decode.dt_proj", kGemmDtProj));
+        SSM_TIMED("decode.state_update", s, launch_decode_ssm(sa, adt == SSM_BF16, s));
+    }
     SSM_TRY(gemm(B, dm, E, L.g, E, adt, w->out_proj_w, E, adt, y, dm, adt, s, "decode.out_proj", kGemmOutProj,
                  L.splitk));
     return SSM_OK;

@@ -164,6 +164,9 @@ struct ScanArgs {
     float* pool;                                                   // [S][E][N]
     const int32_t* cu; const int32_t* slot; const int32_t* has_init;
     int32_t* status;
+    // decode with dt_proj fused into the state step: dt_proj weight [E][R] (act dtype);
+    // delta is x_dbl's first R columns
+    const void* w_dt;
     // scan scratch (prefill only)
     float* h_local; float* sum_delta; float* h_in; float* h0_seq;
     int64_t T; int E, nseq, S, win;                                // win: tokens per window
@@ -172,6 +175,9 @@ int scan_window_len(int64_t T, int E);
 size_t scan_scratch_bytes(int64_t max_T, int E, int max_seqs);
 hipError_t launch_scan_prefill(const ScanArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_decode_ssm(const ScanArgs& a, bool bf16_act, hipStream_t s);
+// the same state step with dt = delta . W_dt^T computed in place of reading it (dt_rank a
+// multiple of 8); hipErrorNotSupported otherwise
+hipError_t launch_decode_dt_ssm(const ScanArgs& a, bool bf16_act, hipStream_t s);
 
 // Names the launches made while it is alive; when timing is on (and the stream is not
 // being captured into a graph), each of those launches is timed by the kernel's own

@@ -513,6 +513,18 @@ DmaTiles dma_tiles(int64_t M, int64_t N) {
 }
 bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; }
 
+// Decode batches above the few-row kernels (65..512 rows): 64x64 tiles without K-slices
+// when they give at least 128 workgroups. Against 128x128 tiles cut into K-slices plus the
+// slices' reduce kernel, each tile reads more operand rows from L2, but the step loses a
+// launch and the partials' round trip (the 2.8B quarter shard's in_proj of 256 sequences:
+// 160 tiles).
+bool dma_decode_tiles(int64_t M, int64_t N, int64_t K) {
+    return K % 64 == 0 && M > 64 && M <= 512 && ((M + 63) / 64) * ((N + 63) / 64) >= 128;
+}
+// x_proj of a decode batch (up to 512 rows, at most 256 columns): 16-row tiles of the
+// few-row kernel, which spread over more workgroups than 64-row tiles and need no K-slices
+bool xproj_decode_skinny(int64_t M, int64_t N) { return M <= 512 && N <= 256; }
+
 // Split-K for outputs of fewer tiles than CUs: K is cut into equal slices of whole
 // 64-wide k-tiles (at least two per slice) so that up to ~384 workgroups run; the slices'
 // fp32 partials are added by a reduce kernel in slice order (deterministic).
@@ -532,6 +544,7 @@ int fit_slices(int sp, int64_t M, int64_t N, size_t scratch_bytes) {
 template <int ROLE, bool CF>
 hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                         void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
+    if (dma_decode_tiles(M, N, K)) return run_dma<ROLE, 64, 64, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     if (K % 64 == 0) {
         const DmaTiles t = dma_tiles(M, N);
         if (t == kTiles256x320) return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
@@ -827,7 +840,8 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
     // few rows: the weight read dominates; stream it with many narrow workgroups. fp32-A
     // dt_proj of a large decode batch (K = dt_rank) goes the same way: its staged 128x128
     // tiles would give only a few workgroups (20 for 256 sequences of a 1280-channel shard)
-    if (M <= 64 || (ROLE == kGemmDtProj && AF && M <= 512 && K <= 512)) {
+    if (M <= 64 || (ROLE == kGemmDtProj && AF && M <= 512 && K <= 512) ||
+        (ROLE == kGemmXProj && !AF && xproj_decode_skinny(M, N))) {
         SkinnyArgs p{};
         p.A = A; p.lda = lda; p.a_f32 = AF; p.B = (const bf16*)B; p.ldb = ldb; p.C = C; p.ldc = ldc;
         p.M = (int)M; p.N = (int)N; p.K = (int)K;
@@ -871,6 +885,8 @@ size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, Ge
     // mirrors the dispatch below: the DMA paths with bf16 operands and K % 64 == 0
     if (M <= 64 || N == 0 || b_dt != SSM_BF16 || a_dt != SSM_BF16 || K % 64 != 0) return 0;
     int64_t tiles;
+    if (role == kGemmXProj && xproj_decode_skinny(M, N)) return 0;
+    if (dma_decode_tiles(M, N, K)) return 0;
     if (role == kGemmXProj && N <= 256) tiles = (M + 63) / 64;
     else if (dma_big_tiles(M, N)) return 0;
     else tiles = ((M + 127) / 128) * ((N + 127) / 128);

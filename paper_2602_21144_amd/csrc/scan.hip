@@ -393,6 +393,78 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
     if (q == 0) ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>((y + Dc * u) * silu_f(z));
 }
 
+// The large-batch state step with dt_proj fused in: four lanes per (sequence, channel)
+// first form dt = sum_r delta[r] * W_dt[c][r] (delta rounded to the activation dtype, as
+// dt_proj's operand; lane q takes the 8-wide chunks q, q + 4, ... of the R columns, the
+// quad sums them with two shuffles), round dt to the activation dtype as dt_proj stores
+// it, then take the step of decode_ssm_kernel. One launch and no dt round trip instead of
+// a dt_proj GEMM followed by the state kernel.
+template <typename T>
+__global__ __launch_bounds__(256) void decode_dt_ssm_kernel(ScanArgs a) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t item = gid >> 2;
+    const int q = (int)(gid & 3);
+    const bool live = item < (int64_t)a.nseq * a.E;
+    const int64_t itc = live ? item : 0;
+    const int b = (int)(itc / a.E), c = (int)(itc % a.E);
+    const int slot = a.slot[b];
+    const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
+    const float* xrow = a.xdbl + (int64_t)b * a.ld_xdbl;
+    const float* xb = xrow + a.R;  // B at 0, C at kN (16-byte aligned)
+    const float4 Bq = ((const float4*)xb)[q], Cq = ((const float4*)(xb + kN))[q];
+    const float u = to_f32(((const T*)a.u)[(int64_t)b * a.E + c]);
+    const float z = to_f32(((const T*)a.z)[(int64_t)b * a.ld_z + c]);
+    const float bdt = a.b_dt[c], Dc = a.D[c];
+    // dt: chunks of 8 columns, chunk j on lane j % 4
+    const T* wrow = (const T*)a.w_dt + (int64_t)c * a.R;
+    float dt = 0.0f;
+    for (int j = q; j < a.R / 8; j += 4) {
+        const float4 d0 = *(const float4*)(xrow + 8 * j), d1 = *(const float4*)(xrow + 8 * j + 4);
+        const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        float wv[8];
+        if constexpr (sizeof(T) == 2) {
+            const bf16x8 w8 = *(const bf16x8*)(wrow + 8 * j);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) wv[e] = (float)w8[e];
+        } else {
+            const float4 w0 = *(const float4*)((const float*)wrow + 8 * j), w1 = *(const float4*)((const float*)wrow + 8 * j + 4);
+            wv[0] = w0.x; wv[1] = w0.y; wv[2] = w0.z; wv[3] = w0.w; wv[4] = w1.x; wv[5] = w1.y; wv[6] = w1.z; wv[7] = w1.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dt += to_f32(from_f32<T>(dv[e])) * wv[e];
+    }
+    dt += __shfl_xor(dt, 1);
+    dt += __shfl_xor(dt, 2);
+    dt = to_f32(from_f32<T>(dt));
+    __builtin_amdgcn_sched_barrier(0);
+    const bool slot_ok = slot >= 0 && slot < a.S;
+    float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
+    const float4 h = *hp;
+    const float delta = softplus_f(dt + bdt);
+    const float du = delta * u;
+    const float hv[4] = {h.x, h.y, h.z, h.w}, av[4] = {al.x, al.y, al.z, al.w};
+    const float bv[4] = {Bq.x, Bq.y, Bq.z, Bq.w}, cv[4] = {Cq.x, Cq.y, Cq.z, Cq.w};
+    float hn[4], y = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
+        y += cv[i] * hn[i];
+    }
+    y += __shfl_xor(y, 1);
+    y += __shfl_xor(y, 2);
+    asm volatile("" ::"v"(z), "v"(Dc));
+    if (!live) return;
+    if (!slot_ok) {
+        if (q == 0) {
+            atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+            ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>(0.0f);
+        }
+        return;
+    }
+    *hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
+    if (q == 0) ((T*)a.g)[(int64_t)b * a.E + c] = from_f32<T>((y + Dc * u) * silu_f(z));
+}
+
 }  // namespace
 
 // Window length: about target_windows(E) windows over the T tokens, so that every SIMD
@@ -473,6 +545,21 @@ hipError_t launch_decode_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
     const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
     if (bf) SSM_LAUNCH(decode_ssm_kernel<bf16>, grid, block, 0, s, a);
     else SSM_LAUNCH(decode_ssm_kernel<float>, grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace ssm
+
+namespace ssm {
+
+hipError_t launch_decode_dt_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
+    const int64_t lanes = (int64_t)a.nseq * a.E * 4;
+    if (lanes <= 0) return hipSuccess;
+    if (a.R % 8 != 0 || a.ld_xdbl % 4 != 0 || ((uintptr_t)a.xdbl & 15) != 0 || ((uintptr_t)a.w_dt & 15) != 0)
+        return hipErrorNotSupported;
+    const dim3 grid((unsigned)((lanes + 255) / 256)), block(256);
+    if (bf) SSM_LAUNCH(decode_dt_ssm_kernel<bf16>, grid, block, 0, s, a);
+    else SSM_LAUNCH(decode_dt_ssm_kernel<float>, grid, block, 0, s, a);
     return hipGetLastError();
 }
 

@@ -694,7 +694,10 @@ hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda
     if (M <= 8) SSM_F32S(1, 3);
     else if (M <= 16) SSM_F32S(2, 3);
     else if (M <= 32) SSM_F32S(4, 3);
-    else if constexpr (NW <= 8) SSM_F32S(8, 2);   // 64 activation rows: 10 KB of LDS per wave
+    else if constexpr (NW <= 8) {
+        if (M <= 48) SSM_F32S(6, 2);
+        else SSM_F32S(8, 2);   // 64 activation rows: 10 KB of LDS per wave
+    }
     else return hipErrorNotSupported;
 #undef SSM_F32S
     return hipGetLastError();

@@ -34,6 +34,16 @@ def test_decode_batches_across_tile_limit(batch, init):
     _decode_batch_case(synth.LayerShape(320, 384, 16, 32, 4, 2, "bf16"), batch, init, 11)
 
 
+# the 2.8B quarter shard (1280 channels) above 64 sequences: in_proj and out_proj on 64x64
+# tiles without K-slices (160 tiles at 256 sequences), x_proj on 16-row tiles, dt_proj
+# fused into the state step
+@pytest.mark.parametrize("batch", [65, 130, 256])
+@pytest.mark.parametrize("init", ["baseline", "stress"])
+def test_decode_large_batch_quarter_shard(batch, init):
+    _decode_batch_case(synth.LayerShape(2560, 5120, 16, 160, 4, 4, "bf16"), batch, init, 13,
+                       state_tol=TOL["bf16"] if init == "stress" else None)
+
+
 # wide shards: 17..64 sequences take the 32-column fragment kernel for in_proj, with the
 # conv window in its epilogue (3072 channels per shard: 6144 columns). Under the stress init
 # dt reaches a few units, and where the GPU's fp32 sum and the oracle's fp64 sum of a dt
@@ -58,7 +68,7 @@ def test_decode_f32_batches(batch):
 
 # fp32, wide shard (2048 channels: in_proj 4096 columns, 8-wave workgroups on the streamed
 # kernel; x_proj 16 column tiles on 16 waves up to 32 rows, 8 waves for 64 rows)
-@pytest.mark.parametrize("batch", [5, 24, 40, 64])
+@pytest.mark.parametrize("batch", [5, 24, 40, 48, 64])
 def test_decode_f32_wide_shard(batch):
     _decode_batch_case(synth.LayerShape(256, 4096, 16, 64, 4, 2, "f32"), batch, "stress", 15)
 

@@ -42,6 +42,8 @@ GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 9
                # 17..64 rows over at least 192 tiles of 32 columns (32-column fragment kernel: 32- and
                # 64-row tiles, ragged N, a K tail of 8)
                (17, 6150, 512), (40, 6176, 808), (64, 7168, 1024),
+               # decode batches of 65..512 rows over at least 128 tiles of 64x64, unsplit (ragged M and N)
+               (256, 2560, 2560), (130, 8192, 1280), (500, 1100, 640),
                # float32 at prefill sizes: 128x128 tiles (ragged M and N, K of 96 to 3584)
                (2000, 3588, 224), (1500, 4100, 96), (2048, 7168, 3584)]
 
@@ -89,9 +91,9 @@ def test_gemm_wide_tiles(B, M, N, K):
     assert_close(got, ref, 8e-3, f"gemm {M}x{N}x{K}")
 
 
-SPLITK_SHAPES = [("out_proj", 256, 2560, 5120, False), ("in_proj", 256, 10240, 2560, False),
-                 ("x_proj", 300, 192, 5120, True), ("x_proj", 2048, 256, 3584, True), ("in_proj", 100, 5416, 2560, False),
-                 ("out_proj", 333, 3584, 3584, False), ("generic", 129, 130, 1024, False), ("x_proj", 65, 80, 1536, True)]
+SPLITK_SHAPES = [("out_proj", 600, 2560, 5120, False), ("in_proj", 600, 3000, 2560, False),
+                 ("x_proj", 1000, 192, 5120, True), ("x_proj", 2048, 256, 3584, True), ("in_proj", 600, 2000, 2560, False),
+                 ("out_proj", 700, 3584, 3584, False), ("generic", 129, 130, 1024, False), ("x_proj", 600, 80, 1536, True)]
 
 
 @pytest.mark.parametrize("role,M,N,K,c_f32", SPLITK_SHAPES)
@@ -118,6 +120,21 @@ def test_gemm_split_k(B, role, M, N, K, c_f32):
     tol = 1e-5 if c_f32 else 8e-3
     assert_close(C.to(torch.float64).cpu().numpy(), ref, tol, f"split-K {role} {M}x{N}x{K}")
     assert_close(C1.to(torch.float64).cpu().numpy(), ref, tol, f"unsplit {role} {M}x{N}x{K}")
+
+
+@pytest.mark.parametrize("M,N,K", [(65, 192, 1280), (256, 192, 1280), (511, 256, 3584), (300, 80, 1536)])
+def test_gemm_x_proj_decode_rows(B, M, N, K):
+    """x_proj of a decode batch of 65..512 rows runs on 16-row tiles of the few-row kernel
+    (no K-slices, no scratch needed); bf16 operands, float32 output."""
+    assert B.gemm_splitk_bytes(M, N, K, B.SSM_BF16, B.SSM_BF16, "x_proj") == 0
+    rng = np.random.default_rng(M + N + K)
+    A = _rnd_host(rng, (M, K), "bf16")
+    Bm = _rnd_host(rng, (N, K), "bf16", 1.0 / np.sqrt(K))
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    B.ssm_gemm_nt_role(_dev(A, torch.bfloat16), _dev(Bm, torch.bfloat16), C, "x_proj", None)
+    torch.cuda.synchronize()
+    ref = A.astype(np.float64) @ Bm.astype(np.float64).T
+    assert_close(C.to(torch.float64).cpu().numpy(), ref, 1e-5, f"x_proj {M}x{N}x{K}")
 
 
 F32_SPLITK_SHAPES = [("x_proj", 2048, 256, 3584), ("x_proj", 2000, 256, 3584), ("in_proj", 256, 3072, 768),
