@@ -147,6 +147,8 @@ struct DecodeWs {
     char *xz, *u, *dt, *g;
     float* xdbl;
     Scratch splitk;  // fp32 partials of the projections that run split-K (large batches)
+    float* inproj_part;  // in_proj's K-slice partials, added by the conv step (large bf16 batches)
+    int inproj_slices;   // 0: in_proj and the conv step run apart
     size_t total;
 };
 
@@ -181,6 +183,10 @@ DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
     }
     L.splitk.p = (float*)take(sk);
     L.splitk.bytes = sk;
+    L.inproj_slices = 0;
+    if (B > kFusedDecodeMax && adt == SSM_BF16 && d->d_conv >= 2)
+        L.inproj_slices = decode_inproj_slices(B, 2 * E, dm);
+    L.inproj_part = (float*)take((size_t)L.inproj_slices * B * 2 * E * 4);
     L.total = off;
     return L;
 }
@@ -299,10 +305,21 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
         SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
         return SSM_OK;
     }
-    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj", kGemmInProj,
-                 L.splitk));
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
-    SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
+    if (L.inproj_slices > 0) {
+        // in_proj as K-slice partials; the conv step adds them, stores the gate half and
+        // convolves the SSM half (no separate reduce launch)
+        SSM_TIMED("decode.in_proj", s, launch_gemm_partials_bf16(B, 2 * E, dm, x, dm, w->in_proj_w, dm, L.inproj_part,
+                                                                 L.inproj_slices, s));
+        ca.part = L.inproj_part;
+        ca.splits = L.inproj_slices;
+        ca.xz_out = L.xz;
+        SSM_TIMED("decode.conv", s, launch_conv_decode_partials(ca, true, s));
+    } else {
+        SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj",
+                     kGemmInProj, L.splitk));
+        SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
+    }
     SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj,
                  L.splitk));
     return SSM_OK;

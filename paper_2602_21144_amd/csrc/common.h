@@ -111,6 +111,12 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
                           hipStream_t s, GemmRole role, float* scratch = nullptr, size_t scratch_bytes = 0);
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role);
+// in_proj of a decode batch of 65..512 rows as float32 K-slice partials (bf16 operands,
+// 64x64 tiles), for a consumer that adds the slices itself: the number of slices, 0 when
+// the shape does not take this path
+int decode_inproj_slices(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_partials_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                                     int64_t ldb, float* part, int splits, hipStream_t s);
 
 // Few-row (decode) GEMM C = A * B^T with a fused epilogue; bf16 weights.
 enum SkinnyEpi { kSkinnyStoreBf16 = 0, kSkinnyStoreF32 = 1, kSkinnyConv = 2, kSkinnyState = 3 };
@@ -151,8 +157,14 @@ struct ConvArgs {
     const int32_t* cu; const int32_t* slot; const int32_t* has_init;
     int32_t* status;
     int64_t T; int E, K, nseq, S;
+    // decode from in_proj's K-slice partials (launch_conv_decode_partials): part
+    // [splits][nseq][2E] float32; the gate half is stored to xz_out (row stride ld_xz)
+    const float* part; int splits; void* xz_out;
 };
 hipError_t launch_conv_prefill(const ConvArgs& a, bool bf16_act, hipStream_t s);
+// decode: sum in_proj's K-slice partials of each row (in slice order), store the gate half,
+// and take the conv step on the SSM half (as launch_conv_decode does on a stored xz)
+hipError_t launch_conv_decode_partials(const ConvArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_conv_state_update(const ConvArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_conv_decode(const ConvArgs& a, bool bf16_act, hipStream_t s);
 

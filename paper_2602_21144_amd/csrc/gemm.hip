@@ -875,6 +875,25 @@ hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t 
     return hipGetLastError();
 }
 
+int decode_inproj_slices(int64_t M, int64_t N, int64_t K) {
+    if (K % 64 != 0 || M <= 64 || M > 512) return 0;
+    const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64), nk = K / 64;
+    int best = 1;  // slices dividing the stages, at least 8 stages each, about two workgroups per CU
+    for (int64_t d = 2; tiles * d <= 512 && nk / d >= 8; ++d)
+        if (nk % d == 0) best = (int)d;
+    return best;
+}
+
+hipError_t launch_gemm_partials_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                                     int64_t ldb, float* part, int splits, hipStream_t s) {
+    if (splits < 1 || K % (64 * splits) != 0) return hipErrorInvalidValue;
+    const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
+    SSM_LAUNCH((gemm_bf16_dma<kGemmInProj, 64, 64, 64, 3, 2, 2, true, true>), dim3(tm * tn, splits), dim3(256), 0, s,
+               (int)M, (int)N, (int)(K / splits), (const bf16*)A, lda, (const bf16*)B, ldb, (void*)part, N, tm, tn,
+               part);
+    return hipGetLastError();
+}
+
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role) {
     // float32 operands on 128x128 tiles (more than the 64 rows of the streamed kernel)
     if (a_dt == SSM_F32 && b_dt == SSM_F32) {

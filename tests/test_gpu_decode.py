@@ -44,6 +44,13 @@ def test_decode_large_batch_quarter_shard(batch, init):
                        state_tol=TOL["bf16"] if init == "stress" else None)
 
 
+# conv widths 2 and 3 above 64 sequences: the conv step adds in_proj's partials itself
+@pytest.mark.parametrize("d_conv", [2, 3])
+def test_decode_large_batch_conv_widths(d_conv):
+    _decode_batch_case(synth.LayerShape(320, 384, 16, 32, d_conv, 2, "bf16"), 100, "stress", 16,
+                       state_tol=TOL["bf16"])
+
+
 # wide shards: 17..64 sequences take the 32-column fragment kernel for in_proj, with the
 # conv window in its epilogue (3072 channels per shard: 6144 columns). Under the stress init
 # dt reaches a few units, and where the GPU's fp32 sum and the oracle's fp64 sum of a dt
