@@ -147,22 +147,21 @@ def kernel_work(sh, kind, n, nseq):
             out["prefill.dt_round"] = ("hbm", T * R * 4 + T * R * 2)
         return out
     M = n
-    if bf and K >= 2 and M <= 64:
+    # dt_proj with the state step fused (its epilogue up to 64 sequences, the state-step
+    # kernel above): weights, delta, B and C, u and z, g, state read + write
+    state = ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4 + E * (N + 2) * 4)
+    if bf and K >= 2 and M <= 512:
         return {
             # in_proj with the conv window fused: weights, x_t, u and z out, history read + write
             "decode.in_proj_conv": ("hbm", 2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
                                     + E * (K + 1) * s),
             "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
-            # dt_proj with the state step fused: weights, delta, B and C, u and z, g, state read + write
-            "decode.dt_proj_state": ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4
-                                     + E * (N + 2) * 4),
+            "decode.dt_proj_state": state,
             "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
     return {"decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
             "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
             "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
-            # dt_proj fused into the state step: weights, delta, B and C, u and z, g, state read + write
-            "decode.dt_proj_state": ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4
-                                     + E * (N + 2) * 4),
+            "decode.dt_proj_state": state,
             "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
 
 
@@ -311,21 +310,23 @@ class Workload:
 
 def measure(B, torch, wl, steps, warmup, dominant_every=None):
     """Warm-up steps, one step with every kernel timed (the per-kernel breakdown; the host
-    waits for each phase), then the
+    drains the stream before each launch), then the
     timed steps with events at every phase boundary and the dominant kernel's dispatches
     timed by their own events (every launch if it runs 200 us or more, else every 16th)."""
     import numpy as np
     for _ in range(max(warmup, 1)):
         wl.step()
     torch.cuda.synchronize()
-    # the breakdown step waits for each phase before issuing the next: a timed dispatch
-    # queued behind running work can read its wait in the queue as part of its duration
+    # the breakdown step drains the stream before each timed launch: a dispatch queued
+    # behind unfinished work reads part of its wait in the queue as its own duration
     B.ssm_timing_collect()
     B.ssm_timing_enable(True)
+    B.ssm_timing_serialize(True)
     for cs in wl.calls:
         for c in cs:
             c()
-        torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    B.ssm_timing_serialize(False)
     B.ssm_timing_enable(False)
     breakdown = B.ssm_timing_collect()
     dominant = max(breakdown, key=lambda n: breakdown[n][1])

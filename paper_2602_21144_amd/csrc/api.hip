@@ -147,18 +147,19 @@ struct DecodeWs {
     char *xz, *u, *dt, *g;
     float* xdbl;
     Scratch splitk;  // fp32 partials of the projections that run split-K (large batches)
-    float* inproj_part;  // in_proj's K-slice partials, added by the conv step (large bf16 batches)
-    int inproj_slices;   // 0: in_proj and the conv step run apart
     size_t total;
 };
 
-// Largest decode batch that takes the fused kernels (in_proj with the conv step in its
-// epilogue, dt_proj with the state step in its epilogue): each of their workgroups reads
-// every activation row, which suits a few rows. Larger batches run tiled projections
-// (split-K when the output has few tiles), a conv-step kernel and a state-step kernel
-// with four lanes per (sequence, channel). Measured on the 2.8B quarter shard: fused
-// faster at 64 sequences (42.9 against 48.6 us per step), tiled at 128 (61.5 against 68.3).
+// Largest decode batch whose dt_proj takes the state step in its epilogue (each workgroup
+// of that kernel reads every activation row, which suits a few rows); larger batches run
+// the state-step kernel with four lanes per (sequence, channel) and dt_proj folded in.
+// Measured on the 2.8B quarter shard: the epilogue form faster at 64 sequences, the
+// state-step kernel at 128.
 constexpr int kFusedDecodeMax = 64;
+// Largest bf16 decode batch whose in_proj takes the conv step in its epilogue: the
+// streamed projection kernels cover up to 512 rows (16-row tiles, then tiles of 32 or 64
+// rows over 32 columns).
+constexpr int kConvEpilogueMax = 512;
 
 DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
     const size_t s = act_bytes(d);
@@ -183,10 +184,6 @@ DecodeWs decode_layout(const ssm_shard_desc_t* d, int64_t B, void* base) {
     }
     L.splitk.p = (float*)take(sk);
     L.splitk.bytes = sk;
-    L.inproj_slices = 0;
-    if (B > kFusedDecodeMax && adt == SSM_BF16 && d->d_conv >= 2)
-        L.inproj_slices = decode_inproj_slices(B, 2 * E, dm);
-    L.inproj_part = (float*)take((size_t)L.inproj_slices * B * 2 * E * 4);
     L.total = off;
     return L;
 }
@@ -294,7 +291,7 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
             void* conv_pool, int32_t S, float* xdbl, const DecodeWs& L, hipStream_t s) {
     const int adt = d->act_dtype;
     const int64_t E = d->d_inner_shard, W = d->dt_rank + 2 * d->d_state, dm = d->d_model;
-    if (adt == SSM_BF16 && d->d_conv >= 2 && B <= kFusedDecodeMax) {
+    if (adt == SSM_BF16 && d->d_conv >= 2 && B <= kConvEpilogueMax) {
         // in_proj with the conv window shift + SiLU fused into its epilogue; x_proj
         SkinnyArgs p = skinny(x, dm, false, w->in_proj_w, dm, L.xz, 2 * E, B, 2 * E, dm);
         p.slot = slot; p.S = S; p.status = L.status; p.E = (int)E;
@@ -306,20 +303,9 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
         return SSM_OK;
     }
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
-    if (L.inproj_slices > 0) {
-        // in_proj as K-slice partials; the conv step adds them, stores the gate half and
-        // convolves the SSM half (no separate reduce launch)
-        SSM_TIMED("decode.in_proj", s, launch_gemm_partials_bf16(B, 2 * E, dm, x, dm, w->in_proj_w, dm, L.inproj_part,
-                                                                 L.inproj_slices, s));
-        ca.part = L.inproj_part;
-        ca.splits = L.inproj_slices;
-        ca.xz_out = L.xz;
-        SSM_TIMED("decode.conv", s, launch_conv_decode_partials(ca, true, s));
-    } else {
-        SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj",
-                     kGemmInProj, L.splitk));
-        SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
-    }
+    SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj",
+                 kGemmInProj, L.splitk));
+    SSM_TIMED("decode.conv", s, launch_conv_decode(ca, adt == SSM_BF16, s));
     SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj,
                  L.splitk));
     return SSM_OK;
@@ -1078,7 +1064,7 @@ int ssm2_shard_decode_stage1(const ssm2_shard_desc_t* d, const ssm2_shard_weight
     SSM_TRY(check_ptr(conv_pool, "conv_pool"));
     SSM_TRY(check_ptr(ssm_pool, "ssm_pool"));
     SSM_TRY(check_ptr(sumsq_partial, "sumsq_partial"));
-    if (B <= kFusedDecodeMax) {
+    if (B <= kConvEpilogueMax) {
         // in_proj with the conv window shift + SiLU of the x, B, C columns in its epilogue
         SkinnyArgs p = skinny(x, m.dm, false, w->in_proj_w, m.dm, L.zx, m.rows, B, m.rows, m.dm);
         p.slot = slot; p.S = S; p.status = L.status;

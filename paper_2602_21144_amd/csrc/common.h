@@ -94,6 +94,60 @@ __device__ __forceinline__ int xcd_contiguous(int b, int n) {
     return x * per + (x < rem ? x : rem) + i;
 }
 
+// n elements at a 16-byte aligned address, as whole 16-byte loads and stores
+template <typename T, int n> __device__ __forceinline__ void load16(const T* p, T (&o)[n]) {
+    static_assert((n * sizeof(T)) % 16 == 0, "whole 16-byte pieces");
+    u32x4 r[n * sizeof(T) / 16];
+#pragma unroll
+    for (int i = 0; i < (int)(n * sizeof(T) / 16); ++i) r[i] = ((const u32x4*)p)[i];
+    __builtin_memcpy(o, r, sizeof o);
+}
+template <typename T, int n> __device__ __forceinline__ void store16(T* p, const T (&o)[n]) {
+    static_assert((n * sizeof(T)) % 16 == 0, "whole 16-byte pieces");
+    u32x4 r[n * sizeof(T) / 16];
+    __builtin_memcpy(r, o, sizeof o);
+#pragma unroll
+    for (int i = 0; i < (int)(n * sizeof(T) / 16); ++i) ((u32x4*)p)[i] = r[i];
+}
+
+// One decode step of the cached convolution window (Section IV-A: the conv half of the
+// cache) for 8 consecutive channels c0..c0+7 of one sequence: out = SiLU(b + sum_j w[j] *
+// window), with cur (the new input, already in the activation dtype) as the newest tap,
+// then the history [8][K-1] (oldest first) shifted by one with cur appended. The history (8 (K-1) elements), the weights [8][K] and the
+// bias are contiguous 16-byte multiples at 16-byte aligned addresses (c0 % 8 == 0), so
+// each is read and written in whole 16-byte pieces. hist_ok false: the slot was bad;
+// nothing is written to the history and out is zero.
+template <typename T, int K>
+__device__ __forceinline__ void conv_window_step8(const float (&cur)[8], T* hist, bool hist_ok, const T* w,
+                                                  const T* b, float (&out)[8]) {
+    T wv[8 * K], bv[8];
+    load16(w, wv);
+    load16(b, bv);
+    if constexpr (K > 1) {
+        T hv[8 * (K - 1)];
+        load16(hist, hv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float acc = to_f32(bv[i]);
+#pragma unroll
+            for (int j = 0; j < K - 1; ++j) acc += to_f32(wv[i * K + j]) * to_f32(hv[i * (K - 1) + j]);
+            acc += to_f32(wv[i * K + K - 1]) * cur[i];
+            out[i] = hist_ok ? silu_f(acc) : 0.0f;
+        }
+        T nh[8 * (K - 1)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j + 1 < K - 1; ++j) nh[i * (K - 1) + j] = hv[i * (K - 1) + j + 1];
+            nh[i * (K - 1) + K - 2] = from_f32<T>(cur[i]);
+        }
+        if (hist_ok) store16(hist, nh);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) out[i] = hist_ok ? silu_f(to_f32(bv[i]) + to_f32(wv[i]) * cur[i]) : 0.0f;
+    }
+}
+
 // Workspace header: status word at offset 0; regions start 256-byte aligned.
 constexpr size_t kWsHeader = 256;
 __host__ __device__ inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
@@ -111,13 +165,6 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
                           const void* B, int64_t ldb, int b_dt, void* C, int64_t ldc, int c_dt,
                           hipStream_t s, GemmRole role, float* scratch = nullptr, size_t scratch_bytes = 0);
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role);
-// in_proj of a decode batch of 65..512 rows as float32 K-slice partials (bf16 operands,
-// 64x64 tiles), for a consumer that adds the slices itself: the number of slices, 0 when
-// the shape does not take this path
-int decode_inproj_slices(int64_t M, int64_t N, int64_t K);
-hipError_t launch_gemm_partials_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
-                                     int64_t ldb, float* part, int splits, hipStream_t s);
-
 // Few-row (decode) GEMM C = A * B^T with a fused epilogue; bf16 weights.
 enum SkinnyEpi { kSkinnyStoreBf16 = 0, kSkinnyStoreF32 = 1, kSkinnyConv = 2, kSkinnyState = 3 };
 struct SkinnyArgs {
@@ -157,14 +204,8 @@ struct ConvArgs {
     const int32_t* cu; const int32_t* slot; const int32_t* has_init;
     int32_t* status;
     int64_t T; int E, K, nseq, S;
-    // decode from in_proj's K-slice partials (launch_conv_decode_partials): part
-    // [splits][nseq][2E] float32; the gate half is stored to xz_out (row stride ld_xz)
-    const float* part; int splits; void* xz_out;
 };
 hipError_t launch_conv_prefill(const ConvArgs& a, bool bf16_act, hipStream_t s);
-// decode: sum in_proj's K-slice partials of each row (in slice order), store the gate half,
-// and take the conv step on the SSM half (as launch_conv_decode does on a stored xz)
-hipError_t launch_conv_decode_partials(const ConvArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_conv_state_update(const ConvArgs& a, bool bf16_act, hipStream_t s);
 hipError_t launch_conv_decode(const ConvArgs& a, bool bf16_act, hipStream_t s);
 

@@ -209,32 +209,13 @@ __global__ __launch_bounds__(256) void conv_decode_kernel(ConvArgs a) {
     const int bidx = (int)(gid / groups);
     const int c0 = (int)(gid % groups) * kCV;
     const int slot = a.slot[bidx];
-    float out[kCV];
-    if (slot < 0 || slot >= a.S) {
-        atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-#pragma unroll
-        for (int i = 0; i < kCV; ++i) out[i] = 0.0f;
-        Vec8<T>::store((T*)a.u + (int64_t)bidx * a.E + c0, out);
-        return;
-    }
-    float cur[kCV];
+    const bool slot_ok = slot >= 0 && slot < a.S;
+    float cur[kCV], out[kCV];
     Vec8<T>::load((const T*)a.xz + (int64_t)bidx * a.ld_xz + c0, cur);
-    T* hist = (T*)a.conv_pool + ((int64_t)slot * a.E + c0) * (K - 1);
-#pragma unroll
-    for (int i = 0; i < kCV; ++i) {
-        float hv[K > 1 ? K - 1 : 1];
-#pragma unroll
-        for (int j = 0; j < K - 1; ++j) hv[j] = to_f32(hist[i * (K - 1) + j]);
-        float acc = to_f32(((const T*)a.b)[c0 + i]);
-        const T* wr = (const T*)a.w + (c0 + i) * K;
-#pragma unroll
-        for (int j = 0; j < K - 1; ++j) acc += to_f32(wr[j]) * hv[j];
-        acc += to_f32(wr[K - 1]) * cur[i];
-        out[i] = silu_f(acc);
-#pragma unroll
-        for (int j = 0; j + 1 < K - 1; ++j) hist[i * (K - 1) + j] = from_f32<T>(hv[j + 1]);
-        if (K > 1) hist[i * (K - 1) + (K > 1 ? K - 2 : 0)] = from_f32<T>(cur[i]);
-    }
+    // a bad slot still addresses slot 0 for the (discarded) history read
+    T* hist = (T*)a.conv_pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c0) * (K - 1);
+    conv_window_step8<T, K>(cur, hist, slot_ok, (const T*)a.w + (int64_t)c0 * K, (const T*)a.b + c0, out);
+    if (!slot_ok) atomicOr(a.status, SSM_STATUS_BAD_SLOT);
     Vec8<T>::store((T*)a.u + (int64_t)bidx * a.E + c0, out);
 }
 
@@ -252,65 +233,6 @@ __global__ __launch_bounds__(256) void conv_decode_kernel(ConvArgs a) {
         return hipGetLastError();                                                             \
     } while (0)
 
-// Decode from in_proj's K-slice partials: one thread per 8 columns of one row of the
-// [nseq][2E] product. The slices are added in order; gate columns are stored rounded to
-// the activation dtype; SSM-path columns, rounded the same way, enter the cached window
-// (the arithmetic of conv_decode_kernel). One launch in place of a split-K reduce and the
-// conv step.
-template <typename T, int K>
-__global__ __launch_bounds__(256) void conv_decode_partials_kernel(ConvArgs a) {
-    const int groups = 2 * a.E / kCV;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= (int64_t)a.nseq * groups) return;
-    const int bidx = (int)(gid / groups);
-    const int n0 = (int)(gid % groups) * kCV;
-    const int64_t n2 = 2 * (int64_t)a.E;
-    float v[kCV];
-#pragma unroll
-    for (int i = 0; i < kCV; ++i) v[i] = 0.0f;
-    const float* p = a.part + (int64_t)bidx * n2 + n0;
-    const int64_t slice = (int64_t)a.nseq * n2;
-    for (int sp = 0; sp < a.splits; ++sp, p += slice) {
-        const float4 x0 = *(const float4*)p, x1 = *(const float4*)(p + 4);
-        v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w;
-        v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
-    }
-    if (n0 >= a.E) {
-        Vec8<T>::store((T*)a.xz_out + (int64_t)bidx * a.ld_xz + n0, v);
-        return;
-    }
-    const int c0 = n0;
-    const int slot = a.slot[bidx];
-    float out[kCV];
-    if (slot < 0 || slot >= a.S) {
-        atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-#pragma unroll
-        for (int i = 0; i < kCV; ++i) out[i] = 0.0f;
-        Vec8<T>::store((T*)a.u + (int64_t)bidx * a.E + c0, out);
-        return;
-    }
-    float cur[kCV];
-#pragma unroll
-    for (int i = 0; i < kCV; ++i) cur[i] = to_f32(from_f32<T>(v[i]));  // the stored projection output
-    T* hist = (T*)a.conv_pool + ((int64_t)slot * a.E + c0) * (K - 1);
-#pragma unroll
-    for (int i = 0; i < kCV; ++i) {
-        float hv[K > 1 ? K - 1 : 1];
-#pragma unroll
-        for (int j = 0; j < K - 1; ++j) hv[j] = to_f32(hist[i * (K - 1) + j]);
-        float acc = to_f32(((const T*)a.b)[c0 + i]);
-        const T* wr = (const T*)a.w + (c0 + i) * K;
-#pragma unroll
-        for (int j = 0; j < K - 1; ++j) acc += to_f32(wr[j]) * hv[j];
-        acc += to_f32(wr[K - 1]) * cur[i];
-        out[i] = silu_f(acc);
-#pragma unroll
-        for (int j = 0; j + 1 < K - 1; ++j) hist[i * (K - 1) + j] = from_f32<T>(hv[j + 1]);
-        if (K > 1) hist[i * (K - 1) + (K > 1 ? K - 2 : 0)] = from_f32<T>(cur[i]);
-    }
-    Vec8<T>::store((T*)a.u + (int64_t)bidx * a.E + c0, out);
-}
-
 }  // namespace
 
 hipError_t launch_conv_prefill(const ConvArgs& a, bool bf, hipStream_t s) {
@@ -323,12 +245,6 @@ hipError_t launch_conv_state_update(const ConvArgs& a, bool bf, hipStream_t s) {
     const int64_t threads = (int64_t)a.nseq * (a.E / kCV);
     if (bf) SSM_CONV_LAUNCH(conv_state_update_kernel, bf16, a, threads, s);
     SSM_CONV_LAUNCH(conv_state_update_kernel, float, a, threads, s);
-}
-hipError_t launch_conv_decode_partials(const ConvArgs& a, bool bf, hipStream_t s) {
-    if (a.K < 2 || a.E % kCV != 0) return hipErrorInvalidValue;
-    const int64_t threads = (int64_t)a.nseq * (2 * a.E / kCV);
-    if (bf) SSM_CONV_LAUNCH(conv_decode_partials_kernel, bf16, a, threads, s);
-    SSM_CONV_LAUNCH(conv_decode_partials_kernel, float, a, threads, s);
 }
 hipError_t launch_conv_decode(const ConvArgs& a, bool bf, hipStream_t s) {
     const int64_t threads = (int64_t)a.nseq * (a.E / kCV);

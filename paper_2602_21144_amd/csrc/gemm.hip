@@ -513,13 +513,11 @@ DmaTiles dma_tiles(int64_t M, int64_t N) {
 }
 bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; }
 
-// Decode batches above the few-row kernels (65..512 rows): 64x64 tiles without K-slices
-// when they give at least 128 workgroups. Against 128x128 tiles cut into K-slices plus the
-// slices' reduce kernel, each tile reads more operand rows from L2, but the step loses a
-// launch and the partials' round trip (the 2.8B quarter shard's in_proj of 256 sequences:
-// 160 tiles).
-bool dma_decode_tiles(int64_t M, int64_t N, int64_t K) {
-    return K % 64 == 0 && M > 64 && M <= 512 && ((M + 63) / 64) * ((N + 63) / 64) >= 128;
+// Decode batches above the few-row kernels (65..512 rows) with bf16 output: the streamed
+// tile kernel of the decode projections (launch_gemm_skinny) when its tiles give at least
+// 128 workgroups, without K-slices
+bool decode_tiles(int64_t M, int64_t N, int64_t K) {
+    return K % 64 == 0 && M > 64 && M <= 512 && ((M + 31) / 32) * ((N + 31) / 32) >= 128;
 }
 // x_proj of a decode batch (up to 512 rows, at most 256 columns): 16-row tiles of the
 // few-row kernel, which spread over more workgroups than 64-row tiles and need no K-slices
@@ -544,7 +542,6 @@ int fit_slices(int sp, int64_t M, int64_t N, size_t scratch_bytes) {
 template <int ROLE, bool CF>
 hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
                         void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
-    if (dma_decode_tiles(M, N, K)) return run_dma<ROLE, 64, 64, 64, 3, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
     if (K % 64 == 0) {
         const DmaTiles t = dma_tiles(M, N);
         if (t == kTiles256x320) return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
@@ -841,7 +838,7 @@ hipError_t dispatch_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t
     // dt_proj of a large decode batch (K = dt_rank) goes the same way: its staged 128x128
     // tiles would give only a few workgroups (20 for 256 sequences of a 1280-channel shard)
     if (M <= 64 || (ROLE == kGemmDtProj && AF && M <= 512 && K <= 512) ||
-        (ROLE == kGemmXProj && !AF && xproj_decode_skinny(M, N))) {
+        (ROLE == kGemmXProj && !AF && xproj_decode_skinny(M, N)) || (!AF && !CF && decode_tiles(M, N, K))) {
         SkinnyArgs p{};
         p.A = A; p.lda = lda; p.a_f32 = AF; p.B = (const bf16*)B; p.ldb = ldb; p.C = C; p.ldc = ldc;
         p.M = (int)M; p.N = (int)N; p.K = (int)K;
@@ -875,25 +872,6 @@ hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t 
     return hipGetLastError();
 }
 
-int decode_inproj_slices(int64_t M, int64_t N, int64_t K) {
-    if (K % 64 != 0 || M <= 64 || M > 512) return 0;
-    const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64), nk = K / 64;
-    int best = 1;  // slices dividing the stages, at least 8 stages each, about two workgroups per CU
-    for (int64_t d = 2; tiles * d <= 512 && nk / d >= 8; ++d)
-        if (nk % d == 0) best = (int)d;
-    return best;
-}
-
-hipError_t launch_gemm_partials_bf16(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
-                                     int64_t ldb, float* part, int splits, hipStream_t s) {
-    if (splits < 1 || K % (64 * splits) != 0) return hipErrorInvalidValue;
-    const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
-    SSM_LAUNCH((gemm_bf16_dma<kGemmInProj, 64, 64, 64, 3, 2, 2, true, true>), dim3(tm * tn, splits), dim3(256), 0, s,
-               (int)M, (int)N, (int)(K / splits), (const bf16*)A, lda, (const bf16*)B, ldb, (void*)part, N, tm, tn,
-               part);
-    return hipGetLastError();
-}
-
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role) {
     // float32 operands on 128x128 tiles (more than the 64 rows of the streamed kernel)
     if (a_dt == SSM_F32 && b_dt == SSM_F32) {
@@ -905,7 +883,7 @@ size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, Ge
     if (M <= 64 || N == 0 || b_dt != SSM_BF16 || a_dt != SSM_BF16 || K % 64 != 0) return 0;
     int64_t tiles;
     if (role == kGemmXProj && xproj_decode_skinny(M, N)) return 0;
-    if (dma_decode_tiles(M, N, K)) return 0;
+    if (decode_tiles(M, N, K) && role != kGemmXProj) return 0;
     if (role == kGemmXProj && N <= 256) tiles = (M + 63) / 64;
     else if (dma_big_tiles(M, N)) return 0;
     else tiles = ((M + 127) / 128) * ((N + 127) / 128);

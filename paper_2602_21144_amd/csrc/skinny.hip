@@ -566,6 +566,218 @@ hipError_t launch_epi(const SkinnyArgs& p, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// Decode projections of more rows (bf16, K a multiple of 64): a workgroup owns a TM x TN
+// output tile and its NW waves split K. Each wave streams its share of the tile's
+// activation and weight rows into a ring of RD stages in its own part of LDS on the DMA
+// path (buffer_load ... lds: whole lines, 8 rows x 128 bytes per instruction, no registers
+// held), waits for them with its own vmcnt and reads them back as
+// v_mfma_f32_16x16x32_bf16 fragments. No barrier sits inside the k loop, so each wave
+// keeps RD - 1 stages in flight on its own. (A 64 x 64 tile kernel that moves both
+// operands through a shared LDS ring with a barrier per 64-wide k-step fetched about 20
+// bytes per clock per CU; the CUs take about 64 from L2. Staging the stages through
+// registers instead lost most of the prefetch: the compiler's counter waits at the top of
+// the k loop assumed few loads in flight.) The waves' partial tiles are summed through LDS;
+// each thread then takes whole 8-column groups of the tile through the epilogue (plain
+// stores, or the conv window of in_proj, 16-byte accesses throughout).
+template <int TM, int TN, int NW, int RD, int EPI>
+__global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
+    constexpr int AB = TM / 8, BB = TN / 8;   // 8-row blocks of one stage
+    constexpr int OPS = AB + BB;              // DMA instructions per stage
+    constexpr int MT = TM / 16, NT = TN / 16;
+    constexpr int SLOT = OPS * 1024;          // one stage: activation rows, then weight rows
+    constexpr int RING = NW * RD * SLOT;
+    constexpr int RED = NW * TM * TN * 4;
+    constexpr int SMEM = RING > RED ? RING : RED;
+    constexpr int G = TM * TN / 8 / (NW * 64);  // epilogue groups per thread
+    static_assert(TM % 16 == 0 && TM <= 64 && TN % 16 == 0 && G >= 1 && G * NW * 64 * 8 == TM * TN, "tile");
+    static_assert(RD >= 2 && (RD - 1) * OPS < 64, "stages in flight within the vmcnt range");
+    __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+    // column tiles outer, row tiles inner: the row tiles of one column tile (which read
+    // the same weight rows) take consecutive indices, hence one XCD's L2
+    const int tiles_m = (p.M + TM - 1) / TM;
+    const int t = xcd_contiguous((int)blockIdx.x, (int)gridDim.x);
+    const int m0 = (t % tiles_m) * TM, n0 = (t / tiles_m) * TN;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+    // epilogue group k of this thread: tile row er[k], columns ec[k] .. ec[k] + 7
+    int er[G], ec[G], slot[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+        const int g = threadIdx.x + k * NW * 64;
+        er[k] = g / (TN / 8);
+        ec[k] = (g % (TN / 8)) * 8;
+        slot[k] = 0;
+        if constexpr (EPI == kEpiConv) slot[k] = p.slot[min(m0 + er[k], p.M - 1)];
+    }
+
+    const int nall = p.K / kGemvBK;
+    const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
+    // lane l of a DMA instruction lands at byte 16 l of its 1 KB block: row l / 8, stored
+    // chunk l % 8, which holds the row's chunk (l % 8) ^ ((row >> 1) & 7) (the swizzle the
+    // fragment reads undo). Rows past M or N lie outside the resources and land as zero.
+    const int lr = lane >> 3, lp = lane & 7;
+    const __amdgpu_buffer_rsrc_t ra =
+        buffer_rsrc((const bf16*)p.A + (int64_t)m0 * p.lda, (uint32_t)(min(TM, p.M - m0) * p.lda * 2));
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(min(TN, p.N - n0) * p.ldb * 2));
+    uint32_t aoff[AB], boff[BB];
+#pragma unroll
+    for (int q = 0; q < AB; ++q) {
+        const int r = 8 * q + lr;
+        aoff[q] = (uint32_t)(r * p.lda) * 2 + (uint32_t)(gemv_swz(r, lp) * 16 + sb * kGemvBK * 2);
+    }
+#pragma unroll
+    for (int q = 0; q < BB; ++q) {
+        const int r = 8 * q + lr;
+        boff[q] = (uint32_t)(r * p.ldb) * 2 + (uint32_t)(gemv_swz(r, lp) * 16 + sb * kGemvBK * 2);
+    }
+    const uint32_t ring = (uint32_t)(uintptr_t)(lds_ptr_t)(smem + wave * RD * SLOT);
+    // stage st of this wave's run into ring slot j; stages past the run read out of range
+    // (no memory touched), so every refill is OPS instructions and the counter waits are exact
+    auto stage_dma = [&](int st, int j) {
+        const bool ok = st < nst;
+        const uint32_t soff = __builtin_amdgcn_readfirstlane(ok ? (uint32_t)st * kGemvBK * 2 : 0u);  // wave-uniform
+        const uint32_t base = ring + (uint32_t)(j * SLOT);
+#pragma unroll
+        for (int q = 0; q < AB; ++q)
+            dma16(ra, ok ? aoff[q] : kOffOutOfRange, soff, __builtin_amdgcn_readfirstlane(base + q * 1024));
+#pragma unroll
+        for (int q = 0; q < BB; ++q)
+            dma16(rb, ok ? boff[q] : kOffOutOfRange, soff, __builtin_amdgcn_readfirstlane(base + (AB + q) * 1024));
+    };
+#pragma unroll
+    for (int j = 0; j < RD; ++j) stage_dma(j, j);
+
+    const int fr = lane & 15, cg = lane >> 4;
+    f32x4 acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int jn = 0; jn < NT; ++jn) acc[i][jn] = f32x4{};
+    for (int st = 0; st < nst; ++st) {
+        const int j = st % RD;
+        wait_vm<(RD - 1) * OPS>();  // stage st has landed; the RD - 1 after it may not have
+        const char* abuf = smem + (wave * RD + j) * SLOT;
+        const char* wbuf = abuf + AB * 1024;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const int c = 4 * s + cg;
+            bf16x8 af[MT];
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                af[i] = *(const bf16x8*)(abuf + (16 * i + fr) * 128 + gemv_swz(16 * i + fr, c) * 16);
+#pragma unroll
+            for (int jn = 0; jn < NT; ++jn) {
+                const bf16x8 wf = *(const bf16x8*)(wbuf + (16 * jn + fr) * 128 + gemv_swz(16 * jn + fr, c) * 16);
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf, acc[i][jn], 0, 0, 0);
+            }
+        }
+        wait_lgkm0();  // the slot's fragments are read before it is refilled
+        stage_dma(st + RD, j);
+    }
+    wait_vm<0>();  // every DMA (the out-of-range refills too) has landed before LDS is reused
+    // lane l holds column 16 jn + l % 16, rows 16 i + 4 (l / 16) + r of the tile
+    __syncthreads();
+    float* red = (float*)smem;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int jn = 0; jn < NT; ++jn)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[(wave * TM + 16 * i + 4 * cg + r) * TN + 16 * jn + fr] = acc[i][jn][r];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+        const int m = m0 + er[k], n = n0 + ec[k];
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const float* q = red + (w * TM + er[k]) * TN + ec[k];
+            const float4 a = *(const float4*)q, b = *(const float4*)(q + 4);
+            v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w; v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+        }
+        if (m >= p.M || n >= p.N) continue;
+        if constexpr (EPI == kEpiStoreF32) {
+            float* o = (float*)p.C + (int64_t)m * p.ldc + n;
+            *(float4*)o = make_float4(v[0], v[1], v[2], v[3]);
+            *(float4*)(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        } else {
+            bf16x8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
+            const int c = n - p.conv_lo;
+            if (EPI != kEpiConv || c < 0 || c >= p.conv_n) {
+                *(bf16x8*)((bf16*)p.C + (int64_t)m * p.ldc + n) = o;
+                continue;
+            }
+            if constexpr (EPI == kEpiConv) {
+                // the stored (rounded) projection outputs enter the window
+                float cur[8], out[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) cur[e] = (float)o[e];
+                const bool ok = slot_ok(slot[k], p.S);
+                bf16* hist = (bf16*)p.conv_pool + ((int64_t)(ok ? slot[k] : 0) * p.conv_n + c) * (p.Kc - 1);
+                const bf16* w = (const bf16*)p.conv_w + (int64_t)c * p.Kc;
+                const bf16* b = (const bf16*)p.conv_b + c;
+                switch (p.Kc) {
+                    case 2: conv_window_step8<bf16, 2>(cur, hist, ok, w, b, out); break;
+                    case 3: conv_window_step8<bf16, 3>(cur, hist, ok, w, b, out); break;
+                    default: conv_window_step8<bf16, 4>(cur, hist, ok, w, b, out); break;
+                }
+                if (!ok) atomicOr(p.status, SSM_STATUS_BAD_SLOT);
+                bf16x8 uo;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) uo[e] = (bf16)out[e];
+                *(bf16x8*)((bf16*)p.u + (int64_t)m * p.conv_n + c) = uo;
+            }
+        }
+    }
+}
+
+// the tile kernel's shapes: bf16 activations, K a multiple of 64, whole 8-column groups
+// (N, the row strides and the conv column range multiples of 8), 16-byte aligned operands
+bool dtile_fits(const SkinnyArgs& p, int epi) {
+    auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+    if (p.a_f32 || p.K % kGemvBK != 0 || p.N % 8 != 0 || p.lda % 8 != 0 || p.ldb % 8 != 0 || p.ldc % 8 != 0 ||
+        !al16(p.A) || !al16(p.B) || !al16(p.C))
+        return false;
+    if ((int64_t)64 * p.lda * 2 >= (int64_t)1 << 31 || (int64_t)64 * p.ldb * 2 >= (int64_t)1 << 31) return false;
+    if (epi == kEpiConv && (p.conv_lo % 8 != 0 || p.conv_n % 8 != 0 || p.Kc < 2 || p.Kc > 4 || !al16(p.u) ||
+                            !al16(p.conv_w) || !al16(p.conv_b) || !al16(p.conv_pool)))
+        return false;
+    return true;
+}
+
+template <int TM, int TN, int NW, int RD, int EPI>
+hipError_t launch_dtile(const SkinnyArgs& p, hipStream_t s) {
+    const int tiles = ((p.M + TM - 1) / TM) * ((p.N + TN - 1) / TN);
+    SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI>), dim3((unsigned)tiles), dim3(NW * 64), 0, s, p);
+    return hipGetLastError();
+}
+
+// 17..512 rows over outputs of at least 128 tiles: 64 x 64 tiles above 128 rows when they
+// give 128 workgroups, else 64 x 32 tiles (both 4 waves, one stage in flight per wave while
+// the other is multiplied), else 32 x 32 tiles of 2 waves with 3 stages in flight. Measured
+// with the weights coming from the MALL (rotated over copies, as in a decode step):
+// in_proj + conv window of the 2.8B quarter shard (2560 x 2560) at 256 rows 14.0 us (17.8
+// for 64 x 64 DMA tiles in two K-slices plus the conv kernel that added them) and at 128
+// rows 10.0 us; its out_proj (2560 x 1280) 7.7 and 5.8 us (8.9 and 15.3 on 64 x 64 DMA
+// tiles); the hybrid shard's in_proj + conv (7168 x 3584) at 64 rows 13.5 us (23.8 with L2-warm
+// weights on the 32-column kernel) and its out_proj (3584 x 3584) 9.5 us (17.9 on 16-column
+// tiles). hipErrorNotSupported when it does not apply.
+template <int EPI>
+hipError_t launch_dtile_pick(const SkinnyArgs& p, hipStream_t s) {
+    if (p.M <= 16 || p.M > 512 || !dtile_fits(p, EPI)) return hipErrorNotSupported;
+    const int64_t tm64 = (p.M + 63) / 64, tm32 = (p.M + 31) / 32, tn64 = (p.N + 63) / 64, tn32 = (p.N + 31) / 32;
+    if (p.M > 128 && tm64 * tn64 >= 128) return launch_dtile<64, 64, 4, 2, EPI>(p, s);
+    if (tm64 * tn32 >= 128) return launch_dtile<64, 32, 4, 2, EPI>(p, s);
+    if (tm32 * tn32 >= 128) return launch_dtile<32, 32, 2, 4, EPI>(p, s);
+    return hipErrorNotSupported;
+}
+
 // 32-column tiles for 17..64 bf16 rows when they still give at least 192 workgroups.
 // Measured at 64 rows: the 7168-wide in_proj (224 workgroups) 36.6 -> 24.3 us; with 80 or
 // 112 workgroups (2560 or 3584 columns) the 16-column tiles were faster.
@@ -735,6 +947,10 @@ hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s) {
 
 hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    if (epi == kSkinnyStoreBf16 || epi == kSkinnyConv) {
+        const hipError_t e = epi == kSkinnyConv ? launch_dtile_pick<kEpiConv>(p, s) : launch_dtile_pick<kEpiStoreBf16>(p, s);
+        if (e != hipErrorNotSupported) return e;
+    }
     if (use_skinny32(p)) {
         switch (epi) {
             case kSkinnyStoreBf16: return launch_skinny32<kEpiStoreBf16>(p, s);

@@ -34,25 +34,30 @@ def test_decode_batches_across_tile_limit(batch, init):
     _decode_batch_case(synth.LayerShape(320, 384, 16, 32, 4, 2, "bf16"), batch, init, 11)
 
 
-# the 2.8B quarter shard (1280 channels) above 64 sequences: in_proj and out_proj on 64x64
-# tiles without K-slices (160 tiles at 256 sequences), x_proj on 16-row tiles, dt_proj
-# fused into the state step
-@pytest.mark.parametrize("batch", [65, 130, 256])
+# the 2.8B quarter shard (1280 channels): in_proj (with the conv window in its epilogue)
+# and out_proj on the streamed tile kernel (32x32 tiles at 40 sequences, 64x32 at 65 and
+# 130, 64x64 at 256; ragged last row tiles), x_proj on 16-row tiles; dt_proj fused into the
+# state step above 64 sequences
+@pytest.mark.parametrize("batch", [40, 65, 130, 256])
 @pytest.mark.parametrize("init", ["baseline", "stress"])
 def test_decode_large_batch_quarter_shard(batch, init):
     _decode_batch_case(synth.LayerShape(2560, 5120, 16, 160, 4, 4, "bf16"), batch, init, 13,
                        state_tol=TOL["bf16"] if init == "stress" else None)
 
 
-# conv widths 2 and 3 above 64 sequences: the conv step adds in_proj's partials itself
+# conv widths 2 and 3 above 64 sequences, the window in in_proj's epilogue: on the 16- and
+# 64-row tile kernel (384 columns: too few tiles for the streamed tile kernel) and on the
+# streamed tile kernel (the quarter shard's 2560 columns)
 @pytest.mark.parametrize("d_conv", [2, 3])
-def test_decode_large_batch_conv_widths(d_conv):
-    _decode_batch_case(synth.LayerShape(320, 384, 16, 32, d_conv, 2, "bf16"), 100, "stress", 16,
-                       state_tol=TOL["bf16"])
+@pytest.mark.parametrize("shape", ["narrow", "quarter_shard"])
+def test_decode_large_batch_conv_widths(d_conv, shape):
+    sh = (synth.LayerShape(320, 384, 16, 32, d_conv, 2, "bf16") if shape == "narrow"
+          else synth.LayerShape(2560, 5120, 16, 160, d_conv, 4, "bf16"))
+    _decode_batch_case(sh, 100, "stress", 16, state_tol=TOL["bf16"])
 
 
-# wide shards: 17..64 sequences take the 32-column fragment kernel for in_proj, with the
-# conv window in its epilogue (3072 channels per shard: 6144 columns). Under the stress init
+# wide shards: 17..64 sequences take the streamed tile kernel (64x32 tiles) for in_proj,
+# with the conv window in its epilogue (3072 channels per shard: 6144 columns). Under the stress init
 # dt reaches a few units, and where the GPU's fp32 sum and the oracle's fp64 sum of a dt
 # round to neighbouring bf16 values, one bf16 step of dt (2^-7 |dt|) moves that channel's
 # state by up to about 2.4 * 2^-7 * sigmoid(v) |dt| / softplus(v) of the largest state
@@ -119,22 +124,33 @@ def _decode_batch_case(shape, batch, init, seed, state_tol=None):
         assert_close(host(conv[r]), cps[r], TOL[act], f"conv_pool shard {r}")
 
 
-def test_decode_bad_slot_is_flagged():
+# 3 sequences of a small layer (16-row kernels, the state step in dt_proj's epilogue) and
+# 70 of the 2.8B quarter shard (streamed tile kernel with the conv window in its epilogue,
+# the state-step kernel)
+@pytest.mark.parametrize("case", ["few_rows", "tiles"])
+def test_decode_bad_slot_is_flagged(case):
     """A slot outside the pool is flagged; the valid sequences advance exactly as alone."""
     from paper_2602_21144_amd import binding as B
-    shape = synth.LayerShape(64, 128, 16, 16, 4, 1, "bf16")
+    if case == "few_rows":
+        shape, batch, bad = synth.LayerShape(64, 128, 16, 16, 4, 1, "bf16"), 3, 1
+    else:
+        shape, batch, bad = synth.LayerShape(2560, 1280, 16, 160, 4, 1, "bf16"), 70, 37
     full = synth.make_layer(shape, 5)
     g = GpuLayer(shape, full)
-    S = 6
+    S = batch + 3
     rng = np.random.default_rng(1)
-    xt = synth.make_tokens(rng, 3, shape.d_model, "bf16")
+    xt = synth.make_tokens(rng, batch, shape.d_model, "bf16")
     conv, ssm = g.new_pools(S, poison=False)
     conv2, ssm2 = g.new_pools(S, poison=False)
-    y_bad = host(g.decode(xt, torch.tensor([2, 99, 4], dtype=torch.int32, device="cuda"), conv, ssm)[0])
+    slots = rng.permutation(S)[:batch].astype(np.int32)
+    bad_slots = slots.copy()
+    bad_slots[bad] = 99 + S
+    keep = [i for i in range(batch) if i != bad]
+    y_bad = host(g.decode(xt, torch.from_numpy(bad_slots).cuda(), conv, ssm)[0])
     assert B.take_status(g._dws[0]) & B.SSM_STATUS_BAD_SLOT
-    y_ok = host(g.decode(xt[[0, 2]], torch.tensor([2, 4], dtype=torch.int32, device="cuda"), conv2, ssm2)[0])
+    y_ok = host(g.decode(xt[keep], torch.from_numpy(slots[keep]).cuda(), conv2, ssm2)[0])
     assert B.take_status(g._dws[0]) == 0
-    np.testing.assert_array_equal(y_bad[[0, 2]], y_ok)
+    np.testing.assert_array_equal(y_bad[keep], y_ok)
     assert torch.equal(ssm[0], ssm2[0]) and torch.equal(conv[0], conv2[0])
 
 

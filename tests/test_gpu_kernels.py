@@ -42,8 +42,12 @@ GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 9
                # 17..64 rows over at least 192 tiles of 32 columns (32-column fragment kernel: 32- and
                # 64-row tiles, ragged N, a K tail of 8)
                (17, 6150, 512), (40, 6176, 808), (64, 7168, 1024),
-               # decode batches of 65..512 rows over at least 128 tiles of 64x64, unsplit (ragged M and N)
-               (256, 2560, 2560), (130, 8192, 1280), (500, 1100, 640),
+               # decode batches of 17..512 rows, bf16 output, at least 128 tiles: the streamed tile
+               # kernel (64x64 tiles above 128 rows, 64x32, 32x32; ragged last row and column tiles,
+               # waves without a stage at K = 64); other outputs on the DMA tiles
+               (256, 2560, 2560), (130, 8192, 1280), (500, 1100, 640), (17, 4104, 64), (33, 4096, 1344),
+               (100, 4104, 2560), (129, 2560, 1280), (200, 4104, 3584), (511, 2568, 640), (40, 2560, 640),
+               (60, 3584, 3584),
                # float32 at prefill sizes: 128x128 tiles (ragged M and N, K of 96 to 3584)
                (2000, 3588, 224), (1500, 4100, 96), (2048, 7168, 3584)]
 
