@@ -113,39 +113,45 @@ template <typename T, int n> __device__ __forceinline__ void store16(T* p, const
 // One decode step of the cached convolution window (Section IV-A: the conv half of the
 // cache) for 8 consecutive channels c0..c0+7 of one sequence: out = SiLU(b + sum_j w[j] *
 // window), with cur (the new input, already in the activation dtype) as the newest tap,
-// then the history [8][K-1] (oldest first) shifted by one with cur appended. The history (8 (K-1) elements), the weights [8][K] and the
-// bias are contiguous 16-byte multiples at 16-byte aligned addresses (c0 % 8 == 0), so
-// each is read and written in whole 16-byte pieces. hist_ok false: the slot was bad;
-// nothing is written to the history and out is zero.
-template <typename T, int K>
-__device__ __forceinline__ void conv_window_step8(const float (&cur)[8], T* hist, bool hist_ok, const T* w,
-                                                  const T* b, float (&out)[8]) {
-    T wv[8 * K], bv[8];
-    load16(w, wv);
-    load16(b, bv);
-    if constexpr (K > 1) {
-        T hv[8 * (K - 1)];
-        load16(hist, hv);
+// then the history [8][K-1] (oldest first) shifted by one with cur appended. The history
+// (8 (K-1) elements), the weights [8][K] and the bias are contiguous 16-byte multiples at
+// 16-byte aligned addresses (c0 % 8 == 0), so each is read and written in whole 16-byte
+// pieces. load() fetches them; step() computes and writes the new history (ok false: the
+// slot was bad, nothing is written and out is zero).
+template <typename T, int K> struct ConvWindow8 {
+    T wv[8 * K], bv[8], hv[K > 1 ? 8 * (K - 1) : 8];
+    __device__ __forceinline__ void load(const T* hist, const T* w, const T* b) {
+        load16(w, wv);
+        load16(b, bv);
+        if constexpr (K > 1) load16(hist, hv);
+    }
+    __device__ __forceinline__ void step(const float (&cur)[8], T* hist, bool ok, float (&out)[8]) const {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             float acc = to_f32(bv[i]);
 #pragma unroll
             for (int j = 0; j < K - 1; ++j) acc += to_f32(wv[i * K + j]) * to_f32(hv[i * (K - 1) + j]);
             acc += to_f32(wv[i * K + K - 1]) * cur[i];
-            out[i] = hist_ok ? silu_f(acc) : 0.0f;
+            out[i] = ok ? silu_f(acc) : 0.0f;
         }
-        T nh[8 * (K - 1)];
+        if constexpr (K > 1) {
+            T nh[8 * (K - 1)];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+            for (int i = 0; i < 8; ++i) {
 #pragma unroll
-            for (int j = 0; j + 1 < K - 1; ++j) nh[i * (K - 1) + j] = hv[i * (K - 1) + j + 1];
-            nh[i * (K - 1) + K - 2] = from_f32<T>(cur[i]);
+                for (int j = 0; j + 1 < K - 1; ++j) nh[i * (K - 1) + j] = hv[i * (K - 1) + j + 1];
+                nh[i * (K - 1) + K - 2] = from_f32<T>(cur[i]);
+            }
+            if (ok) store16(hist, nh);
         }
-        if (hist_ok) store16(hist, nh);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) out[i] = hist_ok ? silu_f(to_f32(bv[i]) + to_f32(wv[i]) * cur[i]) : 0.0f;
     }
+};
+template <typename T, int K>
+__device__ __forceinline__ void conv_window_step8(const float (&cur)[8], T* hist, bool hist_ok, const T* w,
+                                                  const T* b, float (&out)[8]) {
+    ConvWindow8<T, K> cw;
+    cw.load(hist, w, b);
+    cw.step(cur, hist, hist_ok, out);
 }
 
 // Workspace header: status word at offset 0; regions start 256-byte aligned.

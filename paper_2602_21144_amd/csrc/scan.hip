@@ -403,24 +403,28 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
 // serves the 4 sequences of one workgroup instead of being fetched per sequence, and each
 // wave's states are one sequence's 16 channels, 1 KB contiguous per load instruction (with
 // 8 x 8 tiles, two 512-byte runs per instruction, the step took 15.7 instead of 10 us).
-constexpr int kDtCh = 16, kDtSeq = 4;
+constexpr int kDtCh = 16, kDtSeq = 4;  // tiles of the fp32 / general state-step kernel
+constexpr int kDtSeqM = 16;            // sequences per tile of the bf16 MFMA state-step kernel
 
-// bf16 and dt_rank a multiple of 32: the workgroup's 4 x 16 tile of dt is one small
-// product, delta[4 sequences][R] x W_dt[16 channels][R]^T, which wave 0 takes on
-// v_mfma_f32_16x16x32_bf16 (operand rows past the 4 sequences zero; R / 32 MFMAs), rounds
-// to bf16 and hands to the other waves through LDS; the W_dt rows are fetched once per 4
-// sequences. Measured on 256 sequences of 1280 channels: 14.5 us, against 10 us for the
-// state step alone plus ~9.5 us for a separate dt_proj. (Per-lane dot products made each
-// lane fetch 240 bytes of delta and W, mostly repeats of its neighbours': 20 us; per-wave
-// products without the barrier: 21 us; wave 0 issuing its operands ahead of its state,
-// which keeps them live across the state load and costs occupancy: 20 us.)
+// bf16 and dt_rank a multiple of 32 (up to 512): a workgroup of 16 waves takes 16
+// channels of 16 sequences, wave w sequence w (its 16 channels' states are 1 KB
+// contiguous per load instruction, four lanes per channel). The workgroup's 16 x 16 tile
+// of dt is the product delta[16 sequences][R] x W_dt[16 channels][R]^T: its R / 32
+// k-chunks go to waves 0 .. R/32 - 1, one v_mfma_f32_16x16x32_bf16 each, whose partial
+// tiles meet in LDS; every thread adds the partials of its (sequence, channel) in chunk
+// order and rounds dt to bf16 as dt_proj stores it. Each workgroup fetches its 16 delta
+// rows and 16 W_dt rows once: 15 KB per 16 x 16 items. (4 x 16 tiles fetched the W_dt
+// rows once per 4 sequences, about as many L2 bytes as the states themselves, and took
+// 15.5 us for 256 sequences of 1280 channels; per-lane dot products made each lane fetch
+// 240 bytes of delta and W, mostly repeats of its neighbours'.)
 template <int NK>
-__global__ __launch_bounds__(256) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
-    __shared__ float dt_tile[kDtSeq][kDtCh];
+__global__ __launch_bounds__(1024) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
+    __shared__ float dt_part[NK][kDtSeqM][kDtCh];
     const int ctiles = a.E / kDtCh;
     const int tb = blockIdx.x / ctiles, tc = blockIdx.x % ctiles;
-    const int it = threadIdx.x >> 2, q = threadIdx.x & 3;
-    const int bb = tb * kDtSeq + it / kDtCh, cc = tc * kDtCh + it % kDtCh;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int it = lane >> 2, q = lane & 3;  // channel tc * 16 + it of sequence tb * 16 + wave
+    const int bb = tb * kDtSeqM + wave, cc = tc * kDtCh + it;
     const bool live = bb < a.nseq;
     const int b = live ? bb : 0, c = cc;
     const int slot = a.slot[b];
@@ -433,39 +437,30 @@ __global__ __launch_bounds__(256) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
     const bool slot_ok = slot >= 0 && slot < a.S;
     float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
     const float4 h = *hp;
-    if (threadIdx.x < 64) {
-        // lane l: W_dt row l % 16 and, for l % 16 below the tile's sequences, that
-        // sequence's delta (other rows zero), columns 32 k + 8 (l / 16) .. + 7
-        const int lane = threadIdx.x, r = lane & 15, kq = (lane >> 4) * 8;
-        const int sr = tb * kDtSeq + (r % kDtSeq);
-        const bool rok = r < kDtSeq && sr < a.nseq;
+    if (wave < NK) {
+        // chunk k = wave: lane l takes delta row l % 16 (rows past the batch zero) and W_dt
+        // row l % 16, columns 32 k + 8 (l / 16) .. + 7
+        const int r = lane & 15, kq = (lane >> 4) * 8, k0 = 32 * wave + kq;
+        const int sr = tb * kDtSeqM + r;
+        const bool rok = sr < a.nseq;
         const float* drow = a.xdbl + (int64_t)(rok ? sr : 0) * a.ld_xdbl;
         const bf16* wrow = (const bf16*)a.w_dt + (int64_t)(tc * kDtCh + r) * a.R;
-        float4 d0[NK], d1[NK];
-        bf16x8 wf[NK];
+        const float4 d0 = *(const float4*)(drow + k0), d1 = *(const float4*)(drow + k0 + 4);
+        const bf16x8 wf = *(const bf16x8*)(wrow + k0);
+        bf16x8 af;
+        af[0] = (bf16)d0.x; af[1] = (bf16)d0.y; af[2] = (bf16)d0.z; af[3] = (bf16)d0.w;
+        af[4] = (bf16)d1.x; af[5] = (bf16)d1.y; af[6] = (bf16)d1.z; af[7] = (bf16)d1.w;
+        if (!rok) af = bf16x8{};
+        const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf, f32x4{}, 0, 0, 0);
+        // lane l holds sequences 4 (l / 16) + j of the tile, channel l % 16
 #pragma unroll
-        for (int k = 0; k < NK; ++k) {
-            d0[k] = *(const float4*)(drow + 32 * k + kq);
-            d1[k] = *(const float4*)(drow + 32 * k + kq + 4);
-            wf[k] = *(const bf16x8*)(wrow + 32 * k + kq);
-        }
-        f32x4 acc = f32x4{};
-#pragma unroll
-        for (int k = 0; k < NK; ++k) {
-            bf16x8 af;
-            af[0] = (bf16)d0[k].x; af[1] = (bf16)d0[k].y; af[2] = (bf16)d0[k].z; af[3] = (bf16)d0[k].w;
-            af[4] = (bf16)d1[k].x; af[5] = (bf16)d1[k].y; af[6] = (bf16)d1[k].z; af[7] = (bf16)d1[k].w;
-            if (!rok) af = bf16x8{};
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[k], acc, 0, 0, 0);
-        }
-        // lane l holds sequences 4 (l / 16) + j, channel l % 16: rows 0..3 in lanes 0..15
-        if (lane < 16) {
-#pragma unroll
-            for (int j = 0; j < kDtSeq; ++j) dt_tile[j][r] = (float)(bf16)acc[j];  // dt stored in bf16
-        }
+        for (int j = 0; j < 4; ++j) dt_part[wave][4 * (lane >> 4) + j][r] = acc[j];
     }
     __syncthreads();
-    const float dt = dt_tile[it / kDtCh][it % kDtCh];
+    float dsum = dt_part[0][wave][it];
+#pragma unroll
+    for (int k = 1; k < NK; ++k) dsum += dt_part[k][wave][it];
+    const float dt = (float)(bf16)dsum;  // stored in bf16 as dt_proj's output
     const float delta = softplus_f(dt + bdt);
     const float du = delta * u;
     const float hv[4] = {h.x, h.y, h.z, h.w}, av[4] = {al.x, al.y, al.z, al.w};
@@ -667,20 +662,18 @@ hipError_t launch_decode_dt_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
     if (a.R % 8 != 0 || a.E % kDtCh != 0 || a.ld_xdbl % 4 != 0 || ((uintptr_t)a.xdbl & 15) != 0 ||
         ((uintptr_t)a.w_dt & 15) != 0)
         return hipErrorNotSupported;
-    const dim3 grid((unsigned)(((a.nseq + kDtSeq - 1) / kDtSeq) * (a.E / kDtCh))), block(256);
-    if (bf && a.R % 32 == 0 && a.R <= 256) {
+    if (bf && a.R % 32 == 0 && a.R <= 16 * 32) {
+        const dim3 g16((unsigned)(((a.nseq + kDtSeqM - 1) / kDtSeqM) * (a.E / kDtCh))), b16(1024);
         switch (a.R / 32) {
-            case 1: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<1>, grid, block, 0, s, a); break;
-            case 2: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<2>, grid, block, 0, s, a); break;
-            case 3: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<3>, grid, block, 0, s, a); break;
-            case 4: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<4>, grid, block, 0, s, a); break;
-            case 5: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<5>, grid, block, 0, s, a); break;
-            case 6: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<6>, grid, block, 0, s, a); break;
-            case 7: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<7>, grid, block, 0, s, a); break;
-            default: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<8>, grid, block, 0, s, a); break;
+#define SSM_DTM(NK) case NK: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<NK>, g16, b16, 0, s, a); break;
+            SSM_DTM(1) SSM_DTM(2) SSM_DTM(3) SSM_DTM(4) SSM_DTM(5) SSM_DTM(6) SSM_DTM(7) SSM_DTM(8)
+            SSM_DTM(9) SSM_DTM(10) SSM_DTM(11) SSM_DTM(12) SSM_DTM(13) SSM_DTM(14) SSM_DTM(15)
+            default: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<16>, g16, b16, 0, s, a); break;
+#undef SSM_DTM
         }
         return hipGetLastError();
     }
+    const dim3 grid((unsigned)(((a.nseq + kDtSeq - 1) / kDtSeq) * (a.E / kDtCh))), block(256);
     // chunks of 8 columns per lane: ceil(R / 32), R up to 256
     const int nch = (a.R / 8 + 3) / 4;
 #define SSM_DTSSM(NC)                                                                            \

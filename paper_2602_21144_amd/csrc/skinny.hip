@@ -579,7 +579,7 @@ hipError_t launch_epi(const SkinnyArgs& p, hipStream_t s) {
 // the k loop assumed few loads in flight.) The waves' partial tiles are summed through LDS;
 // each thread then takes whole 8-column groups of the tile through the epilogue (plain
 // stores, or the conv window of in_proj, 16-byte accesses throughout).
-template <int TM, int TN, int NW, int RD, int EPI>
+template <int TM, int TN, int NW, int RD, int EPI, int KC>
 __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
     constexpr int AB = TM / 8, BB = TN / 8;   // 8-row blocks of one stage
     constexpr int OPS = AB + BB;              // DMA instructions per stage
@@ -677,6 +677,21 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
         stage_dma(st + RD, j);
     }
     wait_vm<0>();  // every DMA (the out-of-range refills too) has landed before LDS is reused
+    // the conv window operands of the epilogue groups (conv width KC) go out now, so they
+    // arrive while the waves' partial tiles are summed
+    constexpr int KW = EPI == kEpiConv ? KC : 2;
+    ConvWindow8<bf16, KW> cw[G];
+    bool inconv[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+        const int m = m0 + er[k], c = n0 + ec[k] - p.conv_lo;
+        inconv[k] = EPI == kEpiConv && m < p.M && c >= 0 && c < p.conv_n;
+        if (inconv[k]) {
+            const int sc = slot_ok(slot[k], p.S) ? slot[k] : 0;
+            cw[k].load((const bf16*)p.conv_pool + ((int64_t)sc * p.conv_n + c) * (KW - 1),
+                       (const bf16*)p.conv_w + (int64_t)c * KW, (const bf16*)p.conv_b + c);
+        }
+    }
     // lane l holds column 16 jn + l % 16, rows 16 i + 4 (l / 16) + r of the tile
     __syncthreads();
     float* red = (float*)smem;
@@ -709,7 +724,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) o[e] = (bf16)v[e];
             const int c = n - p.conv_lo;
-            if (EPI != kEpiConv || c < 0 || c >= p.conv_n) {
+            if (!inconv[k]) {
                 *(bf16x8*)((bf16*)p.C + (int64_t)m * p.ldc + n) = o;
                 continue;
             }
@@ -719,14 +734,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) cur[e] = (float)o[e];
                 const bool ok = slot_ok(slot[k], p.S);
-                bf16* hist = (bf16*)p.conv_pool + ((int64_t)(ok ? slot[k] : 0) * p.conv_n + c) * (p.Kc - 1);
-                const bf16* w = (const bf16*)p.conv_w + (int64_t)c * p.Kc;
-                const bf16* b = (const bf16*)p.conv_b + c;
-                switch (p.Kc) {
-                    case 2: conv_window_step8<bf16, 2>(cur, hist, ok, w, b, out); break;
-                    case 3: conv_window_step8<bf16, 3>(cur, hist, ok, w, b, out); break;
-                    default: conv_window_step8<bf16, 4>(cur, hist, ok, w, b, out); break;
-                }
+                cw[k].step(cur, (bf16*)p.conv_pool + ((int64_t)slot[k] * p.conv_n + c) * (KW - 1), ok, out);
                 if (!ok) atomicOr(p.status, SSM_STATUS_BAD_SLOT);
                 bf16x8 uo;
 #pragma unroll
@@ -753,8 +761,16 @@ bool dtile_fits(const SkinnyArgs& p, int epi) {
 
 template <int TM, int TN, int NW, int RD, int EPI>
 hipError_t launch_dtile(const SkinnyArgs& p, hipStream_t s) {
-    const int tiles = ((p.M + TM - 1) / TM) * ((p.N + TN - 1) / TN);
-    SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI>), dim3((unsigned)tiles), dim3(NW * 64), 0, s, p);
+    const dim3 grid((unsigned)(((p.M + TM - 1) / TM) * ((p.N + TN - 1) / TN))), block(NW * 64);
+    if constexpr (EPI == kEpiConv) {
+        switch (p.Kc) {
+            case 2: SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI, 2>), grid, block, 0, s, p); break;
+            case 3: SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI, 3>), grid, block, 0, s, p); break;
+            default: SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI, 4>), grid, block, 0, s, p); break;
+        }
+    } else {
+        SSM_LAUNCH((gemm_dtile_kernel<TM, TN, NW, RD, EPI, 0>), grid, block, 0, s, p);
+    }
     return hipGetLastError();
 }
 
