@@ -682,59 +682,72 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const fl
     }
 }
 
-// fp32 operands at prefill sizes: 128x128 tiles, four waves of 64x64 (4x4 tiles of
-// v_mfma_f32_16x16x4_f32), 32-wide k stages (one 128-byte line of every operand row).
-// Each stage moves global -> registers -> LDS in whole lines (8 threads per row), one
-// stage ahead of the MFMAs, into a double-buffered LDS ring (2 x 32 KB) with one barrier
-// per stage. Fragments are read as float4 along k: lane l takes chunk 4 g + l / 16 of row
-// l % 16 and MFMA u of group g uses component u, the same k for both operands. LDS rows
-// are XOR-swizzled in 16-byte chunks (chunk ^ ((row / 2) % 8)), which keeps both the
-// whole-row writes and the 16-row fragment reads free of bank conflicts. The weight
-// fragment is the MFMA's first operand, so a lane ends up with four consecutive output
-// columns of one row: float4 stores. Rows and columns past M, N read as zero.
+// fp32 operands at prefill sizes: BM x BN tiles of WM x WN waves, each wave a
+// (BM / WM) x (BN / WN) block of 16x16 tiles of v_mfma_f32_16x16x4_f32, 32-wide k stages
+// (one 128-byte line of every operand row). Each stage moves global -> registers -> LDS in
+// whole lines (8 threads per row), one stage ahead of the MFMAs, into a double-buffered
+// LDS ring with one barrier per stage. Fragments are read as float4 along k: lane l takes
+// chunk 4 g + l / 16 of row l % 16 and MFMA u of group g uses component u, the same k for
+// both operands. LDS rows are XOR-swizzled in 16-byte chunks (chunk ^ ((row / 2) % 8)),
+// which keeps both the whole-row writes and the 16-row fragment reads free of bank
+// conflicts. The weight fragment is the MFMA's first operand, so a lane ends up with four
+// consecutive output columns of one row: float4 stores. Rows and columns past M, N read as
+// zero. Two waves per SIMD or more keep the MFMA pipe fed across each stage's barrier and
+// LDS reads: on the hybrid shard's 2048-row chunks (random operands) 128x128 tiles of 8
+// waves took out_proj (3584 x 3584) from 443-468 to 428-431 us against 4 waves, and 256x256
+// tiles of 16 waves in_proj (7168 x 3584) from 880-980 to 832-839 us.
 constexpr int kF32BK = 32;
 
 __device__ __forceinline__ int f32_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int ROLE>
-__global__ __launch_bounds__(256) void gemm_f32_big(int M, int N, int K, const float* __restrict__ A, int64_t lda,
-                                                    const float* __restrict__ B, int64_t ldb, float* __restrict__ C,
-                                                    int64_t ldc, int tiles_m, int tiles_n, float* __restrict__ part) {
-    constexpr int BM = 128, BN = 128, TILE = 128 * 128;  // bytes of one operand tile per stage
-    __shared__ __attribute__((aligned(16))) char lds[2][2 * TILE];
+template <int ROLE, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_f32_big(int M, int N, int K, const float* __restrict__ A,
+                                                             int64_t lda, const float* __restrict__ B, int64_t ldb,
+                                                             float* __restrict__ C, int64_t ldc, int tiles_m,
+                                                             int tiles_n, float* __restrict__ part) {
+    constexpr int NT = 64 * WM * WN;            // threads
+    constexpr int TI = BM / WM / 16, TJ = BN / WN / 16;
+    constexpr int SA = BM * 128, SB = BN * 128; // bytes of each operand's stage
+    constexpr int RS = NT / 8;                  // rows one pass of all threads moves
+    constexpr int CA = BM / RS, CB = BN / RS;   // 16-byte chunks per thread per stage
+    static_assert(CA * RS == BM && CB * RS == BN && TI >= 1 && TJ >= 1, "tile");
+    __shared__ __attribute__((aligned(16))) char lds[2][SA + SB];
     int tm, tn;
     tile_of(tiles_m, tiles_n, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 4));
     const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 4));
-    // loads of one stage: thread t moves chunk t % 8 of rows t / 8 + 32 i of each operand
+    // loads of one stage: thread t moves chunk t % 8 of rows t / 8 + RS i of each operand
     const int lrow = tid >> 3, lck = tid & 7;
-    u32x4 va[4], vb[4];
+    u32x4 va[CA], vb[CB];
     auto gload = [&](int st) {
         const uint32_t kb = (uint32_t)(st * kF32BK + lck * 4) * 4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            va[i] = buffer_load16(ra, (uint32_t)((lrow + 32 * i) * lda) * 4 + kb);
-            vb[i] = buffer_load16(rb, (uint32_t)((lrow + 32 * i) * ldb) * 4 + kb);
-        }
+        for (int i = 0; i < CA; ++i) va[i] = buffer_load16(ra, (uint32_t)((lrow + RS * i) * lda) * 4 + kb);
+#pragma unroll
+        for (int i = 0; i < CB; ++i) vb[i] = buffer_load16(rb, (uint32_t)((lrow + RS * i) * ldb) * 4 + kb);
     };
     auto lstore = [&](int buf) {
         char* a = lds[buf];
-        char* b = lds[buf] + TILE;
+        char* b = lds[buf] + SA;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = lrow + 32 * i;
+        for (int i = 0; i < CA; ++i) {
+            const int r = lrow + RS * i;
             *(u32x4*)(a + r * 128 + f32_swz(r, lck) * 16) = va[i];
+        }
+#pragma unroll
+        for (int i = 0; i < CB; ++i) {
+            const int r = lrow + RS * i;
             *(u32x4*)(b + r * 128 + f32_swz(r, lck) * 16) = vb[i];
         }
     };
-    f32x4 acc[4][4];  // [weight tile j][activation tile i]
+    f32x4 acc[TJ][TI];  // [weight tile j][activation tile i]
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{};
+        for (int i = 0; i < TI; ++i) acc[j][i] = f32x4{};
     // split-K: workgroup row blockIdx.y takes K-slice [s0, s0 + nst) of gridDim.y equal slices
     // and writes its fp32 partial tile to part[blockIdx.y] (row stride N)
     const int nst = K / kF32BK / gridDim.y, s0 = blockIdx.y * nst;
@@ -750,27 +763,27 @@ __global__ __launch_bounds__(256) void gemm_f32_big(int M, int N, int K, const f
         const int cur = st & 1;
         if (st + 1 < nst) gload(s0 + st + 1);
         const char* a = lds[cur];
-        const char* b = lds[cur] + TILE;
+        const char* b = lds[cur] + SA;
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
             const int c = 4 * g + cg;
-            f32x4 af[4], bfr[4];
+            f32x4 af[TI], bfr[TJ];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = wm * 64 + 16 * i + fr;
+            for (int i = 0; i < TI; ++i) {
+                const int r = wm * (BM / WM) + 16 * i + fr;
                 af[i] = *(const f32x4*)(a + r * 128 + f32_swz(r, c) * 16);
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = wn * 64 + 16 * j + fr;
+            for (int j = 0; j < TJ; ++j) {
+                const int r = wn * (BN / WN) + 16 * j + fr;
                 bfr[j] = *(const f32x4*)(b + r * 128 + f32_swz(r, c) * 16);
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < TJ; ++j)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
+                    for (int i = 0; i < TI; ++i)
                         acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(bfr[j][u], af[i][u], acc[j][i], 0, 0, 0);
         }
         if (st + 1 < nst) lstore(cur ^ 1);
@@ -778,12 +791,12 @@ __global__ __launch_bounds__(256) void gemm_f32_big(int M, int N, int K, const f
     }
     // lane l holds activation row l % 16 and weight columns 4 (l / 16) + v of each tile pair
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = m0 + wm * 64 + 16 * i + fr;
+    for (int i = 0; i < TI; ++i) {
+        const int m = m0 + wm * (BM / WM) + 16 * i + fr;
         if (m >= M) continue;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + wn * 64 + 16 * j + 4 * cg;
+        for (int j = 0; j < TJ; ++j) {
+            const int n = n0 + wn * (BN / WN) + 16 * j + 4 * cg;
             float* p = C + (int64_t)m * ldc + n;
             if (n + 3 < N && (ldc & 3) == 0) {
                 *(float4*)p = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
@@ -921,18 +934,39 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
             return hipGetLastError();
         }
         // prefill sizes: 128x128 tiles when they give a few rounds of workgroups, or when the
-        // product can be cut into K-slices to get there (x_proj: 32 tiles)
+        // product can be cut into K-slices to get there (x_proj: 32 tiles); 256x256 tiles of 16
+        // waves when those still give about a round
         {
             const int64_t tm2 = (M + 127) / 128, tn2 = (N + 127) / 128;
             const int sp = fit_slices(f32_slices(tm2 * tn2, K), M, N, scratch_bytes);
+            const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+            const bool big = t256 >= 192 && sp <= 1;
+            const int64_t rows = big ? 256 : 128;
             if (K % kF32BK == 0 && (tm2 * tn2 >= 256 || sp > 1) && lda % 4 == 0 && ldb % 4 == 0 && al16(A) &&
-                al16(B) && al16(C) && 128 * lda * 4 < ((int64_t)1 << 31) && 128 * ldb * 4 < ((int64_t)1 << 31)) {
-                const dim3 grid((unsigned)(tm2 * tn2), (unsigned)sp);
+                al16(B) && al16(C) && rows * lda * 4 < ((int64_t)1 << 31) && rows * ldb * 4 < ((int64_t)1 << 31)) {
                 float* part = sp > 1 ? scratch : nullptr;
+                if (big) {
+                    const int tm4 = (int)((M + 255) / 256), tn4 = (int)((N + 255) / 256);
 #define SSM_F32_BIG(R)                                                                                          \
     case R:                                                                                                     \
-        SSM_LAUNCH(gemm_f32_big<R>, grid, dim3(256), 0, s, (int)M, (int)N, (int)K, (const float*)A, lda,       \
-                   (const float*)B, ldb, (float*)C, ldc, (int)tm2, (int)tn2, part);                             \
+        SSM_LAUNCH((gemm_f32_big<R, 256, 256, 4, 4>), dim3((unsigned)(tm4 * tn4)), dim3(1024), 0, s, (int)M,   \
+                   (int)N, (int)K, (const float*)A, lda, (const float*)B, ldb, (float*)C, ldc, tm4, tn4, part);  \
+        break;
+                    switch (role) {
+                        SSM_F32_BIG(kGemmInProj)
+                        SSM_F32_BIG(kGemmXProj)
+                        SSM_F32_BIG(kGemmDtProj)
+                        SSM_F32_BIG(kGemmOutProj)
+                        default: SSM_F32_BIG(kGemmGeneric)
+                    }
+#undef SSM_F32_BIG
+                    return hipGetLastError();
+                }
+                const dim3 grid((unsigned)(tm2 * tn2), (unsigned)sp);
+#define SSM_F32_BIG(R)                                                                                          \
+    case R:                                                                                                     \
+        SSM_LAUNCH((gemm_f32_big<R, 128, 128, 2, 4>), grid, dim3(512), 0, s, (int)M, (int)N, (int)K,            \
+                   (const float*)A, lda, (const float*)B, ldb, (float*)C, ldc, (int)tm2, (int)tn2, part);       \
         break;
                 switch (role) {
                     SSM_F32_BIG(kGemmInProj)
