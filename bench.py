@@ -308,29 +308,38 @@ class Workload:
         return out
 
 
+def launches_per_step(wl):
+    """Launches of each kernel name in one step: the roles of kernel_work, and the scan's
+    three passes once per prefill call."""
+    n = {role: len(amts) for role, (roof, amts) in wl.work_by_role().items()}
+    if "prefill.scan" in n:
+        for p in ("prefill.scan_local", "prefill.scan_link", "prefill.scan_main"):
+            n[p] = n["prefill.scan"]
+    return n
+
+
 def measure(B, torch, wl, steps, warmup, dominant_every=None):
-    """Warm-up steps, one step with every kernel timed (the per-kernel breakdown; the host
-    drains the stream before each launch), then the
-    timed steps with events at every phase boundary and the dominant kernel's dispatches
-    timed by their own events (every launch if it runs 200 us or more, else every 16th)."""
+    """Warm-up steps; one breakdown step with every 16th launch of each kernel name timed (the
+    first included) by events bound to its own dispatch; then the timed steps with events at
+    every phase boundary and the dominant kernel's dispatches timed by their own events (every
+    launch if it runs 200 us or more, else every 16th). A dispatch's events read its execution
+    plus any time the GPU waits for it (for the host to submit it, or for work queued ahead of
+    it); sampling few launches keeps the host ahead of the GPU, so that wait stays small."""
     import numpy as np
     for _ in range(max(warmup, 1)):
         wl.step()
     torch.cuda.synchronize()
-    # the breakdown step drains the stream before each timed launch: a dispatch queued
-    # behind unfinished work reads part of its wait in the queue as its own duration
     B.ssm_timing_collect()
-    B.ssm_timing_enable(True)
-    B.ssm_timing_serialize(True)
-    for cs in wl.calls:
-        for c in cs:
-            c()
+    B.ssm_timing_enable(True, None, every=16)
+    wl.step()
     torch.cuda.synchronize()
-    B.ssm_timing_serialize(False)
     B.ssm_timing_enable(False)
-    breakdown = B.ssm_timing_collect()
-    dominant = max(breakdown, key=lambda n: breakdown[n][1])
-    dom_avg_ms = breakdown[dominant][1] / breakdown[dominant][0]
+    sampled = B.ssm_timing_collect()
+    per_step = launches_per_step(wl)
+    # per kernel name: (launches per step, average ms of its sampled launches)
+    breakdown = {k: (per_step.get(k, n), ms / n) for k, (n, ms) in sampled.items()}
+    dominant = max(breakdown, key=lambda k: breakdown[k][0] * breakdown[k][1])
+    dom_avg_ms = breakdown[dominant][1]
     every = dominant_every or (1 if dom_avg_ms >= 0.2 else 16)
     B.ssm_timing_enable(True, dominant, every=every)
     nph = len(wl.phases)
@@ -366,20 +375,21 @@ def measure(B, torch, wl, steps, warmup, dominant_every=None):
 
 
 def kernel_figures(wl, m):
-    """Per-kernel (and per-role) figures from the breakdown step: launches, average time,
-    share of the step, roof, achieved rate and fraction of the roof's peak."""
+    """Per-kernel (and per-role) figures from the breakdown step: launches per step, average
+    time of the sampled launches, estimated share of the step, roof, achieved rate (work of
+    the sampled launches over their time) and fraction of the roof's peak."""
     sh = wl.sh
     bd = m["breakdown"]
-    total = sum(v[1] for v in bd.values())
+    total = sum(n * ms for n, ms in bd.values())
     mf_peak = PEAK_TFLOPS[sh.act]
     out = {}
-    for name, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][1]):
-        e = {"launches": n, "avg_us": round(1e3 * ms / n, 3), "share_of_step": round(ms / total, 4)}
+    for name, (n, ms) in sorted(bd.items(), key=lambda kv: -kv[1][0] * kv[1][1]):
+        e = {"launches": n, "avg_us": round(1e3 * ms, 3), "share_of_step": round(n * ms / total, 4)}
         role = role_of(name)
         if role in m["work"] and role == name:
             roof, amts = m["work"][role]
-            amt = sum(amts)
-            rate = amt / (ms * 1e-3)
+            sampled = amts[::16]
+            rate = (sum(sampled) / len(sampled)) / (ms * 1e-3)
             if roof == "mfma":
                 e.update(bound="mfma", achieved=round(rate / 1e12, 2), unit="TFLOP/s", peak=mf_peak,
                          frac=round(rate / 1e12 / mf_peak, 4))
@@ -391,9 +401,10 @@ def kernel_figures(wl, m):
     # VALU issue rate from the committed counter summary, when it matches the source
     scan = [k for k in bd if k.startswith("prefill.scan_")]
     if scan and "prefill.scan" in m["work"]:
-        ms = sum(bd[k][1] for k in scan)
-        launches = bd.get("prefill.scan_main", (1, 0))[0]
-        amt = sum(m["work"]["prefill.scan"][1])
+        amts = m["work"]["prefill.scan"][1][::16]    # the sampled prefill calls
+        ms = sum(bd[k][1] for k in scan) * len(amts)
+        launches = len(amts)
+        amt = sum(amts)
         gbs = amt / (ms * 1e-3) / 1e9
         e = {"passes": sorted(scan), "launches": launches, "avg_us": round(1e3 * ms / launches, 3), "bound": "alu",
              "hbm": {"achieved": round(gbs, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
@@ -514,6 +525,15 @@ def run_workload(B, torch, key, act, steps, warmup, graph=False, drawn=None, kee
 
 # ------------------------------------------------------------------- CPU baseline
 def cpu_model():
+    """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
@@ -524,7 +544,7 @@ def cpu_model():
     return None
 
 
-def cpu_baseline(drawn, n_chunks=4, n_decode=4):
+def cpu_baseline(drawn, n_chunks=20, n_decode=4):
     """The oracle (float64 numpy, untuned) on a bounded sample of the headline workload:
     shard 0's stage 1 + stage 2 over the first prefill chunks of the schedule (the other
     shard's x_proj partials precomputed, as on the GPU) and decode steps of 64 sequences;
@@ -744,7 +764,7 @@ def mamba2_figures(B, torch, steps, warmup):
         step()
     torch.cuda.synchronize()
     B.ssm_timing_collect()
-    B.ssm_timing_enable(True)
+    B.ssm_timing_enable(True, None, every=16)   # sampled, so the queue stays full
     step()
     torch.cuda.synchronize()
     B.ssm_timing_enable(False)
@@ -756,7 +776,7 @@ def mamba2_figures(B, torch, steps, warmup):
     assert B.take_status(wsp[0]) == 0 and B.take_status(wsd[0]) == 0
     pre_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     dec_us = float(np.mean([e[1].elapsed_time(e[2]) for e in evs])) * 1e3 / nd
-    kernels = {k: {"launches": n, "avg_us": round(1e3 * ms / n, 3)} for k, (n, ms) in
+    kernels = {k: {"timed_launches": n, "avg_us": round(1e3 * ms / n, 3)} for k, (n, ms) in
                sorted(bd.items(), key=lambda kv: -kv[1][1])}
     # SSD main pass: per 64-token chunk and head, the four products (two of them on hi/lo
     # operand pairs) and the bytes the pass must move: x, z, B, C, dt in, g out
@@ -1000,7 +1020,7 @@ def main():
         # the oracle's sample: the first chunks of the headline schedule (kept before the
         # large arrays are dropped)
         sh_, full_, phases_, S_, info_ = drawn
-        pre = [q for q in phases_ if q["kind"] == "prefill"][:4]
+        pre = [q for q in phases_ if q["kind"] == "prefill"][:20]
         sample = (sh_, full_, pre, S_, info_)
     if not args.no_extras:
         others = {}

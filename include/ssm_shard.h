@@ -398,12 +398,11 @@ int ssm_stack_decode_step(const ssm_stack_desc_t* desc, const ssm_shard_weights_
 /* ------------------------------------------------------------ measurement
  * Per-kernel device time, for benchmarks and profiles only. While enabled, every kernel
  * the library launches from the calling thread is launched with hipExtLaunchKernel and
- * a start/stop event pair bound to that dispatch. The start timestamp is taken when the
- * queue reaches the dispatch, so a launch issued behind unfinished work can read part of
- * that wait as its own time; ssm_timing_serialize makes each timed launch wait for its
- * stream first, which leaves the kernel's execution plus a fixed event cost of a few
- * microseconds. Leave timing off in production (each timed launch takes two events).
- * Launches on a stream under graph capture are not timed. */
+ * a start/stop event pair bound to that dispatch. A dispatch's reading can include time
+ * the GPU spent waiting for the host to submit it (when the queue has drained) or for
+ * unfinished work ahead of it, so sample few launches (every k-th) to keep the queue full.
+ * Leave timing off in production (each timed launch takes two events). Launches on a
+ * stream under graph capture are not timed. */
 typedef struct ssm_kernel_time {
     char name[48];       /* kernel role, e.g. "prefill.in_proj", "decode.state_update" */
     int64_t launches;    /* launches recorded since the last collection */
@@ -414,11 +413,6 @@ typedef struct ssm_kernel_time {
  * decode-sized kernel, off all but one launch in k; negative: SSM_E_INVAL. only: NULL to
  * time every kernel, else the one kernel name to time. */
 int ssm_timing_enable(int32_t on, const char* only);
-/* on != 0: before each timed launch the host waits for that launch's stream to drain
- * (hipStreamSynchronize), so a timed kernel never waits in the queue behind earlier work
- * (per-kernel breakdowns; it stalls the host, so not for timing whole steps). 0: off (the
- * default). Negative: SSM_E_INVAL. Per calling thread, like ssm_timing_enable. */
-int ssm_timing_serialize(int32_t on);
 /* Waits for the recorded events, sums time per kernel name into out[0 .. *count), at
  * most max entries, and forgets the records. SSM_E_HIP if an event could not be read. */
 int ssm_timing_collect(ssm_kernel_time_t* out, int32_t max, int32_t* count);

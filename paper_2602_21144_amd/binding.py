@@ -114,7 +114,6 @@ _SIGS = {
     "ssm_stack_decode_step": ([_P, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P], _I32),
     "ssm_timing_enable": ([_I32, ctypes.c_char_p], _I32),
     "ssm_timing_collect": ([_P, _I32, _P], _I32),
-    "ssm_timing_serialize": ([_I32], _I32),
 }
 
 
@@ -571,11 +570,6 @@ def scan_scratch_workspace_bytes(desc: Desc, T: int, nseq: int) -> int:
 def ssm_timing_enable(on: bool = True, only: Optional[str] = None, every: int = 1):
     """Per-dispatch kernel timing on (every `every`-th launch of each kernel name) or off."""
     _check(lib().ssm_timing_enable((max(int(every), 1) if on else 0), only.encode() if only else None))
-
-
-def ssm_timing_serialize(on: bool = True):
-    """Wait for the stream before each timed launch (per-kernel breakdowns) or not."""
-    _check(lib().ssm_timing_serialize(1 if on else 0))
 
 
 def ssm_timing_collect(max_kernels: int = 64) -> Dict[str, tuple]:

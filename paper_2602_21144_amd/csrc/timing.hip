@@ -20,7 +20,6 @@ struct Rec {
 thread_local bool g_on = false;
 thread_local std::string g_only;  // when non-empty, only launches with this name are timed
 thread_local int g_stride = 1;    // time every g_stride-th launch of each name
-thread_local bool g_serial = false;  // wait for the stream before each timed launch
 thread_local std::vector<std::pair<std::string, int64_t>> g_seen;  // launches per name while enabled
 
 // true for the launches of `name` to time: every g_stride-th one (the first included)
@@ -60,9 +59,6 @@ KernelTimer::KernelTimer(const char* name, hipStream_t s) : prev_(g_cur) {
         (void)hipGetLastError();
         return;
     }
-    // a dispatch's start timestamp is taken when the queue reaches it, so one queued behind
-    // unfinished work would read part of that wait as its own time
-    if (g_serial && hipStreamSynchronize(s) != hipSuccess) return;
     g_cur = name;
 }
 
@@ -92,12 +88,6 @@ int ssm_timing_enable(int32_t on, const char* only) {
     ssm::g_only = only ? only : "";
     ssm::g_stride = on > 1 ? on : 1;
     ssm::g_seen.clear();
-    return SSM_OK;
-}
-
-int ssm_timing_serialize(int32_t on) {
-    if (on < 0) return SSM_E_INVAL;
-    ssm::g_serial = on != 0;
     return SSM_OK;
 }
 
