@@ -964,6 +964,8 @@ def main():
                     help="only the headline workload (profiling runs): no other workloads, no NEXT-row figures")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--no-next", action="store_true", help="skip the codec, Mamba-2 and ablation figures")
+    ap.add_argument("--mamba2-only", action="store_true",
+                    help="profiling runs of the Mamba-2 shard: only its figures, printed as one JSON line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device once (a kernel of known traffic, "
                          "to scale hardware byte counters)")
@@ -978,6 +980,10 @@ def main():
     from paper_2602_21144_amd import synth
     torch.cuda.set_device(0)
     B.lib()
+    if args.mamba2_only:
+        log("Mamba-2 (SSD) shard")
+        print(json.dumps({"mamba2": mamba2_figures(B, torch, args.steps, args.warmup)}), flush=True)
+        return
     key = args.config
     act = args.dtype or ("f32" if key == "c4" else synth.CONFIGS[CONFIG_KEYS[key]]["shape"].act)
     log(f"{key} ({act}): drawing seeded host inputs")

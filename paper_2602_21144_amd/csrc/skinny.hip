@@ -839,6 +839,11 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
     static_assert(WBUF >= MT * 16 * 16 * 4, "the partial tile fits the wave's buffer");
     __shared__ __attribute__((aligned(16))) char tr[NW][WBUF];
     const int n0 = blockIdx.x * 16;
+    // row tiles of 8 XB activation rows along blockIdx.y (one tile when the grid has one row)
+    const int m0 = blockIdx.y * 8 * XB;
+    A += (int64_t)m0 * lda;
+    C += (int64_t)m0 * ldc;
+    M = min(M - m0, 8 * XB);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int nall = K / kF32Stage;
     const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
@@ -934,9 +939,17 @@ hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda
 template <int ROLE>
 hipError_t launch_f32_stream_role(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
                                   float* C, int64_t ldc, hipStream_t s) {
-    // few column tiles (x_proj: 16): 16 waves, so that each wave's run of K stays short
-    // (up to 32 rows; 64 rows take 8 waves and their LDS)
-    if ((N + 15) / 16 < 128 && M <= 32) return launch_f32_stream_nw<ROLE, 16>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    // few column tiles (x_proj: 16): 16 waves, so that each wave's run of K stays short; more
+    // than 16 rows are cut into 16-row tiles along the grid's second dimension, so that more
+    // CUs share the stream and each reads 16 activation rows instead of all of them (the
+    // hybrid shard's x_proj of 64 rows: 16 workgroups each reading 64 activation rows of
+    // 14 KB took 14 us)
+    if ((N + 15) / 16 < 128) {
+        if (M <= 16) return launch_f32_stream_nw<ROLE, 16>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 15) / 16)), block(16 * 64);
+        SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, 16, 3, 2>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
+        return hipGetLastError();
+    }
     return launch_f32_stream_nw<ROLE, 8>(M, N, K, A, lda, B, ldb, C, ldc, s);
 }
 
