@@ -609,6 +609,24 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
         slot[k] = 0;
         if constexpr (EPI == kEpiConv) slot[k] = p.slot[min(m0 + er[k], p.M - 1)];
     }
+    // the conv window operands of the epilogue groups (conv width KC) go out before the
+    // weight stream, so they arrive with its first stage instead of after its last. (The
+    // compiler waits for the slot indices with a full vector-memory count, which must
+    // happen before any stage is in flight.)
+    constexpr int KW = EPI == kEpiConv ? KC : 2;
+    ConvWindow8<bf16, KW> cw[G];
+    bool inconv[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+        const int m = m0 + er[k], c = n0 + ec[k] - p.conv_lo;
+        inconv[k] = EPI == kEpiConv && m < p.M && c >= 0 && c < p.conv_n;
+        if (inconv[k]) {
+            const int sc = slot_ok(slot[k], p.S) ? slot[k] : 0;
+            cw[k].load((const bf16*)p.conv_pool + ((int64_t)sc * p.conv_n + c) * (KW - 1),
+                       (const bf16*)p.conv_w + (int64_t)c * KW, (const bf16*)p.conv_b + c);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
 
     const int nall = p.K / kGemvBK;
     const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
@@ -677,21 +695,6 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
         stage_dma(st + RD, j);
     }
     wait_vm<0>();  // every DMA (the out-of-range refills too) has landed before LDS is reused
-    // the conv window operands of the epilogue groups (conv width KC) go out now, so they
-    // arrive while the waves' partial tiles are summed
-    constexpr int KW = EPI == kEpiConv ? KC : 2;
-    ConvWindow8<bf16, KW> cw[G];
-    bool inconv[G];
-#pragma unroll
-    for (int k = 0; k < G; ++k) {
-        const int m = m0 + er[k], c = n0 + ec[k] - p.conv_lo;
-        inconv[k] = EPI == kEpiConv && m < p.M && c >= 0 && c < p.conv_n;
-        if (inconv[k]) {
-            const int sc = slot_ok(slot[k], p.S) ? slot[k] : 0;
-            cw[k].load((const bf16*)p.conv_pool + ((int64_t)sc * p.conv_n + c) * (KW - 1),
-                       (const bf16*)p.conv_w + (int64_t)c * KW, (const bf16*)p.conv_b + c);
-        }
-    }
     // lane l holds column 16 jn + l % 16, rows 16 i + 4 (l / 16) + r of the tile
     __syncthreads();
     float* red = (float*)smem;
