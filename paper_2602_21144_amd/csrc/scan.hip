@@ -405,84 +405,122 @@ __global__ __launch_bounds__(256) void decode_ssm_kernel(ScanArgs a) {
 // 8 x 8 tiles, two 512-byte runs per instruction, the step took 15.7 instead of 10 us).
 constexpr int kDtCh = 16, kDtSeq = 4;  // tiles of the fp32 / general state-step kernel
 constexpr int kDtSeqM = 16;            // sequences per tile of the bf16 MFMA state-step kernel
+constexpr int kDtSpw = 2;              // sequences per wave of that kernel
 
-// bf16 and dt_rank a multiple of 32 (up to 512): a workgroup of 16 waves takes 16
-// channels of 16 sequences, wave w sequence w (its 16 channels' states are 1 KB
-// contiguous per load instruction, four lanes per channel). The workgroup's 16 x 16 tile
-// of dt is the product delta[16 sequences][R] x W_dt[16 channels][R]^T: its R / 32
-// k-chunks go to waves 0 .. R/32 - 1, one v_mfma_f32_16x16x32_bf16 each, whose partial
-// tiles meet in LDS; every thread adds the partials of its (sequence, channel) in chunk
-// order and rounds dt to bf16 as dt_proj stores it. Each workgroup fetches its 16 delta
-// rows and 16 W_dt rows once: 15 KB per 16 x 16 items. (4 x 16 tiles fetched the W_dt
-// rows once per 4 sequences, about as many L2 bytes as the states themselves, and took
-// 15.5 us for 256 sequences of 1280 channels; per-lane dot products made each lane fetch
-// 240 bytes of delta and W, mostly repeats of its neighbours'.)
-template <int NK>
-__global__ __launch_bounds__(1024) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
-    __shared__ float dt_part[NK][kDtSeqM][kDtCh];
+// bf16 and dt_rank a multiple of 32 (up to 512): a workgroup takes 16 channels of 16
+// sequences, SPW sequences per wave (four lanes per (sequence, channel), a float4 of states
+// each: every state load and store instruction covers 1 KB contiguous). The step is bound by
+// the state bytes in flight per CU over the memory latency; for 256 sequences of 1280
+// channels one sequence per wave took 13.1 us, two 12.5 us, four 14.3 us. The workgroup's
+// 16 x 16 tile of dt is the product delta[16 sequences][R] x W_dt[16 channels][R]^T:
+// k-chunk k of the R / 32 is one v_mfma_f32_16x16x32_bf16 on wave k % (waves); the waves'
+// partial tiles meet in LDS, every thread adds them in wave order and rounds dt to bf16 as
+// dt_proj stores it. Each workgroup fetches its 16 delta rows and 16 W_dt rows once. (4 x 16
+// tiles fetched the W_dt rows once per 4 sequences, about as many L2 bytes as the states
+// themselves: 15.5 us.)
+template <int NK, int SPW>
+__global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
+    constexpr int NWV = kDtSeqM / SPW;         // waves
+    constexpr int KPW = (NK + NWV - 1) / NWV;  // k-chunks per wave
+    constexpr int NP = NK < NWV ? NK : NWV;    // partial tiles
+    __shared__ float dt_part[NP][kDtSeqM][kDtCh];
     const int ctiles = a.E / kDtCh;
     const int tb = blockIdx.x / ctiles, tc = blockIdx.x % ctiles;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int it = lane >> 2, q = lane & 3;  // channel tc * 16 + it of sequence tb * 16 + wave
-    const int bb = tb * kDtSeqM + wave, cc = tc * kDtCh + it;
-    const bool live = bb < a.nseq;
-    const int b = live ? bb : 0, c = cc;
-    const int slot = a.slot[b];
-    const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
-    const float* xb = a.xdbl + (int64_t)b * a.ld_xdbl + a.R;
-    const float4 Bq = ((const float4*)xb)[q], Cq = ((const float4*)(xb + kN))[q];
-    const float u = (float)((const bf16*)a.u)[(int64_t)b * a.E + c];
-    const float z = (float)((const bf16*)a.z)[(int64_t)b * a.ld_z + c];
-    const float bdt = a.b_dt[c], Dc = a.D[c];
-    const bool slot_ok = slot >= 0 && slot < a.S;
-    float4* hp = (float4*)(a.pool + ((int64_t)(slot_ok ? slot : 0) * a.E + c) * kN) + q;
-    const float4 h = *hp;
+    const int it = lane >> 2, q = lane & 3;  // channel tc * 16 + it; states 4q .. 4q + 3
+    const int c = tc * kDtCh + it;
+    int bsq[SPW], slot[SPW];
+    bool live[SPW], sok[SPW];
+    float4 Bq[SPW], Cq[SPW], h[SPW];
+    float u[SPW], z[SPW];
+    float4* hp[SPW];
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+        const int bb = tb * kDtSeqM + SPW * wave + j;
+        live[j] = bb < a.nseq;
+        bsq[j] = live[j] ? bb : 0;
+        slot[j] = a.slot[bsq[j]];
+        const float* xb = a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R;
+        Bq[j] = ((const float4*)xb)[q];
+        u[j] = (float)((const bf16*)a.u)[(int64_t)bsq[j] * a.E + c];
+    }
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+        sok[j] = slot[j] >= 0 && slot[j] < a.S;
+        hp[j] = (float4*)(a.pool + ((int64_t)(sok[j] ? slot[j] : 0) * a.E + c) * kN) + q;
+        h[j] = *hp[j];
+    }
     if (wave < NK) {
-        // chunk k = wave: lane l takes delta row l % 16 (rows past the batch zero) and W_dt
-        // row l % 16, columns 32 k + 8 (l / 16) .. + 7
-        const int r = lane & 15, kq = (lane >> 4) * 8, k0 = 32 * wave + kq;
+        // chunks k = wave + NWV kk: lane l takes delta row l % 16 (rows past the batch zero)
+        // and W_dt row l % 16, columns 32 k + 8 (l / 16) .. + 7
+        const int r = lane & 15, kq = (lane >> 4) * 8;
         const int sr = tb * kDtSeqM + r;
         const bool rok = sr < a.nseq;
         const float* drow = a.xdbl + (int64_t)(rok ? sr : 0) * a.ld_xdbl;
         const bf16* wrow = (const bf16*)a.w_dt + (int64_t)(tc * kDtCh + r) * a.R;
-        const float4 d0 = *(const float4*)(drow + k0), d1 = *(const float4*)(drow + k0 + 4);
-        const bf16x8 wf = *(const bf16x8*)(wrow + k0);
-        bf16x8 af;
-        af[0] = (bf16)d0.x; af[1] = (bf16)d0.y; af[2] = (bf16)d0.z; af[3] = (bf16)d0.w;
-        af[4] = (bf16)d1.x; af[5] = (bf16)d1.y; af[6] = (bf16)d1.z; af[7] = (bf16)d1.w;
-        if (!rok) af = bf16x8{};
-        const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf, f32x4{}, 0, 0, 0);
+        float4 d0[KPW], d1[KPW];
+        bf16x8 wf[KPW];
+#pragma unroll
+        for (int kk = 0; kk < KPW; ++kk) {
+            const int k = wave + NWV * kk < NK ? wave + NWV * kk : wave;  // past the last chunk: re-read, not added
+            d0[kk] = *(const float4*)(drow + 32 * k + kq);
+            d1[kk] = *(const float4*)(drow + 32 * k + kq + 4);
+            wf[kk] = *(const bf16x8*)(wrow + 32 * k + kq);
+        }
+        f32x4 acc = f32x4{};
+#pragma unroll
+        for (int kk = 0; kk < KPW; ++kk) {
+            bf16x8 af;
+            af[0] = (bf16)d0[kk].x; af[1] = (bf16)d0[kk].y; af[2] = (bf16)d0[kk].z; af[3] = (bf16)d0[kk].w;
+            af[4] = (bf16)d1[kk].x; af[5] = (bf16)d1[kk].y; af[6] = (bf16)d1[kk].z; af[7] = (bf16)d1[kk].w;
+            if (!rok || wave + NWV * kk >= NK) af = bf16x8{};
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[kk], acc, 0, 0, 0);
+        }
         // lane l holds sequences 4 (l / 16) + j of the tile, channel l % 16
 #pragma unroll
         for (int j = 0; j < 4; ++j) dt_part[wave][4 * (lane >> 4) + j][r] = acc[j];
     }
     __syncthreads();
-    float dsum = dt_part[0][wave][it];
+    // operands of the output alone, fetched after the dt tile so that fewer registers are
+    // live across it (eight waves per SIMD without spills)
 #pragma unroll
-    for (int k = 1; k < NK; ++k) dsum += dt_part[k][wave][it];
-    const float dt = (float)(bf16)dsum;  // stored in bf16 as dt_proj's output
-    const float delta = softplus_f(dt + bdt);
-    const float du = delta * u;
-    const float hv[4] = {h.x, h.y, h.z, h.w}, av[4] = {al.x, al.y, al.z, al.w};
-    const float bv[4] = {Bq.x, Bq.y, Bq.z, Bq.w}, cv[4] = {Cq.x, Cq.y, Cq.z, Cq.w};
-    float hn[4], y = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
-        y += cv[i] * hn[i];
+    for (int j = 0; j < SPW; ++j) {
+        Cq[j] = ((const float4*)(a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R + kN))[q];
+        z[j] = (float)((const bf16*)a.z)[(int64_t)bsq[j] * a.ld_z + c];
     }
-    y += __shfl_xor(y, 1);
-    y += __shfl_xor(y, 2);
-    if (!live) return;
-    if (!slot_ok) {
-        if (q == 0) {
-            atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-            ((bf16*)a.g)[(int64_t)b * a.E + c] = (bf16)0.0f;
+    const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
+    const float bdt = a.b_dt[c], Dc = a.D[c];
+    const float av[4] = {al.x, al.y, al.z, al.w};
+#pragma unroll
+    for (int j = 0; j < SPW; ++j) {
+        const int ts = SPW * wave + j;
+        float dsum = dt_part[0][ts][it];
+#pragma unroll
+        for (int k = 1; k < NP; ++k) dsum += dt_part[k][ts][it];
+        const float dt = (float)(bf16)dsum;  // stored in bf16 as dt_proj's output
+        const float delta = softplus_f(dt + bdt);
+        const float du = delta * u[j];
+        const float hv[4] = {h[j].x, h[j].y, h[j].z, h[j].w};
+        const float bv[4] = {Bq[j].x, Bq[j].y, Bq[j].z, Bq[j].w}, cv[4] = {Cq[j].x, Cq[j].y, Cq[j].z, Cq[j].w};
+        float hn[4], y = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
+            y += cv[i] * hn[i];
         }
-        return;
+        y += __shfl_xor(y, 1);
+        y += __shfl_xor(y, 2);
+        if (!live[j]) continue;
+        if (!sok[j]) {
+            if (q == 0) {
+                atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+                ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)0.0f;
+            }
+            continue;
+        }
+        *hp[j] = make_float4(hn[0], hn[1], hn[2], hn[3]);
+        if (q == 0) ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)((y + Dc * u[j]) * silu_f(z[j]));
     }
-    *hp = make_float4(hn[0], hn[1], hn[2], hn[3]);
-    if (q == 0) ((bf16*)a.g)[(int64_t)b * a.E + c] = (bf16)((y + Dc * u) * silu_f(z));
 }
 
 template <typename T, int NCH>
@@ -663,12 +701,12 @@ hipError_t launch_decode_dt_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
         ((uintptr_t)a.w_dt & 15) != 0)
         return hipErrorNotSupported;
     if (bf && a.R % 32 == 0 && a.R <= 16 * 32) {
-        const dim3 g16((unsigned)(((a.nseq + kDtSeqM - 1) / kDtSeqM) * (a.E / kDtCh))), b16(1024);
+        const dim3 g16((unsigned)(((a.nseq + kDtSeqM - 1) / kDtSeqM) * (a.E / kDtCh))), b16(64 * kDtSeqM / kDtSpw);
         switch (a.R / 32) {
-#define SSM_DTM(NK) case NK: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<NK>, g16, b16, 0, s, a); break;
+#define SSM_DTM(NK) case NK: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<NK, kDtSpw>), g16, b16, 0, s, a); break;
             SSM_DTM(1) SSM_DTM(2) SSM_DTM(3) SSM_DTM(4) SSM_DTM(5) SSM_DTM(6) SSM_DTM(7) SSM_DTM(8)
             SSM_DTM(9) SSM_DTM(10) SSM_DTM(11) SSM_DTM(12) SSM_DTM(13) SSM_DTM(14) SSM_DTM(15)
-            default: SSM_LAUNCH(decode_dt_ssm_mfma_kernel<16>, g16, b16, 0, s, a); break;
+            default: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<16, kDtSpw>), g16, b16, 0, s, a); break;
 #undef SSM_DTM
         }
         return hipGetLastError();

@@ -676,23 +676,29 @@ __global__ __launch_bounds__(NW * 64) void gemm_dtile_kernel(SkinnyArgs p) {
         wait_vm<(RD - 1) * OPS>();  // stage st has landed; the RD - 1 after it may not have
         const char* abuf = smem + (wave * RD + j) * SLOT;
         const char* wbuf = abuf + AB * 1024;
+        // the whole stage goes to registers first and its slot is refilled before the
+        // MFMAs, so RD stages (not RD - 1) are in flight while the wave multiplies
+        bf16x8 af[2][MT], wf[2][NT];
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
             const int c = 4 * s + cg;
-            bf16x8 af[MT];
 #pragma unroll
             for (int i = 0; i < MT; ++i)
-                af[i] = *(const bf16x8*)(abuf + (16 * i + fr) * 128 + gemv_swz(16 * i + fr, c) * 16);
+                af[s][i] = *(const bf16x8*)(abuf + (16 * i + fr) * 128 + gemv_swz(16 * i + fr, c) * 16);
 #pragma unroll
-            for (int jn = 0; jn < NT; ++jn) {
-                const bf16x8 wf = *(const bf16x8*)(wbuf + (16 * jn + fr) * 128 + gemv_swz(16 * jn + fr, c) * 16);
-#pragma unroll
-                for (int i = 0; i < MT; ++i)
-                    acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf, acc[i][jn], 0, 0, 0);
-            }
+            for (int jn = 0; jn < NT; ++jn)
+                wf[s][jn] = *(const bf16x8*)(wbuf + (16 * jn + fr) * 128 + gemv_swz(16 * jn + fr, c) * 16);
         }
         wait_lgkm0();  // the slot's fragments are read before it is refilled
         stage_dma(st + RD, j);
+        __builtin_amdgcn_sched_barrier(0);  // no MFMA moves above the refill
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int jn = 0; jn < NT; ++jn)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s][i], wf[s][jn], acc[i][jn], 0, 0, 0);
     }
     wait_vm<0>();  // every DMA (the out-of-range refills too) has landed before LDS is reused
     // lane l holds column 16 jn + l % 16, rows 16 i + 4 (l / 16) + r of the tile
