@@ -434,39 +434,45 @@ __global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(
     float4 Bq[SPW], Cq[SPW], h[SPW];
     float u[SPW], z[SPW];
     float4* hp[SPW];
+    // the slot indices first: the state loads wait for them alone
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
         const int bb = tb * kDtSeqM + SPW * wave + j;
         live[j] = bb < a.nseq;
         bsq[j] = live[j] ? bb : 0;
         slot[j] = a.slot[bsq[j]];
-        const float* xb = a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R;
-        Bq[j] = ((const float4*)xb)[q];
-        u[j] = (float)((const bf16*)a.u)[(int64_t)bsq[j] * a.E + c];
     }
+    // the dt tile's operands, issued before the states so that the MFMAs wait for them and
+    // not for the states (which stay in flight across the dt tile and the barrier). Chunks
+    // k = wave + NWV kk: lane l takes delta row l % 16 (rows past the batch zero) and W_dt
+    // row l % 16, columns 32 k + 8 (l / 16) .. + 7
+    const bool mw = wave < NK;
+    const int r = lane & 15, kq = (lane >> 4) * 8;
+    const bool rok = tb * kDtSeqM + r < a.nseq;
+    // every wave issues them (waves past the last chunk re-read chunk 0, unused), so that no
+    // branch hides the loads' count from the compiler's counter waits
+    float4 d0[KPW], d1[KPW];
+    bf16x8 wf[KPW];
+    {
+        const float* drow = a.xdbl + (int64_t)(rok ? tb * kDtSeqM + r : 0) * a.ld_xdbl;
+        const bf16* wrow = (const bf16*)a.w_dt + (int64_t)(tc * kDtCh + r) * a.R;
+#pragma unroll
+        for (int kk = 0; kk < KPW; ++kk) {
+            const int k = wave + NWV * kk < NK ? wave + NWV * kk : 0;  // past the last chunk: re-read, not added
+            d0[kk] = *(const float4*)(drow + 32 * k + kq);
+            d1[kk] = *(const float4*)(drow + 32 * k + kq + 4);
+            wf[kk] = *(const bf16x8*)(wrow + 32 * k + kq);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
         sok[j] = slot[j] >= 0 && slot[j] < a.S;
         hp[j] = (float4*)(a.pool + ((int64_t)(sok[j] ? slot[j] : 0) * a.E + c) * kN) + q;
         h[j] = *hp[j];
     }
-    if (wave < NK) {
-        // chunks k = wave + NWV kk: lane l takes delta row l % 16 (rows past the batch zero)
-        // and W_dt row l % 16, columns 32 k + 8 (l / 16) .. + 7
-        const int r = lane & 15, kq = (lane >> 4) * 8;
-        const int sr = tb * kDtSeqM + r;
-        const bool rok = sr < a.nseq;
-        const float* drow = a.xdbl + (int64_t)(rok ? sr : 0) * a.ld_xdbl;
-        const bf16* wrow = (const bf16*)a.w_dt + (int64_t)(tc * kDtCh + r) * a.R;
-        float4 d0[KPW], d1[KPW];
-        bf16x8 wf[KPW];
-#pragma unroll
-        for (int kk = 0; kk < KPW; ++kk) {
-            const int k = wave + NWV * kk < NK ? wave + NWV * kk : wave;  // past the last chunk: re-read, not added
-            d0[kk] = *(const float4*)(drow + 32 * k + kq);
-            d1[kk] = *(const float4*)(drow + 32 * k + kq + 4);
-            wf[kk] = *(const bf16x8*)(wrow + 32 * k + kq);
-        }
+    __builtin_amdgcn_sched_barrier(0);
+    if (mw) {
         f32x4 acc = f32x4{};
 #pragma unroll
         for (int kk = 0; kk < KPW; ++kk) {
@@ -480,16 +486,18 @@ __global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < 4; ++j) dt_part[wave][4 * (lane >> 4) + j][r] = acc[j];
     }
-    __syncthreads();
-    // operands of the output alone, fetched after the dt tile so that fewer registers are
-    // live across it (eight waves per SIMD without spills)
+    // the operands of the output alone, in flight across the barrier
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
-        Cq[j] = ((const float4*)(a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R + kN))[q];
+        const float* xb = a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R;
+        Bq[j] = ((const float4*)xb)[q];
+        Cq[j] = ((const float4*)(xb + kN))[q];
+        u[j] = (float)((const bf16*)a.u)[(int64_t)bsq[j] * a.E + c];
         z[j] = (float)((const bf16*)a.z)[(int64_t)bsq[j] * a.ld_z + c];
     }
     const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
     const float bdt = a.b_dt[c], Dc = a.D[c];
+    __syncthreads();
     const float av[4] = {al.x, al.y, al.z, al.w};
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
