@@ -204,7 +204,10 @@ template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
 // are covered by the other's MFMAs. SPLIT: workgroup (tile, blockIdx.y) multiplies the
 // K-slice [blockIdx.y * K, (blockIdx.y + 1) * K) (K is the slice length) and stores its
 // fp32 partial tile at part[blockIdx.y][M][N]; a reduce kernel adds the slices.
-template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false>
+// F32: the operands are float32 rows passed as bf16 rows of twice the length (K, lda and
+// ldb in bf16 units); the DMA and the LDS layout only move bytes, and each 16-byte fragment
+// (4 floats along k) feeds four v_mfma_f32_32x32x2_f32 instead of one bf16 MFMA.
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false, bool F32 = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
                                                               int64_t lda, const bf16* __restrict__ B, int64_t ldb,
                                                               void* __restrict__ Cp, int64_t ldc, int tiles_m,
@@ -214,11 +217,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     constexpr int TM = WTM / 32, TN = WTN / 32;
     constexpr int CPR = BK / 8;             // 16-byte chunks per row
     constexpr int RPB = 64 / CPR;           // rows per 1 KB DMA block
-    constexpr int AG = BM / RPB / NW, BG = BN / RPB / NW;  // DMA blocks per wave per stage
-    constexpr int OPS = AG + BG;
+    // DMA blocks of one stage: BM / RPB activation blocks, then BN / RPB weight blocks. When
+    // they split evenly, wave w takes AG consecutive activation and BG weight blocks;
+    // otherwise (a 2-deep ring only, whose waits are for all of a wave's loads) block b goes to
+    // wave b % NW, so waves take QM or QM - 1 blocks
+    constexpr bool EVEN = BM % (RPB * NW) == 0 && BN % (RPB * NW) == 0;
+    constexpr int TBA = BM / RPB, TBT = (BM + BN) / RPB, QM = (TBT + NW - 1) / NW;
+    constexpr int AG = EVEN ? BM / RPB / NW : 0, BG = EVEN ? BN / RPB / NW : 0;  // DMA blocks per wave per stage
+    constexpr int OPS = EVEN ? AG + BG : QM;
     constexpr int SUB = BK / 16;            // MFMA k-substeps per stage
-    static_assert(AG >= 1 && BG >= 1 && NS >= 2, "tile");
-    static_assert(BM % (RPB * NW) == 0 && BN % (RPB * NW) == 0, "tile rows split evenly over the waves' DMA blocks");
+    static_assert(NS >= 2 && BM % RPB == 0 && BN % RPB == 0, "tile");
+    static_assert(EVEN ? (AG >= 1 && BG >= 1) : NS == 2, "uneven DMA blocks need the 2-deep ring");
     static_assert(SUB % 2 == 0, "fragment sets alternate within a tile");
     // one LDS block: the operand ring, reused after the k loop to stage the output tile
     constexpr int RING = NS * (BM + BN) * BK * 2;
@@ -249,27 +258,44 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     // them and the k advance goes in the scalar offset
     const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A + (int64_t)m0 * lda, (uint32_t)((int64_t)min(BM, M - m0) * lda * 2));
     const __amdgpu_buffer_rsrc_t rbr = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)((int64_t)min(BN, N - n0) * ldb * 2));
-    uint32_t aoff[AG], boff[BG];
-#pragma unroll
-    for (int q = 0; q < AG; ++q) {
-        const int r = (wave * AG + q) * RPB + lr;
-        aoff[q] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * lda + swz_k<BK>(r, lp) * 8) * 2);
-    }
-#pragma unroll
-    for (int q = 0; q < BG; ++q) {
-        const int r = (wave * BG + q) * RPB + lr;
-        boff[q] = (uint32_t)(((int64_t)(min(n0 + r, N - 1) - n0) * ldb + swz_k<BK>(r, lp) * 8) * 2);
-    }
+    auto a_off = [&](int r) { return (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * lda + swz_k<BK>(r, lp) * 8) * 2); };
+    auto b_off = [&](int r) { return (uint32_t)(((int64_t)(min(n0 + r, N - 1) - n0) * ldb + swz_k<BK>(r, lp) * 8) * 2); };
     const uint32_t a_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&As[0][0];
     const uint32_t b_lds = (uint32_t)(uintptr_t)(lds_ptr_t)&Bs[0][0];
+    constexpr int NA = EVEN ? AG : QM, NB = EVEN ? BG : 1;
+    uint32_t aoff[NA], boff[NB];
+    const int wu = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform, for the block choice
+    if constexpr (EVEN) {
+#pragma unroll
+        for (int q = 0; q < AG; ++q) aoff[q] = a_off((wave * AG + q) * RPB + lr);
+#pragma unroll
+        for (int q = 0; q < BG; ++q) boff[q] = b_off((wave * BG + q) * RPB + lr);
+    } else {
+#pragma unroll
+        for (int q = 0; q < QM; ++q) {
+            const int b = wu + NW * q;
+            aoff[q] = b < TBA ? a_off(b * RPB + lr) : b_off((b - TBA) * RPB + lr);
+        }
+    }
     auto dma = [&](int kt, int stage) {
         const int k0 = kt * BK;
+        if constexpr (EVEN) {
 #pragma unroll
-        for (int q = 0; q < AG; ++q)
-            dma16(ra, aoff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + q) * RPB) * BK * 2)));
+            for (int q = 0; q < AG; ++q)
+                dma16(ra, aoff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + q) * RPB) * BK * 2)));
 #pragma unroll
-        for (int q = 0; q < BG; ++q)
-            dma16(rbr, boff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + q) * RPB) * BK * 2)));
+            for (int q = 0; q < BG; ++q)
+                dma16(rbr, boff[q], (uint32_t)k0 * 2, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + q) * RPB) * BK * 2)));
+        } else {
+#pragma unroll
+            for (int q = 0; q < QM; ++q) {
+                const int b = wu + NW * q;
+                if (b < TBA)
+                    dma16(ra, aoff[q], (uint32_t)k0 * 2, a_lds + (uint32_t)((stage * BM + b * RPB) * BK * 2));
+                else if (b < TBT)
+                    dma16(rbr, aoff[q], (uint32_t)k0 * 2, b_lds + (uint32_t)((stage * BN + (b - TBA) * RPB) * BK * 2));
+            }
+        }
     };
 
     f32x16 acc[TM][TN];
@@ -295,20 +321,35 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         for (int j = 0; j < TN; ++j) fb[set][j] = *(const bf16x8*)&bs[brow[j] * BK + swz_k<BK>(brow[j], c) * 8];
     };
     auto mfma = [&](int set) {
+        if constexpr (F32) {
+            // float32 operands: a 16-byte chunk holds 4 floats along k; lanes 0-31 take chunk
+            // 2s, lanes 32-63 chunk 2s + 1, so MFMA u sums k = 8s + u and 8s + 4 + u
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
+                                                                         __builtin_bit_cast(f32x4, fa[set][i])[u],
+                                                                         acc[i][j], 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+        }
     };
     // one MFMA per fragment read, then the remaining MFMAs of the substep
+    constexpr int NMF = TM * TN * (F32 ? 4 : 1);
     auto interleave = [&]() {
 #pragma unroll
         for (int q = 0; q < TM + TN; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-        if (TM * TN > TM + TN) __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
+        if (NMF > TM + TN) __builtin_amdgcn_sched_group_barrier(0x008, NMF - (TM + TN), 0);
     };
 
 #pragma unroll
@@ -495,6 +536,29 @@ hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, 
     return hipGetLastError();
 }
 
+// float32 operands on the DMA tiles: the rows are moved as bytes, so the kernel sees them as
+// bf16 rows of twice the length (K, lda, ldb doubled); only the MFMAs read them as floats
+template <int ROLE, int BM, int BN, int NS, int WM, int WN>
+hipError_t run_dma_f32(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B, int64_t ldb,
+                       float* C, int64_t ldc, hipStream_t s, int splits = 1, float* part = nullptr) {
+    const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
+    if (splits <= 1) {
+        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, false, true>), dim3(tm * tn), dim3(64 * WM * WN),
+                   0, s, (int)M, (int)N, (int)(2 * K), (const bf16*)A, 2 * lda, (const bf16*)B, 2 * ldb, C, ldc, tm,
+                   tn, nullptr);
+        return hipGetLastError();
+    }
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, true, true>), dim3(tm * tn, splits),
+               dim3(64 * WM * WN), 0, s, (int)M, (int)N, (int)(2 * K / splits), (const bf16*)A, 2 * lda,
+               (const bf16*)B, 2 * ldb, C, ldc, tm, tn, part);
+    if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    KernelTimer kt("gemm.splitk_reduce", s);
+    const int64_t n4 = M * ((N + 3) / 4);
+    SSM_LAUNCH((splitk_reduce_kernel<true>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, (const float*)part,
+               splits, (int)M, (int)N, C, ldc);
+    return hipGetLastError();
+}
+
 // Tile shape by a wave-quantisation cost model: whole rounds of 256 workgroups (one per
 // CU) times tile area over the shape's measured efficiency (256x256 does the most MFMA
 // work per LDS byte; 128x128 gives more workgroups when the grid is small). 256x320 (4x2
@@ -512,6 +576,29 @@ DmaTiles dma_tiles(int64_t M, int64_t N) {
     return (N % 320 == 0 && cost(256, 320, 1.0) < c256) ? kTiles256x320 : kTiles256;
 }
 bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; }
+
+// Float32 tiles by the same kind of model: rounds of workgroups (one per CU; two for the 64 KB
+// ring of 128x128) times the work a CU does per round over the tile's measured per-CU MFMA
+// efficiency. On the hybrid shard's 2048-row chunks: 256x256 tiles (8 waves of 128x64) 0.91,
+// 256x224 (8 waves of 32x224) 0.93, 128x224 (4 waves of 32x224) 0.85, 128x128 (8 waves of
+// 64x32, two per CU) 0.89. The 224-wide tiles exist for outputs whose 256-wide tiles leave
+// part of a round empty: in_proj (2048 x 7168) takes 256 tiles of 256x224 where 256x256 gave
+// 224 (840 -> 720 us), out_proj (2048 x 3584) 256 tiles of 128x224 where 128x128 gave 448
+// over two slots per CU (430 -> 393 us).
+enum F32Tiles { kF32Tiles128 = 0, kF32Tiles256 = 1, kF32Tiles256x224 = 2, kF32Tiles128x224 = 3 };
+F32Tiles f32_tiles(int64_t M, int64_t N) {
+    auto cost = [&](int bm, int bn, int per_cu, double eff) {
+        const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn), slots = 256 * per_cu;
+        return (double)((tiles + slots - 1) / slots) * per_cu * bm * bn / eff;
+    };
+    F32Tiles best = kF32Tiles128;
+    double c = cost(128, 128, 2, 0.89);
+    const double c256 = cost(256, 256, 1, 0.91), c224 = cost(256, 224, 1, 0.93), c128x224 = cost(128, 224, 1, 0.85);
+    if (c256 < c) { c = c256; best = kF32Tiles256; }
+    if (c224 < c) { c = c224; best = kF32Tiles256x224; }
+    if (c128x224 < c) { c = c128x224; best = kF32Tiles128x224; }
+    return best;
+}
 
 // Decode batches above the few-row kernels (65..512 rows) with bf16 output: the streamed
 // tile kernel of the decode projections (launch_gemm_skinny) when its tiles give at least
@@ -682,132 +769,8 @@ __global__ __launch_bounds__(256) void gemm_f32_nt(int M, int N, int K, const fl
     }
 }
 
-// fp32 operands at prefill sizes: BM x BN tiles of WM x WN waves, each wave a
-// (BM / WM) x (BN / WN) block of 16x16 tiles of v_mfma_f32_16x16x4_f32, 32-wide k stages
-// (one 128-byte line of every operand row). Each stage moves global -> registers -> LDS in
-// whole lines (8 threads per row), one stage ahead of the MFMAs, into a double-buffered
-// LDS ring with one barrier per stage. Fragments are read as float4 along k: lane l takes
-// chunk 4 g + l / 16 of row l % 16 and MFMA u of group g uses component u, the same k for
-// both operands. LDS rows are XOR-swizzled in 16-byte chunks (chunk ^ ((row / 2) % 8)),
-// which keeps both the whole-row writes and the 16-row fragment reads free of bank
-// conflicts. The weight fragment is the MFMA's first operand, so a lane ends up with four
-// consecutive output columns of one row: float4 stores. Rows and columns past M, N read as
-// zero. Two waves per SIMD or more keep the MFMA pipe fed across each stage's barrier and
-// LDS reads: on the hybrid shard's 2048-row chunks (random operands) 128x128 tiles of 8
-// waves took out_proj (3584 x 3584) from 443-468 to 428-431 us against 4 waves, and 256x256
-// tiles of 16 waves in_proj (7168 x 3584) from 880-980 to 832-839 us.
+// float32 k stages: 32 floats, one 128-byte line of every operand row
 constexpr int kF32BK = 32;
-
-__device__ __forceinline__ int f32_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
-
-template <int ROLE, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_f32_big(int M, int N, int K, const float* __restrict__ A,
-                                                             int64_t lda, const float* __restrict__ B, int64_t ldb,
-                                                             float* __restrict__ C, int64_t ldc, int tiles_m,
-                                                             int tiles_n, float* __restrict__ part) {
-    constexpr int NT = 64 * WM * WN;            // threads
-    constexpr int TI = BM / WM / 16, TJ = BN / WN / 16;
-    constexpr int SA = BM * 128, SB = BN * 128; // bytes of each operand's stage
-    constexpr int RS = NT / 8;                  // rows one pass of all threads moves
-    constexpr int CA = BM / RS, CB = BN / RS;   // 16-byte chunks per thread per stage
-    static_assert(CA * RS == BM && CB * RS == BN && TI >= 1 && TJ >= 1, "tile");
-    __shared__ __attribute__((aligned(16))) char lds[2][SA + SB];
-    int tm, tn;
-    tile_of(tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WN, wn = wave % WN;
-    const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A + (int64_t)m0 * lda, (uint32_t)(min(BM, M - m0) * lda * 4));
-    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)(min(BN, N - n0) * ldb * 4));
-    // loads of one stage: thread t moves chunk t % 8 of rows t / 8 + RS i of each operand
-    const int lrow = tid >> 3, lck = tid & 7;
-    u32x4 va[CA], vb[CB];
-    auto gload = [&](int st) {
-        const uint32_t kb = (uint32_t)(st * kF32BK + lck * 4) * 4;
-#pragma unroll
-        for (int i = 0; i < CA; ++i) va[i] = buffer_load16(ra, (uint32_t)((lrow + RS * i) * lda) * 4 + kb);
-#pragma unroll
-        for (int i = 0; i < CB; ++i) vb[i] = buffer_load16(rb, (uint32_t)((lrow + RS * i) * ldb) * 4 + kb);
-    };
-    auto lstore = [&](int buf) {
-        char* a = lds[buf];
-        char* b = lds[buf] + SA;
-#pragma unroll
-        for (int i = 0; i < CA; ++i) {
-            const int r = lrow + RS * i;
-            *(u32x4*)(a + r * 128 + f32_swz(r, lck) * 16) = va[i];
-        }
-#pragma unroll
-        for (int i = 0; i < CB; ++i) {
-            const int r = lrow + RS * i;
-            *(u32x4*)(b + r * 128 + f32_swz(r, lck) * 16) = vb[i];
-        }
-    };
-    f32x4 acc[TJ][TI];  // [weight tile j][activation tile i]
-#pragma unroll
-    for (int j = 0; j < TJ; ++j)
-#pragma unroll
-        for (int i = 0; i < TI; ++i) acc[j][i] = f32x4{};
-    // split-K: workgroup row blockIdx.y takes K-slice [s0, s0 + nst) of gridDim.y equal slices
-    // and writes its fp32 partial tile to part[blockIdx.y] (row stride N)
-    const int nst = K / kF32BK / gridDim.y, s0 = blockIdx.y * nst;
-    if (part) {
-        C = part + (int64_t)blockIdx.y * M * N;
-        ldc = N;
-    }
-    const int fr = lane & 15, cg = lane >> 4;
-    gload(s0);
-    lstore(0);
-    __syncthreads();
-    for (int st = 0; st < nst; ++st) {
-        const int cur = st & 1;
-        if (st + 1 < nst) gload(s0 + st + 1);
-        const char* a = lds[cur];
-        const char* b = lds[cur] + SA;
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            const int c = 4 * g + cg;
-            f32x4 af[TI], bfr[TJ];
-#pragma unroll
-            for (int i = 0; i < TI; ++i) {
-                const int r = wm * (BM / WM) + 16 * i + fr;
-                af[i] = *(const f32x4*)(a + r * 128 + f32_swz(r, c) * 16);
-            }
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) {
-                const int r = wn * (BN / WN) + 16 * j + fr;
-                bfr[j] = *(const f32x4*)(b + r * 128 + f32_swz(r, c) * 16);
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int j = 0; j < TJ; ++j)
-#pragma unroll
-                    for (int i = 0; i < TI; ++i)
-                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(bfr[j][u], af[i][u], acc[j][i], 0, 0, 0);
-        }
-        if (st + 1 < nst) lstore(cur ^ 1);
-        __syncthreads();
-    }
-    // lane l holds activation row l % 16 and weight columns 4 (l / 16) + v of each tile pair
-#pragma unroll
-    for (int i = 0; i < TI; ++i) {
-        const int m = m0 + wm * (BM / WM) + 16 * i + fr;
-        if (m >= M) continue;
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) {
-            const int n = n0 + wn * (BN / WN) + 16 * j + 4 * cg;
-            float* p = C + (int64_t)m * ldc + n;
-            if (n + 3 < N && (ldc & 3) == 0) {
-                *(float4*)p = make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (n + v < N) p[v] = acc[j][i][v];
-            }
-        }
-    }
-}
 
 // K-slices for a float32 product with few 128x128 tiles: the most slices (dividing the
 // 32-wide stages, at least 4 stages each) that keep the grid within about two workgroups
@@ -933,56 +896,35 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
 #undef SSM_F32_GEMV
             return hipGetLastError();
         }
-        // prefill sizes: 128x128 tiles when they give a few rounds of workgroups, or when the
-        // product can be cut into K-slices to get there (x_proj: 32 tiles); 256x256 tiles of 16
-        // waves when those still give about a round
+        // prefill sizes on the DMA tiles (float32 rows moved as bytes, run_dma_f32): K-slices of
+        // 128x128 tiles when the output has few tiles (x_proj), else the tile shape of least
+        // modelled time (f32_tiles)
         {
             const int64_t tm2 = (M + 127) / 128, tn2 = (N + 127) / 128;
             const int sp = fit_slices(f32_slices(tm2 * tn2, K), M, N, scratch_bytes);
-            const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
-            const bool big = t256 >= 192 && sp <= 1;
-            const int64_t rows = big ? 256 : 128;
             if (K % kF32BK == 0 && (tm2 * tn2 >= 256 || sp > 1) && lda % 4 == 0 && ldb % 4 == 0 && al16(A) &&
-                al16(B) && al16(C) && rows * lda * 4 < ((int64_t)1 << 31) && rows * ldb * 4 < ((int64_t)1 << 31)) {
+                al16(B) && al16(C) && 256 * lda * 4 < ((int64_t)1 << 31) && 256 * ldb * 4 < ((int64_t)1 << 31)) {
+                const F32Tiles t = sp > 1 ? kF32Tiles128 : f32_tiles(M, N);
                 float* part = sp > 1 ? scratch : nullptr;
-                if (big) {
-                    const int tm4 = (int)((M + 255) / 256), tn4 = (int)((N + 255) / 256);
-#define SSM_F32_BIG(R)                                                                                          \
-    case R:                                                                                                     \
-        SSM_LAUNCH((gemm_f32_big<R, 256, 256, 4, 4>), dim3((unsigned)(tm4 * tn4)), dim3(1024), 0, s, (int)M,   \
-                   (int)N, (int)K, (const float*)A, lda, (const float*)B, ldb, (float*)C, ldc, tm4, tn4, part);  \
-        break;
-                    switch (role) {
-                        SSM_F32_BIG(kGemmInProj)
-                        SSM_F32_BIG(kGemmXProj)
-                        SSM_F32_BIG(kGemmDtProj)
-                        SSM_F32_BIG(kGemmOutProj)
-                        default: SSM_F32_BIG(kGemmGeneric)
-                    }
-#undef SSM_F32_BIG
-                    return hipGetLastError();
-                }
-                const dim3 grid((unsigned)(tm2 * tn2), (unsigned)sp);
-#define SSM_F32_BIG(R)                                                                                          \
-    case R:                                                                                                     \
-        SSM_LAUNCH((gemm_f32_big<R, 128, 128, 2, 4>), grid, dim3(512), 0, s, (int)M, (int)N, (int)K,            \
-                   (const float*)A, lda, (const float*)B, ldb, (float*)C, ldc, (int)tm2, (int)tn2, part);       \
-        break;
+                const float* fA = (const float*)A;
+                const float* fB = (const float*)B;
+                float* fC = (float*)C;
+#define SSM_F32_DMA(R)                                                                                         \
+    case R:                                                                                                    \
+        switch (t) {                                                                                           \
+            case kF32Tiles256: return run_dma_f32<R, 256, 256, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
+            case kF32Tiles256x224: return run_dma_f32<R, 256, 224, 2, 8, 1>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
+            case kF32Tiles128x224: return run_dma_f32<R, 128, 224, 2, 4, 1>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
+            default: return run_dma_f32<R, 128, 128, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s, sp, part); \
+        }
                 switch (role) {
-                    SSM_F32_BIG(kGemmInProj)
-                    SSM_F32_BIG(kGemmXProj)
-                    SSM_F32_BIG(kGemmDtProj)
-                    SSM_F32_BIG(kGemmOutProj)
-                    default: SSM_F32_BIG(kGemmGeneric)
+                    SSM_F32_DMA(kGemmInProj)
+                    SSM_F32_DMA(kGemmXProj)
+                    SSM_F32_DMA(kGemmDtProj)
+                    SSM_F32_DMA(kGemmOutProj)
+                    default: SSM_F32_DMA(kGemmGeneric)
                 }
-#undef SSM_F32_BIG
-                if (sp <= 1) return hipGetLastError();
-                if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-                KernelTimer kt("gemm.splitk_reduce", s);
-                const int64_t n4 = M * ((N + 3) / 4);
-                SSM_LAUNCH((splitk_reduce_kernel<true>), dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s,
-                           (const float*)part, sp, (int)M, (int)N, C, ldc);
-                return hipGetLastError();
+#undef SSM_F32_DMA
             }
         }
         const int tm = (int)((M + 63) / 64), tn = (int)((N + 63) / 64);
