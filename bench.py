@@ -1031,7 +1031,7 @@ def main():
     if not args.no_extras:
         others = {}
         if key == "c4" and act == "f32":
-            r, w2, _ = run_workload(B, torch, "c4", "bf16", max(1, min(args.steps, 3)), 1, drawn=to_bf16(drawn))
+            r, w2, _ = run_workload(B, torch, "c4", "bf16", max(1, min(args.steps, 3)), 2, drawn=to_bf16(drawn))
             others["c4_bf16"] = r
             del w2
             torch.cuda.empty_cache()
@@ -1040,7 +1040,7 @@ def main():
             if k == key:
                 continue
             a = synth.CONFIGS[CONFIG_KEYS[k]]["shape"].act
-            r, w2, _ = run_workload(B, torch, k, a, max(1, min(args.steps, 3)), 1, graph=(k in ("c1", "c3")),
+            r, w2, _ = run_workload(B, torch, k, a, max(1, min(args.steps, 3)), 2, graph=(k in ("c1", "c3")),
                                     keep_all=(k == "c1"))
             if k == "c1" and not args.no_next:
                 log("quantized exchange codecs on the 2.8B half shard's exchange tensors")
