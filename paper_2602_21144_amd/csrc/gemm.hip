@@ -207,14 +207,21 @@ template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
 // F32: the operands are float32 rows passed as bf16 rows of twice the length (K, lda and
 // ldb in bf16 units); the DMA and the LDS layout only move bytes, and each 16-byte fragment
 // (4 floats along k) feeds four v_mfma_f32_32x32x2_f32 instead of one bf16 MFMA.
-template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false, bool F32 = false>
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false, bool F32 = false,
+          bool MB16 = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
                                                               int64_t lda, const bf16* __restrict__ B, int64_t ldb,
                                                               void* __restrict__ Cp, int64_t ldc, int tiles_m,
                                                               int tiles_n, float* __restrict__ part) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int TM = WTM / 32, TN = WTN / 32;
+    // MFMA blocks: 32x32 (bf16 32x32x16 or fp32 32x32x2), or 16x16 (fp32 16x16x4: MB16)
+    static_assert(!MB16 || F32, "16x16 blocks for float32 operands");
+    constexpr int BLK = MB16 ? 16 : 32;
+    constexpr int TM = WTM / BLK, TN = WTN / BLK;
+    static_assert(TM * BLK == WTM && TN * BLK == WTN, "whole MFMA blocks per wave");
+    using AccT = typename std::conditional<MB16, f32x4, f32x16>::type;
+    constexpr int QG = MB16 ? 1 : 4;        // float4 groups of an accumulator
     constexpr int CPR = BK / 8;             // 16-byte chunks per row
     constexpr int RPB = 64 / CPR;           // rows per 1 KB DMA block
     // DMA blocks of one stage: BM / RPB activation blocks, then BN / RPB weight blocks. When
@@ -225,7 +232,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     constexpr int TBA = BM / RPB, TBT = (BM + BN) / RPB, QM = (TBT + NW - 1) / NW;
     constexpr int AG = EVEN ? BM / RPB / NW : 0, BG = EVEN ? BN / RPB / NW : 0;  // DMA blocks per wave per stage
     constexpr int OPS = EVEN ? AG + BG : QM;
-    constexpr int SUB = BK / 16;            // MFMA k-substeps per stage
+    constexpr int SUB = MB16 ? BK / 32 : BK / 16;  // MFMA k-substeps per stage (2 or 4 chunks of a row each)
     static_assert(NS >= 2 && BM % RPB == 0 && BN % RPB == 0, "tile");
     static_assert(EVEN ? (AG >= 1 && BG >= 1) : NS == 2, "uneven DMA blocks need the 2-deep ring");
     static_assert(SUB % 2 == 0, "fragment sets alternate within a tile");
@@ -298,30 +305,45 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         }
     };
 
-    f32x16 acc[TM][TN];
+    AccT acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < TN; ++j) acc[i][j] = AccT{};
     int arow[TM], brow[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * 32 + (lane & 31);
+    for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * BLK + (lane & (BLK - 1));
 #pragma unroll
-    for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * 32 + (lane & 31);
+    for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * BLK + (lane & (BLK - 1));
+    // lane l's output columns of float4 group g of a block (its row is l % BLK): the MFMA
+    // layouts with the weight fragment as the first operand
+    auto ocol = [&](int g) { return MB16 ? 4 * (lane >> 4) : 8 * g + 4 * (lane >> 5); };
 
     const int nk = K / BK;
     bf16x8 fa[2][TM], fb[2][TN];
     auto frag = [&](int stage, int s, int set) {
         const bf16* as = As[stage];
         const bf16* bs = Bs[stage];
-        const int c = s * 2 + (lane >> 5);
+        const int c = MB16 ? s * 4 + (lane >> 4) : s * 2 + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < TM; ++i) fa[set][i] = *(const bf16x8*)&as[arow[i] * BK + swz_k<BK>(arow[i], c) * 8];
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[set][j] = *(const bf16x8*)&bs[brow[j] * BK + swz_k<BK>(brow[j], c) * 8];
     };
     auto mfma = [&](int set) {
-        if constexpr (F32) {
+        if constexpr (MB16) {
+            // float32 operands on 16x16 blocks: lane group g = l / 16 takes chunk 4s + g, so
+            // MFMA u sums k = 16s + 4g + u over the four groups
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
+                                                                         __builtin_bit_cast(f32x4, fa[set][i])[u],
+                                                                         acc[i][j], 0, 0, 0);
+        } else if constexpr (F32) {
             // float32 operands: a 16-byte chunk holds 4 floats along k; lanes 0-31 take chunk
             // 2s, lanes 32-63 chunk 2s + 1, so MFMA u sums k = 8s + u and 8s + 4 + u
 #pragma unroll
@@ -400,12 +422,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
             if (wm * WTM >= pass * RB && wm * WTM < (pass + 1) * RB) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
-                    const int r = wm * WTM - pass * RB + i * 32 + (lane & 31);
+                    const int r = wm * WTM - pass * RB + i * BLK + (lane & (BLK - 1));
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
 #pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            const int col = wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+                        for (int g = 0; g < QG; ++g) {
+                            const int col = wn * WTN + j * BLK + ocol(g);
                             OT* q = st + r * BN + (((col / E16) ^ (r & 7)) * E16) + col % E16;
                             const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
                             const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
@@ -437,13 +459,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        const int m = m0 + wm * WTM + i * 32 + (lane & 31);
+        const int m = m0 + wm * WTM + i * BLK + (lane & (BLK - 1));
         if (m >= M) continue;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int n = n0 + wn * WTN + j * 32 + 8 * g + 4 * (lane >> 5);
+            for (int g = 0; g < QG; ++g) {
+                const int n = n0 + wn * WTN + j * BLK + ocol(g);
                 const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1];
                 const float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
                 if constexpr (SPLIT) {
@@ -538,17 +560,17 @@ hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, 
 
 // float32 operands on the DMA tiles: the rows are moved as bytes, so the kernel sees them as
 // bf16 rows of twice the length (K, lda, ldb doubled); only the MFMAs read them as floats
-template <int ROLE, int BM, int BN, int NS, int WM, int WN>
+template <int ROLE, int BM, int BN, int NS, int WM, int WN, bool MB16 = false>
 hipError_t run_dma_f32(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B, int64_t ldb,
                        float* C, int64_t ldc, hipStream_t s, int splits = 1, float* part = nullptr) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     if (splits <= 1) {
-        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, false, true>), dim3(tm * tn), dim3(64 * WM * WN),
+        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, false, true, MB16>), dim3(tm * tn), dim3(64 * WM * WN),
                    0, s, (int)M, (int)N, (int)(2 * K), (const bf16*)A, 2 * lda, (const bf16*)B, 2 * ldb, C, ldc, tm,
                    tn, nullptr);
         return hipGetLastError();
     }
-    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, true, true>), dim3(tm * tn, splits),
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, 64, NS, WM, WN, true, true, true, MB16>), dim3(tm * tn, splits),
                dim3(64 * WM * WN), 0, s, (int)M, (int)N, (int)(2 * K / splits), (const bf16*)A, 2 * lda,
                (const bf16*)B, 2 * ldb, C, ldc, tm, tn, part);
     if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
@@ -580,11 +602,12 @@ bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; 
 // Float32 tiles by the same kind of model: rounds of workgroups (one per CU; two for the 64 KB
 // ring of 128x128) times the work a CU does per round over the tile's measured per-CU MFMA
 // efficiency. On the hybrid shard's 2048-row chunks: 256x256 tiles (8 waves of 128x64) 0.91,
-// 256x224 (8 waves of 32x224) 0.93, 128x224 (4 waves of 32x224) 0.85, 128x128 (8 waves of
-// 64x32, two per CU) 0.89. The 224-wide tiles exist for outputs whose 256-wide tiles leave
-// part of a round empty: in_proj (2048 x 7168) takes 256 tiles of 256x224 where 256x256 gave
-// 224 (840 -> 720 us), out_proj (2048 x 3584) 256 tiles of 128x224 where 128x128 gave 448
-// over two slots per CU (430 -> 393 us).
+// 256x224 (8 waves of 32x224) 0.93, 128x224 (8 waves of 32x112 on 16x16 blocks) 0.91,
+// 128x128 (8 waves of 64x32, two per CU) 0.89. The 224-wide tiles exist for outputs whose
+// 256-wide tiles leave part of a round empty: in_proj (2048 x 7168) takes 256 tiles of 256x224
+// where 256x256 gave 224 (840 -> 720 us), out_proj (2048 x 3584) 256 tiles of 128x224 where
+// 128x128 gave 448 over two slots per CU (430 -> 368 us; 4 waves of 32x224, one per SIMD,
+// took 393 us; 64x112 wave tiles on 16x16 blocks for 256x224 spill).
 enum F32Tiles { kF32Tiles128 = 0, kF32Tiles256 = 1, kF32Tiles256x224 = 2, kF32Tiles128x224 = 3 };
 F32Tiles f32_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, int per_cu, double eff) {
@@ -593,7 +616,7 @@ F32Tiles f32_tiles(int64_t M, int64_t N) {
     };
     F32Tiles best = kF32Tiles128;
     double c = cost(128, 128, 2, 0.89);
-    const double c256 = cost(256, 256, 1, 0.91), c224 = cost(256, 224, 1, 0.93), c128x224 = cost(128, 224, 1, 0.85);
+    const double c256 = cost(256, 256, 1, 0.91), c224 = cost(256, 224, 1, 0.93), c128x224 = cost(128, 224, 1, 0.91);
     if (c256 < c) { c = c256; best = kF32Tiles256; }
     if (c224 < c) { c = c224; best = kF32Tiles256x224; }
     if (c128x224 < c) { c = c128x224; best = kF32Tiles128x224; }
@@ -914,7 +937,7 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
         switch (t) {                                                                                           \
             case kF32Tiles256: return run_dma_f32<R, 256, 256, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
             case kF32Tiles256x224: return run_dma_f32<R, 256, 224, 2, 8, 1>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
-            case kF32Tiles128x224: return run_dma_f32<R, 128, 224, 2, 4, 1>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
+            case kF32Tiles128x224: return run_dma_f32<R, 128, 224, 2, 4, 2, true>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
             default: return run_dma_f32<R, 128, 128, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s, sp, part); \
         }
                 switch (role) {
