@@ -147,22 +147,28 @@ def kernel_work(sh, kind, n, nseq):
             out["prefill.dt_round"] = ("hbm", T * R * 4 + T * R * 2)
         return out
     M = n
+
+    def proj(nbytes, flops):
+        # a decode projection: both its bytes and its flops; its roof over a whole step is the
+        # one that takes longer (work_by_role): float32 weights at 64 rows are MFMA-bound
+        return ("proj", (nbytes, flops))
+
     # dt_proj with the state step fused (its epilogue up to 64 sequences, the state-step
     # kernel above): weights, delta, B and C, u and z, g, state read + write
     state = ("hbm", E * R * s + M * R * 4 + M * 2 * N * 4 + 3 * M * E * s + 2 * M * E * N * 4 + E * (N + 2) * 4)
     if bf and K >= 2 and M <= 512:
         return {
             # in_proj with the conv window fused: weights, x_t, u and z out, history read + write
-            "decode.in_proj_conv": ("hbm", 2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
-                                    + E * (K + 1) * s),
-            "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
+            "decode.in_proj_conv": proj(2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
+                                        + E * (K + 1) * s, 2.0 * M * 2 * E * dm),
+            "decode.x_proj": proj(W * E * s + M * E * s + M * W * 4, 2.0 * M * W * E),
             "decode.dt_proj_state": state,
-            "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
-    return {"decode.in_proj": ("hbm", 2 * E * dm * s + M * dm * s + M * 2 * E * s),
+            "decode.out_proj": proj(dm * E * s + M * E * s + M * dm * s, 2.0 * M * dm * E)}
+    return {"decode.in_proj": proj(2 * E * dm * s + M * dm * s + M * 2 * E * s, 2.0 * M * 2 * E * dm),
             "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
-            "decode.x_proj": ("hbm", W * E * s + M * E * s + M * W * 4),
+            "decode.x_proj": proj(W * E * s + M * E * s + M * W * 4, 2.0 * M * W * E),
             "decode.dt_proj_state": state,
-            "decode.out_proj": ("hbm", dm * E * s + M * E * s + M * dm * s)}
+            "decode.out_proj": proj(dm * E * s + M * E * s + M * dm * s, 2.0 * M * dm * E)}
 
 
 def role_of(name):
@@ -300,11 +306,23 @@ class Workload:
         return self.B.take_status(self.wsp[0]) == 0 and self.B.take_status(self.wsd[0]) == 0
 
     def work_by_role(self):
-        """role -> (roof, [work of each launch in schedule order]) over one step."""
-        out = {}
+        """role -> (roof, [work of each launch in schedule order]) over one step. A decode
+        projection takes the roof on which the step's launches take longer in all: their
+        bytes at the HBM peak or their flops at the MFMA peak."""
+        out, proj = {}, {}
         for q in self.phases:
             for role, (roof, amt) in kernel_work(self.sh, q["kind"], q["n"], q["nseq"]).items():
-                out.setdefault(role, (roof, []))[1].append(float(amt))
+                if roof == "proj":
+                    proj.setdefault(role, []).append(amt)
+                else:
+                    out.setdefault(role, (roof, []))[1].append(float(amt))
+        for role, amts in proj.items():
+            t_hbm = sum(b for b, _ in amts) / (PEAK_HBM_GBS * 1e9)
+            t_mfma = sum(f for _, f in amts) / (PEAK_TFLOPS[self.sh.act] * 1e12)
+            if t_mfma > t_hbm:
+                out[role] = ("mfma", [float(f) for _, f in amts])
+            else:
+                out[role] = ("hbm", [float(b) for b, _ in amts])
         return out
 
 

@@ -828,26 +828,27 @@ hipError_t launch_skinny32(const SkinnyArgs& p, hipStream_t s) {
 
 // Float32 operands, at most 64 rows (the decode projections of a float32 layer): the
 // weight stream is 4 bytes per element, so moving it in whole cache lines matters as much as
-// in the bf16 kernel above. A workgroup owns 16 output columns; its NW waves split K into
-// runs of 32-wide stages (128 bytes of a float32 row). Each stage arrives by whole-line
-// loads, 8 rows x 128 bytes per instruction (16 weight rows, then the 8 XB activation
-// rows), NST stages ahead in registers; it is written to a wave-private LDS buffer
+// in the bf16 kernel above. A workgroup owns CT tiles of 16 output columns; its NW waves
+// split K into runs of 32-wide stages (128 bytes of a float32 row). Each stage arrives by
+// whole-line loads, 8 rows x 128 bytes per instruction (16 CT weight rows, then the 8 XB
+// activation rows), NST stages ahead in registers; it is written to a wave-private LDS buffer
 // (XOR-swizzled 16-byte chunks) and read back as v_mfma_f32_16x16x4_f32 operands: lane l
 // takes the float4 of chunk 4 j + l / 16 of row l % 16, and MFMA t of group j uses
 // component t, so operand and weight agree on every k. Rows past M or N read as zero. The
 // waves' partial tiles are summed through the same LDS at the end.
 constexpr int kF32Stage = 32;  // k per stage: one 128-byte line of a float32 row
 
-template <int ROLE, int NW, int NST, int XB>
+template <int ROLE, int NW, int NST, int XB, int CT = 1>
 __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, int K, const float* __restrict__ A,
                                                                   int64_t lda, const float* __restrict__ B,
                                                                   int64_t ldb, float* __restrict__ C, int64_t ldc) {
-    constexpr int ROWS = 16 + 8 * XB;          // LDS rows of one stage: weights, then activations
+    constexpr int WR = 16 * CT;                // weight rows of a workgroup (CT 16-column tiles)
+    constexpr int ROWS = WR + 8 * XB;          // LDS rows of one stage: weights, then activations
     constexpr int MT = (8 * XB + 15) / 16;     // 16-row output tiles
     constexpr int WBUF = ROWS * 128;           // bytes of a wave's buffer
-    static_assert(WBUF >= MT * 16 * 16 * 4, "the partial tile fits the wave's buffer");
+    static_assert(WBUF >= CT * MT * 16 * 16 * 4, "the partial tiles fit the wave's buffer");
     __shared__ __attribute__((aligned(16))) char tr[NW][WBUF];
-    const int n0 = blockIdx.x * 16;
+    const int n0 = blockIdx.x * WR;
     // row tiles of 8 XB activation rows along blockIdx.y (one tile when the grid has one row)
     const int m0 = blockIdx.y * 8 * XB;
     A += (int64_t)m0 * lda;
@@ -857,19 +858,20 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
     const int nall = K / kF32Stage;
     const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
     const int lr = lane >> 3, lp = lane & 7;
-    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)(min(16, N - n0) * ldb * 4));
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(B + (int64_t)n0 * ldb, (uint32_t)(min(WR, N - n0) * ldb * 4));
     const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(A, (uint32_t)(M * lda * 4));
     const uint32_t kb = (uint32_t)(sb * kF32Stage + lp * 4) * 4;
-    const uint32_t wo0 = (uint32_t)(lr * ldb) * 4 + kb, wo1 = (uint32_t)((8 + lr) * ldb) * 4 + kb;
-    uint32_t xo[XB];
+    uint32_t wo[2 * CT], xo[XB];
+#pragma unroll
+    for (int q = 0; q < 2 * CT; ++q) wo[q] = (uint32_t)((8 * q + lr) * ldb) * 4 + kb;
 #pragma unroll
     for (int q = 0; q < XB; ++q) xo[q] = (uint32_t)((8 * q + lr) * lda) * 4 + kb;
 
-    u32x4 w0[NST], w1[NST], xv[NST][XB];
+    u32x4 wv[NST][2 * CT], xv[NST][XB];
     auto issue = [&](int j, int st) {  // stage st of this wave's run into register slot j
         const bool ok = st < nst;
-        w0[j] = buffer_load16(rb, ok ? wo0 + st * 128 : kOffOutOfRange);
-        w1[j] = buffer_load16(rb, ok ? wo1 + st * 128 : kOffOutOfRange);
+#pragma unroll
+        for (int q = 0; q < 2 * CT; ++q) wv[j][q] = buffer_load16(rb, ok ? wo[q] + st * 128 : kOffOutOfRange);
 #pragma unroll
         for (int q = 0; q < XB; ++q) xv[j][q] = buffer_load16(ra, ok ? xo[q] + st * 128 : kOffOutOfRange);
     };
@@ -878,47 +880,59 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
 
     char* t = tr[wave];
     const int wr = lane & 15, cg = lane >> 4;
-    f32x4 acc[MT];
+    f32x4 acc[CT][MT];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) acc[i] = f32x4{};
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[ct][i] = f32x4{};
     for (int base = 0; base < nst; base += NST) {
 #pragma unroll
         for (int j = 0; j < NST; ++j) {
             if (base + j < nst) {
-                *(u32x4*)(t + lr * 128 + gemv_swz(lr, lp) * 16) = w0[j];
-                *(u32x4*)(t + (8 + lr) * 128 + gemv_swz(8 + lr, lp) * 16) = w1[j];
+#pragma unroll
+                for (int q = 0; q < 2 * CT; ++q)
+                    *(u32x4*)(t + (8 * q + lr) * 128 + gemv_swz(8 * q + lr, lp) * 16) = wv[j][q];
 #pragma unroll
                 for (int q = 0; q < XB; ++q)
-                    *(u32x4*)(t + (16 + 8 * q + lr) * 128 + gemv_swz(16 + 8 * q + lr, lp) * 16) = xv[j][q];
+                    *(u32x4*)(t + (WR + 8 * q + lr) * 128 + gemv_swz(WR + 8 * q + lr, lp) * 16) = xv[j][q];
                 issue(j, base + j + NST);  // refill the slot just written out
 #pragma unroll
                 for (int g = 0; g < 2; ++g) {
                     const int c = 4 * g + cg;
-                    const f32x4 wf = *(const f32x4*)(t + wr * 128 + gemv_swz(wr, c) * 16);
+                    f32x4 xf[MT];
 #pragma unroll
                     for (int i = 0; i < MT; ++i) {
                         // rows past the staged 8 XB activation rows repeat earlier ones; their
                         // outputs lie past M and are never stored
-                        const int ar = 16 + ((16 * i + wr) % (8 * XB));
-                        const f32x4 xf = *(const f32x4*)(t + ar * 128 + gemv_swz(ar, c) * 16);
+                        const int ar = WR + ((16 * i + wr) % (8 * XB));
+                        xf[i] = *(const f32x4*)(t + ar * 128 + gemv_swz(ar, c) * 16);
+                    }
 #pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[u], wf[u], acc[i], 0, 0, 0);
+                    for (int ct = 0; ct < CT; ++ct) {
+                        const int rw = 16 * ct + wr;
+                        const f32x4 wf = *(const f32x4*)(t + rw * 128 + gemv_swz(rw, c) * 16);
+#pragma unroll
+                        for (int i = 0; i < MT; ++i)
+#pragma unroll
+                            for (int u = 0; u < 4; ++u)
+                                acc[ct][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xf[i][u], wf[u], acc[ct][i], 0, 0, 0);
                     }
                 }
             }
         }
     }
-    // lane l holds column l % 16 and rows 16 i + 4 (l / 16) + r of tile i
+    // lane l holds column l % 16 and rows 16 i + 4 (l / 16) + r of tile (ct, i)
     __syncthreads();
     float* red = (float*)t;
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[(16 * i + 4 * cg + r) * 16 + wr] = acc[i][r];
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[((ct * MT + i) * 16 + 4 * cg + r) * 16 + wr] = acc[ct][i][r];
     __syncthreads();
-    for (int e = threadIdx.x; e < MT * 256; e += NW * 64) {
-        const int m = e >> 4, n = n0 + (e & 15);
+    for (int e = threadIdx.x; e < CT * MT * 256; e += NW * 64) {
+        const int ct = e / (MT * 256), m = (e / 16) % (MT * 16), n = n0 + 16 * ct + (e & 15);
         if (m >= M || n >= N) continue;
         float v = 0.0f;
 #pragma unroll
@@ -931,6 +945,18 @@ template <int ROLE, int NW>
 hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
                                 float* C, int64_t ldc, hipStream_t s) {
     const dim3 grid((unsigned)((N + 15) / 16)), block(NW * 64);
+    // 33..64 rows over wide outputs: two 16-column tiles per workgroup, so each staged block
+    // of activation rows serves 32 columns (half the activation re-reads; the hybrid shard's
+    // float32 in_proj of 64 rows 29.8 -> 28.5 us, where its 3.3 GFLOP take 21 us at the fp32
+    // MFMA peak)
+    if constexpr (NW == 8) {
+        if (M > 32 && M <= 64 && (N + 31) / 32 >= 128) {
+            const dim3 g2((unsigned)((N + 31) / 32));
+            if (M <= 48) SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 6, 2>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
+            else SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 8, 2>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
+            return hipGetLastError();
+        }
+    }
 #define SSM_F32S(XB, NST) \
     SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, NST, XB>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc)
     if (M <= 8) SSM_F32S(1, 3);
