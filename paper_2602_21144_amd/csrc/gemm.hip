@@ -608,7 +608,7 @@ bool dma_big_tiles(int64_t M, int64_t N) { return dma_tiles(M, N) != kTiles128; 
 // where 256x256 gave 224 (840 -> 720 us), out_proj (2048 x 3584) 256 tiles of 128x224 where
 // 128x128 gave 448 over two slots per CU (430 -> 368 us; 4 waves of 32x224, one per SIMD,
 // took 393 us; 64x112 wave tiles on 16x16 blocks for 256x224 spill).
-enum F32Tiles { kF32Tiles128 = 0, kF32Tiles256 = 1, kF32Tiles256x224 = 2, kF32Tiles128x224 = 3 };
+enum F32Tiles { kF32Tiles128 = 0, kF32Tiles256 = 1, kF32Tiles256x224 = 2, kF32Tiles128x224 = 3, kF32Tiles64 = 4 };
 F32Tiles f32_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, int per_cu, double eff) {
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn), slots = 256 * per_cu;
@@ -874,8 +874,8 @@ hipError_t launch_round_bf16_rows(const float* a, int64_t lda, void* o, int64_t 
 size_t gemm_splitk_bytes(int64_t M, int64_t N, int64_t K, int a_dt, int b_dt, GemmRole role) {
     // float32 operands on 128x128 tiles (more than the 64 rows of the streamed kernel)
     if (a_dt == SSM_F32 && b_dt == SSM_F32) {
-        if (M <= 64 || N == 0) return 0;
-        const int sp = f32_slices(((M + 127) / 128) * ((N + 127) / 128), K);
+        if (M <= 64 || N == 0 || f32_slices(((M + 127) / 128) * ((N + 127) / 128), K) <= 1) return 0;
+        const int sp = f32_slices(((M + 63) / 64) * ((N + 63) / 64), K);
         return sp > 1 ? (size_t)sp * M * N * 4 : 0;
     }
     // mirrors the dispatch below: the DMA paths with bf16 operands and K % 64 == 0
@@ -919,15 +919,18 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
 #undef SSM_F32_GEMV
             return hipGetLastError();
         }
-        // prefill sizes on the DMA tiles (float32 rows moved as bytes, run_dma_f32): K-slices of
-        // 128x128 tiles when the output has few tiles (x_proj), else the tile shape of least
-        // modelled time (f32_tiles)
+        // prefill sizes on the DMA tiles (float32 rows moved as bytes, run_dma_f32): when the
+        // output has few 128x128 tiles (x_proj: 32), K-slices of 64x64 tiles (4 waves of 32x32,
+        // a 4-deep ring of 16 KB stages, two workgroups per CU), whose partials are a quarter of
+        // those of 128x128 slices for as many workgroups; else the tile shape of least modelled
+        // time (f32_tiles)
         {
             const int64_t tm2 = (M + 127) / 128, tn2 = (N + 127) / 128;
-            const int sp = fit_slices(f32_slices(tm2 * tn2, K), M, N, scratch_bytes);
-            if (K % kF32BK == 0 && (tm2 * tn2 >= 256 || sp > 1) && lda % 4 == 0 && ldb % 4 == 0 && al16(A) &&
+            const bool few = f32_slices(tm2 * tn2, K) > 1;
+            const int sp = few ? fit_slices(f32_slices(((M + 63) / 64) * ((N + 63) / 64), K), M, N, scratch_bytes) : 1;
+            if (K % kF32BK == 0 && (tm2 * tn2 >= 256 || few) && lda % 4 == 0 && ldb % 4 == 0 && al16(A) &&
                 al16(B) && al16(C) && 256 * lda * 4 < ((int64_t)1 << 31) && 256 * ldb * 4 < ((int64_t)1 << 31)) {
-                const F32Tiles t = sp > 1 ? kF32Tiles128 : f32_tiles(M, N);
+                const F32Tiles t = few ? kF32Tiles64 : f32_tiles(M, N);
                 float* part = sp > 1 ? scratch : nullptr;
                 const float* fA = (const float*)A;
                 const float* fB = (const float*)B;
@@ -938,7 +941,8 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const void* A, int64_
             case kF32Tiles256: return run_dma_f32<R, 256, 256, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
             case kF32Tiles256x224: return run_dma_f32<R, 256, 224, 2, 8, 1>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
             case kF32Tiles128x224: return run_dma_f32<R, 128, 224, 2, 4, 2, true>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
-            default: return run_dma_f32<R, 128, 128, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s, sp, part); \
+            case kF32Tiles64: return run_dma_f32<R, 64, 64, 4, 2, 2>(M, N, K, fA, lda, fB, ldb, fC, ldc, s, sp, part); \
+            default: return run_dma_f32<R, 128, 128, 2, 2, 4>(M, N, K, fA, lda, fB, ldb, fC, ldc, s); \
         }
                 switch (role) {
                     SSM_F32_DMA(kGemmInProj)
