@@ -407,33 +407,32 @@ constexpr int kDtCh = 16, kDtSeq = 4;  // tiles of the fp32 / general state-step
 constexpr int kDtSeqM = 16;            // sequences per tile of the bf16 MFMA state-step kernel
 constexpr int kDtSpw = 2;              // sequences per wave of that kernel
 
-// bf16 and dt_rank a multiple of 32 (up to 512): a workgroup takes 16 channels of 16
-// sequences, SPW sequences per wave (four lanes per (sequence, channel), a float4 of states
-// each: every state load and store instruction covers 1 KB contiguous). The step is bound by
-// the state bytes in flight per CU over the memory latency; for 256 sequences of 1280
-// channels one sequence per wave took 13.1 us, two 12.5 us, four 14.3 us. The workgroup's
-// 16 x 16 tile of dt is the product delta[16 sequences][R] x W_dt[16 channels][R]^T:
-// k-chunk k of the R / 32 is one v_mfma_f32_16x16x32_bf16 on wave k % (waves); the waves'
-// partial tiles meet in LDS, every thread adds them in wave order and rounds dt to bf16 as
-// dt_proj stores it. Each workgroup fetches its 16 delta rows and 16 W_dt rows once. (4 x 16
-// tiles fetched the W_dt rows once per 4 sequences, about as many L2 bytes as the states
-// themselves: 15.5 us.)
-template <int NK, int SPW>
+// bf16 and dt_rank a multiple of 32 (up to 512): a workgroup takes CT tiles of 16 channels
+// (adjacent, so they share the delta rows and B, C) of 16 sequences, SPW sequences per wave
+// (four lanes per (sequence, channel), a float4 of states each: every state load and store
+// instruction covers 1 KB contiguous). The step is bound by the state bytes in flight over the
+// memory latency; for 256 sequences of 1280 channels one sequence per wave took 13.1 us, two
+// 12.5 us, four 14.3 us; two tiles per workgroup (640 workgroups, one round at 76 VGPRs and
+// three workgroups per CU, instead of 1280 in 1.25 rounds) 11.7 us. Each tile's 16 x 16 dt is
+// the product delta[16 sequences][R] x W_dt[16 channels][R]^T: k-chunk k of the R / 32 is one
+// v_mfma_f32_16x16x32_bf16 on wave k % (waves); the waves' partial tiles meet in LDS, every
+// thread adds them in wave order and rounds dt to bf16 as dt_proj stores it. Each workgroup
+// fetches its 16 delta rows and its W_dt rows once. (4 x 16 tiles fetched the W_dt rows once
+// per 4 sequences, about as many L2 bytes as the states themselves: 15.5 us.)
+template <int NK, int SPW, int CT>
 __global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(ScanArgs a) {
     constexpr int NWV = kDtSeqM / SPW;         // waves
     constexpr int KPW = (NK + NWV - 1) / NWV;  // k-chunks per wave
     constexpr int NP = NK < NWV ? NK : NWV;    // partial tiles
-    __shared__ float dt_part[NP][kDtSeqM][kDtCh];
-    const int ctiles = a.E / kDtCh;
-    const int tb = blockIdx.x / ctiles, tc = blockIdx.x % ctiles;
+    __shared__ float dt_part[CT][NP][kDtSeqM][kDtCh];
+    const int cgroups = a.E / (kDtCh * CT);
+    const int tb = blockIdx.x / cgroups, tg = blockIdx.x % cgroups;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int it = lane >> 2, q = lane & 3;  // channel tc * 16 + it; states 4q .. 4q + 3
-    const int c = tc * kDtCh + it;
+    const int it = lane >> 2, q = lane & 3;  // channel (tg CT + t) 16 + it of tile t; states 4q .. 4q + 3
     int bsq[SPW], slot[SPW];
     bool live[SPW], sok[SPW];
-    float4 Bq[SPW], Cq[SPW], h[SPW];
-    float u[SPW], z[SPW];
-    float4* hp[SPW];
+    float4 Bq[SPW], Cq[SPW], h[CT][SPW];
+    float u[CT][SPW], z[CT][SPW];
     // the slot indices first: the state loads wait for them alone
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
@@ -442,49 +441,54 @@ __global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(
         bsq[j] = live[j] ? bb : 0;
         slot[j] = a.slot[bsq[j]];
     }
-    // the dt tile's operands, issued before the states so that the MFMAs wait for them and
-    // not for the states (which stay in flight across the dt tile and the barrier). Chunks
-    // k = wave + NWV kk: lane l takes delta row l % 16 (rows past the batch zero) and W_dt
-    // row l % 16, columns 32 k + 8 (l / 16) .. + 7
+    // the dt tiles' operands, issued before the states so that the MFMAs wait for them and
+    // not for the states (which stay in flight across the dt tiles and the barrier). Chunks
+    // k = wave + NWV kk: lane l takes delta row l % 16 (rows past the batch zero; shared by
+    // the CT tiles) and W_dt row l % 16 of each tile, columns 32 k + 8 (l / 16) .. + 7
     const bool mw = wave < NK;
     const int r = lane & 15, kq = (lane >> 4) * 8;
     const bool rok = tb * kDtSeqM + r < a.nseq;
     // every wave issues them (waves past the last chunk re-read chunk 0, unused), so that no
     // branch hides the loads' count from the compiler's counter waits
     float4 d0[KPW], d1[KPW];
-    bf16x8 wf[KPW];
+    bf16x8 wf[CT][KPW];
     {
         const float* drow = a.xdbl + (int64_t)(rok ? tb * kDtSeqM + r : 0) * a.ld_xdbl;
-        const bf16* wrow = (const bf16*)a.w_dt + (int64_t)(tc * kDtCh + r) * a.R;
 #pragma unroll
         for (int kk = 0; kk < KPW; ++kk) {
             const int k = wave + NWV * kk < NK ? wave + NWV * kk : 0;  // past the last chunk: re-read, not added
             d0[kk] = *(const float4*)(drow + 32 * k + kq);
             d1[kk] = *(const float4*)(drow + 32 * k + kq + 4);
-            wf[kk] = *(const bf16x8*)(wrow + 32 * k + kq);
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                wf[t][kk] = *(const bf16x8*)((const bf16*)a.w_dt + (int64_t)((tg * CT + t) * kDtCh + r) * a.R + 32 * k + kq);
         }
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < SPW; ++j) {
         sok[j] = slot[j] >= 0 && slot[j] < a.S;
-        hp[j] = (float4*)(a.pool + ((int64_t)(sok[j] ? slot[j] : 0) * a.E + c) * kN) + q;
-        h[j] = *hp[j];
+#pragma unroll
+        for (int t = 0; t < CT; ++t)
+            h[t][j] = ((const float4*)(a.pool + ((int64_t)(sok[j] ? slot[j] : 0) * a.E + (tg * CT + t) * kDtCh + it) * kN))[q];
     }
     __builtin_amdgcn_sched_barrier(0);
     if (mw) {
-        f32x4 acc = f32x4{};
 #pragma unroll
-        for (int kk = 0; kk < KPW; ++kk) {
-            bf16x8 af;
-            af[0] = (bf16)d0[kk].x; af[1] = (bf16)d0[kk].y; af[2] = (bf16)d0[kk].z; af[3] = (bf16)d0[kk].w;
-            af[4] = (bf16)d1[kk].x; af[5] = (bf16)d1[kk].y; af[6] = (bf16)d1[kk].z; af[7] = (bf16)d1[kk].w;
-            if (!rok || wave + NWV * kk >= NK) af = bf16x8{};
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[kk], acc, 0, 0, 0);
+        for (int t = 0; t < CT; ++t) {
+            f32x4 acc = f32x4{};
+#pragma unroll
+            for (int kk = 0; kk < KPW; ++kk) {
+                bf16x8 af;
+                af[0] = (bf16)d0[kk].x; af[1] = (bf16)d0[kk].y; af[2] = (bf16)d0[kk].z; af[3] = (bf16)d0[kk].w;
+                af[4] = (bf16)d1[kk].x; af[5] = (bf16)d1[kk].y; af[6] = (bf16)d1[kk].z; af[7] = (bf16)d1[kk].w;
+                if (!rok || wave + NWV * kk >= NK) af = bf16x8{};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[t][kk], acc, 0, 0, 0);
+            }
+            // lane l holds sequences 4 (l / 16) + j of the tile, channel l % 16
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dt_part[t][wave][4 * (lane >> 4) + j][r] = acc[j];
         }
-        // lane l holds sequences 4 (l / 16) + j of the tile, channel l % 16
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dt_part[wave][4 * (lane >> 4) + j][r] = acc[j];
     }
     // the operands of the output alone, in flight across the barrier
 #pragma unroll
@@ -492,42 +496,50 @@ __global__ __launch_bounds__(64 * kDtSeqM / SPW) void decode_dt_ssm_mfma_kernel(
         const float* xb = a.xdbl + (int64_t)bsq[j] * a.ld_xdbl + a.R;
         Bq[j] = ((const float4*)xb)[q];
         Cq[j] = ((const float4*)(xb + kN))[q];
-        u[j] = (float)((const bf16*)a.u)[(int64_t)bsq[j] * a.E + c];
-        z[j] = (float)((const bf16*)a.z)[(int64_t)bsq[j] * a.ld_z + c];
+#pragma unroll
+        for (int t = 0; t < CT; ++t) {
+            const int c = (tg * CT + t) * kDtCh + it;
+            u[t][j] = (float)((const bf16*)a.u)[(int64_t)bsq[j] * a.E + c];
+            z[t][j] = (float)((const bf16*)a.z)[(int64_t)bsq[j] * a.ld_z + c];
+        }
     }
-    const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
-    const float bdt = a.b_dt[c], Dc = a.D[c];
     __syncthreads();
-    const float av[4] = {al.x, al.y, al.z, al.w};
 #pragma unroll
-    for (int j = 0; j < SPW; ++j) {
-        const int ts = SPW * wave + j;
-        float dsum = dt_part[0][ts][it];
+    for (int t = 0; t < CT; ++t) {
+        const int c = (tg * CT + t) * kDtCh + it;
+        const float4 al = ((const float4*)(a.A_log + (int64_t)c * kN))[q];
+        const float bdt = a.b_dt[c], Dc = a.D[c];
+        const float av[4] = {al.x, al.y, al.z, al.w};
 #pragma unroll
-        for (int k = 1; k < NP; ++k) dsum += dt_part[k][ts][it];
-        const float dt = (float)(bf16)dsum;  // stored in bf16 as dt_proj's output
-        const float delta = softplus_f(dt + bdt);
-        const float du = delta * u[j];
-        const float hv[4] = {h[j].x, h[j].y, h[j].z, h[j].w};
-        const float bv[4] = {Bq[j].x, Bq[j].y, Bq[j].z, Bq[j].w}, cv[4] = {Cq[j].x, Cq[j].y, Cq[j].z, Cq[j].w};
-        float hn[4], y = 0.0f;
+        for (int j = 0; j < SPW; ++j) {
+            const int ts = SPW * wave + j;
+            float dsum = dt_part[t][0][ts][it];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
-            y += cv[i] * hn[i];
-        }
-        y += __shfl_xor(y, 1);
-        y += __shfl_xor(y, 2);
-        if (!live[j]) continue;
-        if (!sok[j]) {
-            if (q == 0) {
-                atomicOr(a.status, SSM_STATUS_BAD_SLOT);
-                ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)0.0f;
+            for (int k = 1; k < NP; ++k) dsum += dt_part[t][k][ts][it];
+            const float dt = (float)(bf16)dsum;  // stored in bf16 as dt_proj's output
+            const float delta = softplus_f(dt + bdt);
+            const float du = delta * u[t][j];
+            const float hv[4] = {h[t][j].x, h[t][j].y, h[t][j].z, h[t][j].w};
+            const float bv[4] = {Bq[j].x, Bq[j].y, Bq[j].z, Bq[j].w}, cv[4] = {Cq[j].x, Cq[j].y, Cq[j].z, Cq[j].w};
+            float hn[4], y = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                hn[i] = fast_exp2(delta * (-__expf(av[i]) * kLog2e)) * hv[i] + du * bv[i];
+                y += cv[i] * hn[i];
             }
-            continue;
+            y += __shfl_xor(y, 1);
+            y += __shfl_xor(y, 2);
+            if (!live[j]) continue;
+            if (!sok[j]) {
+                if (q == 0) {
+                    atomicOr(a.status, SSM_STATUS_BAD_SLOT);
+                    ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)0.0f;
+                }
+                continue;
+            }
+            ((float4*)(a.pool + ((int64_t)slot[j] * a.E + c) * kN))[q] = make_float4(hn[0], hn[1], hn[2], hn[3]);
+            if (q == 0) ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)((y + Dc * u[t][j]) * silu_f(z[t][j]));
         }
-        *hp[j] = make_float4(hn[0], hn[1], hn[2], hn[3]);
-        if (q == 0) ((bf16*)a.g)[(int64_t)bsq[j] * a.E + c] = (bf16)((y + Dc * u[j]) * silu_f(z[j]));
     }
 }
 
@@ -709,12 +721,15 @@ hipError_t launch_decode_dt_ssm(const ScanArgs& a, bool bf, hipStream_t s) {
         ((uintptr_t)a.w_dt & 15) != 0)
         return hipErrorNotSupported;
     if (bf && a.R % 32 == 0 && a.R <= 16 * 32) {
-        const dim3 g16((unsigned)(((a.nseq + kDtSeqM - 1) / kDtSeqM) * (a.E / kDtCh))), b16(64 * kDtSeqM / kDtSpw);
+        // two 16-channel tiles per workgroup: E is a multiple of 64 (checked with the shape)
+        constexpr int CT = 2;
+        if (a.E % (CT * kDtCh) != 0) return hipErrorNotSupported;
+        const dim3 g16((unsigned)(((a.nseq + kDtSeqM - 1) / kDtSeqM) * (a.E / (kDtCh * CT)))), b16(64 * kDtSeqM / kDtSpw);
         switch (a.R / 32) {
-#define SSM_DTM(NK) case NK: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<NK, kDtSpw>), g16, b16, 0, s, a); break;
+#define SSM_DTM(NK) case NK: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<NK, kDtSpw, CT>), g16, b16, 0, s, a); break;
             SSM_DTM(1) SSM_DTM(2) SSM_DTM(3) SSM_DTM(4) SSM_DTM(5) SSM_DTM(6) SSM_DTM(7) SSM_DTM(8)
             SSM_DTM(9) SSM_DTM(10) SSM_DTM(11) SSM_DTM(12) SSM_DTM(13) SSM_DTM(14) SSM_DTM(15)
-            default: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<16, kDtSpw>), g16, b16, 0, s, a); break;
+            default: SSM_LAUNCH((decode_dt_ssm_mfma_kernel<16, kDtSpw, CT>), g16, b16, 0, s, a); break;
 #undef SSM_DTM
         }
         return hipGetLastError();
