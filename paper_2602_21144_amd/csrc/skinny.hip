@@ -400,7 +400,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
             const int i = threadIdx.x + j * NW * 64;
             nwr[j] = i < p.K / 4 ? ((const float4*)p.nrm_w)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        if (threadIdx.x < p.M * p.nrm_G) ssq = p.nrm_sumsq[threadIdx.x];
+        if ((int)threadIdx.x < p.M * p.nrm_G) ssq = p.nrm_sumsq[threadIdx.x];
         __builtin_amdgcn_sched_barrier(0);
     }
     u32x4 w0[NST], w1[NST], xv[NST][XB];
@@ -425,7 +425,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_gemv_kernel(SkinnyArgs p) {
             const int i = threadIdx.x + j * NW * 64;
             if (i < p.K / 4) *(float4*)&nrm_w[4 * i] = nwr[j];
         }
-        if (threadIdx.x < p.M * p.nrm_G) nrm_inv[threadIdx.x] = 1.0f / sqrtf(ssq / (float)p.nrm_gsize + p.nrm_eps);
+        if ((int)threadIdx.x < p.M * p.nrm_G) nrm_inv[threadIdx.x] = 1.0f / sqrtf(ssq / (float)p.nrm_gsize + p.nrm_eps);
         __syncthreads();
     }
     // the inverse RMS of this lane's activation rows (rows past M: 0) for one group per row
