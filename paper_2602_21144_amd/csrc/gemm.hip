@@ -7,6 +7,7 @@
 // fp32 accumulation; fp32 path: v_mfma_f32_16x16x4_f32.
 #include <algorithm>
 #include <type_traits>
+#include <utility>
 
 #include "common.h"
 
@@ -183,12 +184,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt(int M, int N, int K,
     }
 }
 
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F> __device__ __forceinline__ void static_for(F&& f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
 // bf16 operands, K a multiple of BK: tiles move global -> LDS on the DMA path
 // (buffer_load_dwordx4 ... lds: each lane writes 16 bytes at its lane slot of a 1 KB LDS
 // block), so there are no staging registers and no ds_write instructions. A lane picks
 // the global chunk that belongs at its slot under the XOR swizzle. The LDS holds a ring
-// of NS stages: tile k+NS-1 is in flight while tile k is multiplied, which covers
-// NS-1 tiles of MFMA time of memory latency. The DMA is issued from inline assembly
+// of NS stages, NS-1 tiles ahead of the one being multiplied (two schedules, below). The
+// DMA is issued from inline assembly
 // (M0 = LDS destination) and its completion is awaited by explicit vmcnt waits, so the
 // compiler does not serialise the prefetch behind each tile's LDS reads. Rows past M
 // or N are clamped to a valid row (their results are never stored). Fragments of
@@ -207,16 +217,17 @@ template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
 // F32: the operands are float32 rows passed as bf16 rows of twice the length (K, lda and
 // ldb in bf16 units); the DMA and the LDS layout only move bytes, and each 16-byte fragment
 // (4 floats along k) feeds four v_mfma_f32_32x32x2_f32 instead of one bf16 MFMA.
+// MB16: 16x16 MFMA blocks. FINE: the second, fully ordered schedule of the k loop.
 template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false, bool F32 = false,
-          bool MB16 = false>
+          bool MB16 = false, bool FINE = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
                                                               int64_t lda, const bf16* __restrict__ B, int64_t ldb,
                                                               void* __restrict__ Cp, int64_t ldc, int tiles_m,
                                                               int tiles_n, float* __restrict__ part) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
-    // MFMA blocks: 32x32 (bf16 32x32x16 or fp32 32x32x2), or 16x16 (fp32 16x16x4: MB16)
-    static_assert(!MB16 || F32, "16x16 blocks for float32 operands");
+    // MFMA blocks: 32x32 (bf16 32x32x16 or fp32 32x32x2), or 16x16 (MB16: bf16 16x16x32 or
+    // fp32 16x16x4)
     constexpr int BLK = MB16 ? 16 : 32;
     constexpr int TM = WTM / BLK, TN = WTN / BLK;
     static_assert(TM * BLK == WTM && TN * BLK == WTN, "whole MFMA blocks per wave");
@@ -310,11 +321,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = AccT{};
-    int arow[TM], brow[TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * BLK + (lane & (BLK - 1));
-#pragma unroll
-    for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * BLK + (lane & (BLK - 1));
+    // a lane's fragment rows are wm * WTM + i * BLK + lane % BLK: the block offsets are
+    // multiples of 16 rows, which leave the swizzle key (row bits 1-3, or 2-3 for 32-wide
+    // stages) unchanged, so block i is a constant offset from block 0 and every fragment
+    // address is one per-lane base plus an immediate
+    static_assert(WTM % 16 == 0 && WTN % 16 == 0 && BLK % 16 == 0, "swizzle key per lane");
+    const int arow0 = wm * WTM + (lane & (BLK - 1)), brow0 = wn * WTN + (lane & (BLK - 1));
     // lane l's output columns of float4 group g of a block (its row is l % BLK): the MFMA
     // layouts with the weight fragment as the first operand
     auto ocol = [&](int g) { return MB16 ? 4 * (lane >> 4) : 8 * g + 4 * (lane >> 5); };
@@ -326,12 +338,20 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         const bf16* bs = Bs[stage];
         const int c = MB16 ? s * 4 + (lane >> 4) : s * 2 + (lane >> 5);
 #pragma unroll
-        for (int i = 0; i < TM; ++i) fa[set][i] = *(const bf16x8*)&as[arow[i] * BK + swz_k<BK>(arow[i], c) * 8];
+        for (int i = 0; i < TM; ++i) fa[set][i] = *(const bf16x8*)&as[(arow0 + i * BLK) * BK + swz_k<BK>(arow0, c) * 8];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[set][j] = *(const bf16x8*)&bs[brow[j] * BK + swz_k<BK>(brow[j], c) * 8];
+        for (int j = 0; j < TN; ++j) fb[set][j] = *(const bf16x8*)&bs[(brow0 + j * BLK) * BK + swz_k<BK>(brow0, c) * 8];
     };
     auto mfma = [&](int set) {
-        if constexpr (MB16) {
+        if constexpr (MB16 && !F32) {
+            // bf16 on 16x16 blocks: lane group g = l / 16 takes chunk 4s + g, the 8 values of
+            // k = 32s + 8g .. 32s + 8g + 7 that v_mfma_f32_16x16x32_bf16 expects of it
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+        } else if constexpr (MB16) {
             // float32 operands on 16x16 blocks: lane group g = l / 16 takes chunk 4s + g, so
             // MFMA u sums k = 16s + 4g + u over the four groups
 #pragma unroll
@@ -374,37 +394,148 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         if (NMF > TM + TN) __builtin_amdgcn_sched_group_barrier(0x008, NMF - (TM + TN), 0);
     };
 
+    if constexpr (!FINE) {
+        // First schedule: the DMA of tile kt+NS-1 goes out at the top of tile kt, all at once.
 #pragma unroll
-    for (int st = 0; st < NS - 1; ++st)
-        if (st < nk) dma(st, st);
-    // tile 0 complete: NS-2 newer tiles may stay in flight, unless K has fewer tiles than that
-    if (nk >= NS - 1) wait_vm<(NS - 2) * OPS>();
-    else wait_vm<0>();
+        for (int st = 0; st < NS - 1; ++st)
+            if (st < nk) dma(st, st);
+        // tile 0 complete: NS-2 newer tiles may stay in flight, unless K has fewer tiles than that
+        if (nk >= NS - 1) wait_vm<(NS - 2) * OPS>();
+        else wait_vm<0>();
+        __syncthreads();
+        frag(0, 0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+            const int cur = kt % NS;
+            if (kt + NS - 1 < nk) dma(kt + NS - 1, (kt + NS - 1) % NS);
+            // substeps 0 .. SUB-2, each reading the fragments of the next
+#pragma unroll
+            for (int s = 0; s + 1 < SUB; ++s) {
+                frag(cur, s + 1, (s + 1) & 1);
+                mfma(s & 1);
+                interleave();
+            }
+            // Tile kt+1 must be complete in LDS (this wave's DMA, then all waves'), and this
+            // wave's reads of stage cur must be done before anyone refills it. The barrier
+            // sits before the last substep so its MFMAs cover the first reads of tile kt+1.
+            if (kt + 1 < nk) {
+                const int newer = min(NS - 2, nk - 2 - kt);  // tiles newer than kt+1 in flight
+                if (newer >= NS - 2) wait_vm<(NS - 2) * OPS>();
+                else wait_vm<0>();  // tail: wait for everything
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments of the last substep are in
+            __syncthreads();
+            if (kt + 1 < nk) frag((kt + 1) % NS, 0, SUB & 1);
+            mfma((SUB - 1) & 1);
+            interleave();
+        }
+    } else {
+    // Second schedule: every load, fragment read and MFMA in a fixed order. A stage is
+    // refilled as soon as every wave has read its last fragments (at the barrier one substep
+    // before the end of its tile), with the DMA blocks spread one every few MFMAs, so a wave
+    // never waits behind a run of its own loads while the MFMA pipe idles.
+    // One DMA block d of tile kt into stage `stage`, from resources rA / rB (the panels, or
+    // empty resources: a load past the last tile then reads nothing and writes zeros into a
+    // stage that is never read again, which keeps every wave's load count the same)
+    auto dma_one = [&](int kt, int stage, auto D, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB)
+                       __attribute__((always_inline)) {
+        constexpr int d = decltype(D)::value;
+        const uint32_t k2 = (uint32_t)(kt * BK) * 2;
+        if constexpr (EVEN) {
+            if constexpr (d < AG)
+                dma16(rA, aoff[d], k2, __builtin_amdgcn_readfirstlane(a_lds + (uint32_t)((stage * BM + (wave * AG + d) * RPB) * BK * 2)));
+            else
+                dma16(rB, boff[d - AG], k2, __builtin_amdgcn_readfirstlane(b_lds + (uint32_t)((stage * BN + (wave * BG + d - AG) * RPB) * BK * 2)));
+        } else {
+            const int b = wu + NW * d;
+            if (b < TBA)
+                dma16(rA, aoff[d], k2, a_lds + (uint32_t)((stage * BM + b * RPB) * BK * 2));
+            else if (b < TBT)
+                dma16(rB, aoff[d], k2, b_lds + (uint32_t)((stage * BN + (b - TBA) * RPB) * BK * 2));
+        }
+    };
+    const __amdgpu_buffer_rsrc_t ra_none = buffer_rsrc(A, 0), rb_none = buffer_rsrc(B, 0);
+    // every DMA block of tile kt into stage `stage` (none past the last tile)
+    auto dma_all = [&](int kt, int stage) __attribute__((always_inline)) {
+        const bool live = kt < nk;
+        static_for<OPS>([&](auto D) __attribute__((always_inline)) {
+            dma_one(kt, stage, D, live ? ra : ra_none, live ? rbr : rb_none);
+        });
+    };
+    // fragment f (activation blocks, then weight blocks) of substep s of stage `stage`
+    auto frag_one = [&](int stage, int s, auto SET, auto F) __attribute__((always_inline)) {
+        constexpr int set = decltype(SET)::value, f = decltype(F)::value;
+        const int c = MB16 ? s * 4 + (lane >> 4) : s * 2 + (lane >> 5);
+        if constexpr (f < TM) fa[set][f] = *(const bf16x8*)&As[stage][(arow0 + f * BLK) * BK + swz_k<BK>(arow0, c) * 8];
+        else fb[set][f - TM] = *(const bf16x8*)&Bs[stage][(brow0 + (f - TM) * BLK) * BK + swz_k<BK>(brow0, c) * 8];
+    };
+    // MFMA q of a substep, in the order of mfma()
+    auto mfma_one = [&](auto SET, auto Q) __attribute__((always_inline)) {
+        constexpr int set = decltype(SET)::value, q = decltype(Q)::value;
+        if constexpr (F32) {
+            constexpr int u = q / (TM * TN), r = q % (TM * TN), i = r / TN, j = r % TN;
+            if constexpr (MB16)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
+                                                                 __builtin_bit_cast(f32x4, fa[set][i])[u], acc[i][j], 0, 0, 0);
+            else
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
+                                                                 __builtin_bit_cast(f32x4, fa[set][i])[u], acc[i][j], 0, 0, 0);
+        } else {
+            constexpr int i = q / TN, j = q % TN;
+            if constexpr (MB16)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+            else
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+        }
+    };
+    // one substep: the NMF MFMAs of fragment set SET, with the reads of the other set
+    // (substep rsub of stage rs) and, with DMA, the OPS refill blocks of tile dkt into stage
+    // dst spread evenly between them; the order is pinned, so no wave issues a run of loads
+    // while its MFMAs wait
+    auto substep = [&](auto DMA, auto SET, int rs, int rsub, int dkt, int dst) __attribute__((always_inline)) {
+        constexpr int set = decltype(SET)::value;
+        const bool live = dkt < nk;
+        const __amdgpu_buffer_rsrc_t rA = live ? ra : ra_none, rB = live ? rbr : rb_none;
+        static_for<NMF>([&](auto Q) __attribute__((always_inline)) {
+            constexpr int q = decltype(Q)::value;
+            if constexpr (decltype(DMA)::value)
+                static_for<OPS>([&](auto D) __attribute__((always_inline)) {
+                    if constexpr (decltype(D)::value * NMF / OPS == q) dma_one(dkt, dst, D, rA, rB);
+                });
+            // the next set's reads go out first, one per MFMA, so they land early
+            static_for<TM + TN>([&](auto F) __attribute__((always_inline)) {
+                if constexpr ((decltype(F)::value < NMF ? decltype(F)::value : NMF - 1) == q)
+                    frag_one(rs, rsub, std::integral_constant<int, set ^ 1>{}, F);
+            });
+            mfma_one(SET, Q);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    // Every wave issues OPS loads per tile for NS tiles ahead, tiles past the last included
+    // (as loads of nothing), so every wait below is the same count.
+    static_for<NS - 1>([&](auto ST) __attribute__((always_inline)) { dma_all(ST, ST); });
+    wait_vm<(NS - 2) * OPS>();  // tile 0 complete
+    dma_all(NS - 1, NS - 1);    // the last stage of the ring is free from the start
     __syncthreads();
     frag(0, 0, 0);
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt % NS;
-        if (kt + NS - 1 < nk) dma(kt + NS - 1, (kt + NS - 1) % NS);
         // substeps 0 .. SUB-2, each reading the fragments of the next
-#pragma unroll
-        for (int s = 0; s + 1 < SUB; ++s) {
-            frag(cur, s + 1, (s + 1) & 1);
-            mfma(s & 1);
-            interleave();
-        }
-        // Tile kt+1 must be complete in LDS (this wave's DMA, then all waves'), and this
-        // wave's reads of stage cur must be done before anyone refills it. The barrier
-        // sits before the last substep so its MFMAs cover the first reads of tile kt+1.
-        if (kt + 1 < nk) {
-            const int newer = min(NS - 2, nk - 2 - kt);  // tiles newer than kt+1 in flight
-            if (newer >= NS - 2) wait_vm<(NS - 2) * OPS>();
-            else wait_vm<0>();  // tail: wait for everything
-        }
+        static_for<SUB - 1>([&](auto S) __attribute__((always_inline)) {
+            constexpr int s = decltype(S)::value;
+            substep(std::false_type{}, std::integral_constant<int, s & 1>{}, cur, s + 1, 0, 0);
+        });
+        // Tile kt+1 must be complete in LDS (this wave's DMA, then all waves'), and every
+        // wave's reads of stage cur must be done before it is refilled. The barrier sits
+        // before the last substep, so its MFMAs cover the first reads of tile kt+1, and the
+        // refill of stage cur with tile kt+NS goes out between them: each tile's DMA has a
+        // whole tile of MFMAs, from one barrier to the next, to land. (After the last tile
+        // the reads of stage (kt+1) % NS fetch values that are never used.)
+        wait_vm<(NS - 2) * OPS>();
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments of the last substep are in
         __syncthreads();
-        if (kt + 1 < nk) frag((kt + 1) % NS, 0, SUB & 1);
-        mfma((SUB - 1) & 1);
-        interleave();
+        substep(std::true_type{}, std::integral_constant<int, (SUB - 1) & 1>{}, (kt + 1) % NS, 0, kt + NS, cur);
+    }
+    wait_vm<0>();  // the loads of nothing past the last tile write the ring too
     }
 
     if constexpr (STAGE) {
@@ -539,16 +670,16 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
 }
 
-template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF>
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF, bool MB16 = false, bool FINE = false>
 hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                    int64_t ldc, hipStream_t s, int splits = 1, float* part = nullptr) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     if (splits <= 1) {
-        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
+        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, false, false, MB16, FINE>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
                    (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, nullptr);
         return hipGetLastError();
     }
-    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, true>), dim3(tm * tn, splits), dim3(64 * WM * WN), 0,
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, true, false, MB16, FINE>), dim3(tm * tn, splits), dim3(64 * WM * WN), 0,
                s, (int)M, (int)N, (int)(K / splits), (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, part);
     if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     KernelTimer kt("gemm.splitk_reduce", s);
@@ -586,7 +717,12 @@ hipError_t run_dma_f32(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 // work per LDS byte; 128x128 gives more workgroups when the grid is small). 256x320 (4x2
 // waves of 64x160) takes an output whose 256-wide tiles leave the last round part-empty
 // but whose N is a multiple of 320: out_proj of the 2.8B half shard (16384 x 2560) runs
-// 512 of them in 2 rounds instead of 640 256x256 tiles in 3.
+// 512 of them in 2 rounds instead of 640 256x256 tiles in 3. The 256x256 (2x4 waves of
+// 128x64) and 128x128 (2x2 waves of 64x64, two workgroups per CU) tiles run on 16x16
+// blocks with the second schedule (6-7% faster than 32x32 blocks with the first); 256x320
+// keeps 32x32 blocks and the first schedule (on 16x16 blocks its 64x160 wave tiles with
+// two fragment sets do not fit in the registers, and the second schedule alone gained
+// nothing there).
 enum DmaTiles { kTiles128 = 0, kTiles256 = 1, kTiles256x320 = 2 };
 DmaTiles dma_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, double eff) {
@@ -655,11 +791,11 @@ hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t 
     if (K % 64 == 0) {
         const DmaTiles t = dma_tiles(M, N);
         if (t == kTiles256x320) return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
-        if (t == kTiles256) return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (t == kTiles256) return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
     }
     if (K % 64 == 0) {
         const int sp = fit_slices(splitk_slices(((M + 127) / 128) * ((N + 127) / 128), K), M, N, scratch_bytes);
-        return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
+        return run_dma<ROLE, 128, 128, 64, 2, 2, 2, CF, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s, sp, scratch);
     }
     // K a multiple of 32 only (dt_proj: K = dt_rank): a 3-slot ring (48 KB) lets three
     // workgroups share a CU, which shortens the many short-lived tiles' latency rounds
