@@ -217,9 +217,11 @@ template <int BK> __device__ __forceinline__ int swz_k(int row, int chunk) {
 // F32: the operands are float32 rows passed as bf16 rows of twice the length (K, lda and
 // ldb in bf16 units); the DMA and the LDS layout only move bytes, and each 16-byte fragment
 // (4 floats along k) feeds four v_mfma_f32_32x32x2_f32 instead of one bf16 MFMA.
-// MB16: 16x16 MFMA blocks. FINE: the second, fully ordered schedule of the k loop.
+// MB16: 16x16 MFMA blocks. FINE: the second, fully ordered schedule of the k loop. SB (with
+// FINE): one set of weight fragments, each reloaded right after its last MFMA of a substep
+// (the MFMAs run weight block by weight block), which frees registers for wider tiles.
 template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool C_F32, bool SPLIT = false, bool F32 = false,
-          bool MB16 = false, bool FINE = false>
+          bool MB16 = false, bool FINE = false, bool SB = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int K, const bf16* __restrict__ A,
                                                               int64_t lda, const bf16* __restrict__ B, int64_t ldb,
                                                               void* __restrict__ Cp, int64_t ldc, int tiles_m,
@@ -466,7 +468,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         constexpr int set = decltype(SET)::value, f = decltype(F)::value;
         const int c = MB16 ? s * 4 + (lane >> 4) : s * 2 + (lane >> 5);
         if constexpr (f < TM) fa[set][f] = *(const bf16x8*)&As[stage][(arow0 + f * BLK) * BK + swz_k<BK>(arow0, c) * 8];
-        else fb[set][f - TM] = *(const bf16x8*)&Bs[stage][(brow0 + (f - TM) * BLK) * BK + swz_k<BK>(brow0, c) * 8];
+        else fb[SB ? 0 : set][f - TM] = *(const bf16x8*)&Bs[stage][(brow0 + (f - TM) * BLK) * BK + swz_k<BK>(brow0, c) * 8];
     };
     // MFMA q of a substep, in the order of mfma()
     auto mfma_one = [&](auto SET, auto Q) __attribute__((always_inline)) {
@@ -480,11 +482,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
                                                                  __builtin_bit_cast(f32x4, fa[set][i])[u], acc[i][j], 0, 0, 0);
         } else {
-            constexpr int i = q / TN, j = q % TN;
+            constexpr int i = SB ? q % TM : q / TN, j = SB ? q / TM : q % TN, sb = SB ? 0 : set;
             if constexpr (MB16)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
             else
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[set][j], fa[set][i], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
         }
     };
     // one substep: the NMF MFMAs of fragment set SET, with the reads of the other set
@@ -501,12 +503,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
                 static_for<OPS>([&](auto D) __attribute__((always_inline)) {
                     if constexpr (decltype(D)::value * NMF / OPS == q) dma_one(dkt, dst, D, rA, rB);
                 });
-            // the next set's reads go out first, one per MFMA, so they land early
-            static_for<TM + TN>([&](auto F) __attribute__((always_inline)) {
+            // the next set's reads go out first, one per MFMA, so they land early (with SB the
+            // weight fragments only after their last MFMA here)
+            static_for<SB ? TM : TM + TN>([&](auto F) __attribute__((always_inline)) {
                 if constexpr ((decltype(F)::value < NMF ? decltype(F)::value : NMF - 1) == q)
                     frag_one(rs, rsub, std::integral_constant<int, set ^ 1>{}, F);
             });
             mfma_one(SET, Q);
+            if constexpr (SB && q % TM == TM - 1)
+                frag_one(rs, rsub, std::integral_constant<int, set ^ 1>{}, std::integral_constant<int, TM + q / TM>{});
             __builtin_amdgcn_sched_barrier(0);
         });
     };
@@ -670,16 +675,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
 }
 
-template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF, bool MB16 = false, bool FINE = false>
+template <int ROLE, int BM, int BN, int BK, int NS, int WM, int WN, bool CF, bool MB16 = false, bool FINE = false,
+          bool SB = false>
 hipError_t run_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                    int64_t ldc, hipStream_t s, int splits = 1, float* part = nullptr) {
     const int tm = (int)((M + BM - 1) / BM), tn = (int)((N + BN - 1) / BN);
     if (splits <= 1) {
-        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, false, false, MB16, FINE>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
+        SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, false, false, MB16, FINE, SB>), dim3(tm * tn), dim3(64 * WM * WN), 0, s,
                    (int)M, (int)N, (int)K, (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, nullptr);
         return hipGetLastError();
     }
-    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, true, false, MB16, FINE>), dim3(tm * tn, splits), dim3(64 * WM * WN), 0,
+    SSM_LAUNCH((gemm_bf16_dma<ROLE, BM, BN, BK, NS, WM, WN, CF, true, false, MB16, FINE, SB>), dim3(tm * tn, splits), dim3(64 * WM * WN), 0,
                s, (int)M, (int)N, (int)(K / splits), (const bf16*)A, lda, (const bf16*)B, ldb, C, ldc, tm, tn, part);
     if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     KernelTimer kt("gemm.splitk_reduce", s);
@@ -717,12 +723,10 @@ hipError_t run_dma_f32(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 // work per LDS byte; 128x128 gives more workgroups when the grid is small). 256x320 (4x2
 // waves of 64x160) takes an output whose 256-wide tiles leave the last round part-empty
 // but whose N is a multiple of 320: out_proj of the 2.8B half shard (16384 x 2560) runs
-// 512 of them in 2 rounds instead of 640 256x256 tiles in 3. The 256x256 (2x4 waves of
-// 128x64) and 128x128 (2x2 waves of 64x64, two workgroups per CU) tiles run on 16x16
-// blocks with the second schedule (6-7% faster than 32x32 blocks with the first); 256x320
-// keeps 32x32 blocks and the first schedule (on 16x16 blocks its 64x160 wave tiles with
-// two fragment sets do not fit in the registers, and the second schedule alone gained
-// nothing there).
+// 512 of them in 2 rounds instead of 640 256x256 tiles in 3. All three run on 16x16 blocks
+// with the second schedule (5-7% faster than 32x32 blocks with the first): 256x256 as 2x4
+// waves of 128x64, 128x128 as 2x2 waves of 64x64 (two workgroups per CU), 256x320 as 4x2
+// waves of 64x160 with one set of weight fragments (two sets do not fit in the registers).
 enum DmaTiles { kTiles128 = 0, kTiles256 = 1, kTiles256x320 = 2 };
 DmaTiles dma_tiles(int64_t M, int64_t N) {
     auto cost = [&](int bm, int bn, double eff) {
@@ -790,7 +794,8 @@ hipError_t dispatch_dma(int64_t M, int64_t N, int64_t K, const void* A, int64_t 
                         void* C, int64_t ldc, hipStream_t s, float* scratch, size_t scratch_bytes) {
     if (K % 64 == 0) {
         const DmaTiles t = dma_tiles(M, N);
-        if (t == kTiles256x320) return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (t == kTiles256x320)
+            return run_dma<ROLE, 256, 320, 64, 2, 4, 2, CF, true, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
         if (t == kTiles256) return run_dma<ROLE, 256, 256, 64, 2, 2, 4, CF, true, true>(M, N, K, A, lda, B, ldb, C, ldc, s);
     }
     if (K % 64 == 0) {

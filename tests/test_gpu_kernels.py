@@ -48,6 +48,9 @@ GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 9
                (256, 2560, 2560), (130, 8192, 1280), (500, 1100, 640), (17, 4104, 64), (33, 4096, 1344),
                (100, 4104, 2560), (129, 2560, 1280), (200, 4104, 3584), (511, 2568, 640), (40, 2560, 640),
                (60, 3584, 3584), (40, 4104, 640),
+               # bf16 256x320 tiles (N a multiple of 320 whose 256-wide tiles would take an extra
+               # round; ragged last row tile)
+               (8000, 2560, 320),
                # float32 at prefill sizes, by the tile model: 128x128 (2000 x 3588), 128x224 (1500 x 4100,
                # 1200 x 3500), 256x256 (2000 x 7900), 256x224 (2048 x 7168); ragged M and N, K of 96 to 3584
                (2000, 3588, 224), (1500, 4100, 96), (1200, 3500, 352), (2000, 7900, 256), (2048, 7168, 3584)]
