@@ -51,6 +51,8 @@ GEMM_SHAPES = [(1, 64, 16), (7, 130, 48), (300, 200, 32), (33, 200, 160), (64, 9
                # bf16 256x320 tiles (N a multiple of 320 whose 256-wide tiles would take an extra
                # round; ragged last row tile)
                (8000, 2560, 320),
+               # bf16 256x256 tiles over two rounds (ragged last row and column tiles, three k-tiles)
+               (8000, 4000, 192),
                # float32 at prefill sizes, by the tile model: 128x128 (2000 x 3588), 128x224 (1500 x 4100,
                # 1200 x 3500), 256x256 (2000 x 7900), 256x224 (2048 x 7168); ragged M and N, K of 96 to 3584
                (2000, 3588, 224), (1500, 4100, 96), (1200, 3500, 352), (2000, 7900, 256), (2048, 7168, 3584)]
