@@ -71,13 +71,18 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
-// softplus(v) = log(1 + e^v), v itself above 20. log1p is formed as
-// log(1+w) * w / ((1+w) - 1), which keeps full relative accuracy for small w.
+// softplus(v) = log(1 + e^v) = max(v, 0) + log1p(w) with w = e^-|v| in (0, 1]. With
+// p = 1 + w rounded, p - 1 is exact and d = w - (p - 1) is the rounding error of p, so
+// log1p(w) = log(p) + d / p to first order; p lies in (1, 2] and |d| is at most half an ulp
+// of 1, so d / p may take 2 - p for 1 / p (an error of d (p - 1)^2 / p: about w^2 d for
+// small w, at most d / 2 at w = 1, where log1p is 0.69). Two transcendentals (exp, log) and
+// full relative accuracy for small w, as the usual log(p) * w / (p - 1) form of log1p gives
+// with a third (the reciprocal).
 __device__ __forceinline__ float softplus_f(float v) {
-    const float w = fast_exp2(v * kLog2e);
+    const float w = fast_exp2(-fabsf(v) * kLog2e);
     const float p = 1.0f + w;
-    const float l = (p == 1.0f) ? w : fast_log2(p) * kLn2 * w * fast_rcp(p - 1.0f);
-    return v > 20.0f ? v : l;
+    const float d = w - (p - 1.0f);
+    return fmaxf(v, 0.0f) + __builtin_fmaf(d, 2.0f - p, fast_log2(p) * kLn2);
 }
 // SiLU(v) = v / (1 + e^-v)
 // min(rem, cap) for a row count, in integer arithmetic (the 64-bit min of the device headers
