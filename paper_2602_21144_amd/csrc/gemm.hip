@@ -470,24 +470,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_dma(int M, int N, int 
         if constexpr (f < TM) fa[set][f] = *(const bf16x8*)&As[stage][(arow0 + f * BLK) * BK + swz_k<BK>(arow0, c) * 8];
         else fb[SB ? 0 : set][f - TM] = *(const bf16x8*)&Bs[stage][(brow0 + (f - TM) * BLK) * BK + swz_k<BK>(brow0, c) * 8];
     };
-    // MFMA q of a substep, in the order of mfma()
+    // MFMA q of a substep (block row by block row; with SB block column by block column)
+    static_assert(!F32, "the second schedule is for bf16 operands (the float32 tiles keep the first)");
     auto mfma_one = [&](auto SET, auto Q) __attribute__((always_inline)) {
         constexpr int set = decltype(SET)::value, q = decltype(Q)::value;
-        if constexpr (F32) {
-            constexpr int u = q / (TM * TN), r = q % (TM * TN), i = r / TN, j = r % TN;
-            if constexpr (MB16)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
-                                                                 __builtin_bit_cast(f32x4, fa[set][i])[u], acc[i][j], 0, 0, 0);
-            else
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(f32x4, fb[set][j])[u],
-                                                                 __builtin_bit_cast(f32x4, fa[set][i])[u], acc[i][j], 0, 0, 0);
-        } else {
-            constexpr int i = SB ? q % TM : q / TN, j = SB ? q / TM : q % TN, sb = SB ? 0 : set;
-            if constexpr (MB16)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
-            else
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
-        }
+        constexpr int i = SB ? q % TM : q / TN, j = SB ? q / TM : q % TN, sb = SB ? 0 : set;
+        if constexpr (MB16)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
+        else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[sb][j], fa[set][i], acc[i][j], 0, 0, 0);
     };
     // one substep: the NMF MFMAs of fragment set SET, with the reads of the other set
     // (substep rsub of stage rs) and, with DMA, the OPS refill blocks of tile dkt into stage
