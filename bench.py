@@ -164,6 +164,14 @@ def kernel_work(sh, kind, n, nseq):
             "decode.x_proj": proj(W * E * s + M * E * s + M * W * 4, 2.0 * M * W * E),
             "decode.dt_proj_state": state,
             "decode.out_proj": proj(dm * E * s + M * E * s + M * dm * s, 2.0 * M * dm * E)}
+    if not bf and K >= 2 and M <= 64 and dm % 32 == 0:
+        # float32: in_proj with the conv window fused, up to 64 sequences
+        return {
+            "decode.in_proj_conv": proj(2 * E * dm * s + M * dm * s + 2 * M * E * s + 2 * M * E * (K - 1) * s
+                                        + E * (K + 1) * s, 2.0 * M * 2 * E * dm),
+            "decode.x_proj": proj(W * E * s + M * E * s + M * W * 4, 2.0 * M * W * E),
+            "decode.dt_proj_state": state,
+            "decode.out_proj": proj(dm * E * s + M * E * s + M * dm * s, 2.0 * M * dm * E)}
     return {"decode.in_proj": proj(2 * E * dm * s + M * dm * s + M * 2 * E * s, 2.0 * M * 2 * E * dm),
             "decode.conv": ("hbm", 2 * M * E * (K - 1) * s + 2 * M * E * s + E * (K + 1) * s),
             "decode.x_proj": proj(W * E * s + M * E * s + M * W * 4, 2.0 * M * W * E),

@@ -302,6 +302,20 @@ int decode1(const ssm_shard_desc_t* d, const ssm_shard_weights_t* w, const void*
         SSM_SKINNY("decode.x_proj", s, q, kSkinnyStoreF32);
         return SSM_OK;
     }
+    if (adt == SSM_F32 && d->d_conv >= 2) {
+        // float32: in_proj with the conv window in the streamed kernel's epilogue (up to 64
+        // sequences; otherwise the product and the conv kernel below)
+        const F32ConvEpi cv{slot, S, (float*)conv_pool, (const float*)w->conv_w, (const float*)w->conv_b,
+                            (float*)L.u, (int)E, d->d_conv, L.status};
+        const float* xf = (const float*)x;
+        const float* wf = (const float*)w->in_proj_w;
+        if (gemv_f32_conv_fits(B, 2 * E, dm, xf, dm, wf, dm, cv)) {
+            SSM_TIMED("decode.in_proj_conv", s, launch_gemv_f32_conv(B, 2 * E, dm, xf, dm, wf, dm, (float*)L.xz, 2 * E, cv, s));
+            SSM_TRY(gemm(B, W, E, L.u, E, adt, w->x_proj_w, E, adt, xdbl, W, SSM_F32, s, "decode.x_proj", kGemmXProj,
+                         L.splitk));
+            return SSM_OK;
+        }
+    }
     ConvArgs ca = conv_args(d, w, L.xz, B, nullptr, slot, nullptr, B, conv_pool, S, L.u, L.status);
     SSM_TRY(gemm(B, 2 * E, dm, x, dm, adt, w->in_proj_w, dm, adt, L.xz, 2 * E, adt, s, "decode.in_proj",
                  kGemmInProj, L.splitk));

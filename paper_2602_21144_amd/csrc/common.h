@@ -206,6 +206,20 @@ hipError_t launch_gemv_norm(const SkinnyArgs& p, hipStream_t s);
 // hipErrorNotSupported when the shape does not suit it (M > 64, K % 32, unaligned rows).
 hipError_t launch_gemv_f32_stream(int role, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                                   const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t s);
+// The decode in_proj of a float32 layer with the conv window in its epilogue: columns below
+// conv_n of C = A B^T are channel n of the conv path, which takes its K - 1 cached inputs
+// from conv_pool[slot[m]][n] (float32 [S][conv_n][K - 1]), writes u[m][n] = SiLU(window) and
+// shifts the window; the other columns are stored to C. 2 <= K <= 4. gemv_f32_conv_fits says
+// whether a shape suits it (else the caller runs the product and the conv kernel apart;
+// launching it anyway returns hipErrorNotSupported).
+struct F32ConvEpi {
+    const int32_t* slot; int S; float* conv_pool; const float* w; const float* b; float* u; int conv_n; int K;
+    int32_t* status;
+};
+bool gemv_f32_conv_fits(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B, int64_t ldb,
+                        const F32ConvEpi& cv);
+hipError_t launch_gemv_f32_conv(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                                int64_t ldb, float* C, int64_t ldc, const F32ConvEpi& cv, hipStream_t s);
 
 struct ConvArgs {
     const void* xz; int64_t ld_xz;     // SSM half in columns 0..E-1

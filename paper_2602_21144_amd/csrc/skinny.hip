@@ -838,15 +838,21 @@ hipError_t launch_skinny32(const SkinnyArgs& p, hipStream_t s) {
 // waves' partial tiles are summed through the same LDS at the end.
 constexpr int kF32Stage = 32;  // k per stage: one 128-byte line of a float32 row
 
-template <int ROLE, int NW, int NST, int XB, int CT = 1>
+// CONV: the conv window in the epilogue (launch_gemv_f32_conv). A thread's epilogue items are
+// e = tid + i NW 64; their slot indices go out before the weight stream and the
+// slot-addressed window inputs, taps and bias right after it, so they land with the stream.
+template <int ROLE, int NW, int NST, int XB, int CT = 1, bool CONV = false>
 __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, int K, const float* __restrict__ A,
                                                                   int64_t lda, const float* __restrict__ B,
-                                                                  int64_t ldb, float* __restrict__ C, int64_t ldc) {
+                                                                  int64_t ldb, float* __restrict__ C, int64_t ldc,
+                                                                  F32ConvEpi cv = {}) {
     constexpr int WR = 16 * CT;                // weight rows of a workgroup (CT 16-column tiles)
     constexpr int ROWS = WR + 8 * XB;          // LDS rows of one stage: weights, then activations
     constexpr int MT = (8 * XB + 15) / 16;     // 16-row output tiles
     constexpr int WBUF = ROWS * 128;           // bytes of a wave's buffer
     static_assert(WBUF >= CT * MT * 16 * 16 * 4, "the partial tiles fit the wave's buffer");
+    constexpr int NE = CT * MT * 256;          // epilogue items: (tile, row, column)
+    constexpr int EL = (NE + NW * 64 - 1) / (NW * 64);
     __shared__ __attribute__((aligned(16))) char tr[NW][WBUF];
     const int n0 = blockIdx.x * WR;
     // row tiles of 8 XB activation rows along blockIdx.y (one tile when the grid has one row)
@@ -855,6 +861,21 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
     C += (int64_t)m0 * ldc;
     M = min(M - m0, 8 * XB);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // epilogue item i of this thread: its row, column, and (CONV) slot
+    auto item = [&](int i, int& m, int& n) {
+        const int e = (int)threadIdx.x + i * NW * 64;
+        m = (e / 16) % (MT * 16);
+        n = n0 + 16 * (e / (MT * 256)) + (e & 15);
+        return e < NE && m < M && n < N;
+    };
+    int eslot[CONV ? EL : 1];
+    if constexpr (CONV) {
+#pragma unroll
+        for (int i = 0; i < EL; ++i) {
+            int m, n;
+            eslot[i] = item(i, m, n) ? cv.slot[m0 + m] : 0;
+        }
+    }
     const int nall = K / kF32Stage;
     const int sb = wave * nall / NW, nst = (wave + 1) * nall / NW - sb;
     const int lr = lane >> 3, lp = lane & 7;
@@ -877,6 +898,25 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
     };
 #pragma unroll
     for (int j = 0; j < NST; ++j) issue(j, j);
+    // (CONV) each item's window: K - 1 cached inputs, K taps, bias (channel 0 for columns
+    // outside the conv path and slot 0 for a bad slot: read, never used)
+    float ehv[CONV ? EL : 1][kMaxConv - 1], ewv[CONV ? EL : 1][kMaxConv], ebv[CONV ? EL : 1];
+    if constexpr (CONV) {
+        const int Kc = cv.K;
+#pragma unroll
+        for (int i = 0; i < EL; ++i) {
+            int m, n;
+            item(i, m, n);
+            const int c = n < cv.conv_n ? n : 0;
+            const int sc = eslot[i] >= 0 && eslot[i] < cv.S ? eslot[i] : 0;
+            const float* hist = cv.conv_pool + ((int64_t)sc * cv.conv_n + c) * (Kc - 1);
+#pragma unroll
+            for (int j = 0; j < kMaxConv - 1; ++j) ehv[i][j] = hist[j < Kc - 1 ? j : Kc - 2];
+#pragma unroll
+            for (int j = 0; j < kMaxConv; ++j) ewv[i][j] = cv.w[(int64_t)c * Kc + (j < Kc ? j : Kc - 1)];
+            ebv[i] = cv.b[c];
+        }
+    }
 
     char* t = tr[wave];
     const int wr = lane & 15, cg = lane >> 4;
@@ -931,19 +971,50 @@ __global__ __launch_bounds__(NW * 64) void gemv_f32_stream_kernel(int M, int N, 
 #pragma unroll
             for (int r = 0; r < 4; ++r) red[((ct * MT + i) * 16 + 4 * cg + r) * 16 + wr] = acc[ct][i][r];
     __syncthreads();
-    for (int e = threadIdx.x; e < CT * MT * 256; e += NW * 64) {
-        const int ct = e / (MT * 256), m = (e / 16) % (MT * 16), n = n0 + 16 * ct + (e & 15);
-        if (m >= M || n >= N) continue;
+#pragma unroll
+    for (int i = 0; i < EL; ++i) {
+        int m, n;
+        if (!item(i, m, n)) continue;
+        const int e = (int)threadIdx.x + i * NW * 64;
         float v = 0.0f;
 #pragma unroll
         for (int w = 0; w < NW; ++w) v += ((const float*)tr[w])[e];
+        if constexpr (CONV) {
+            if (n < cv.conv_n) {
+                // the conv window step of the conv kernel: bias, the cached inputs, then this
+                // token's input; SiLU; the window shifts by one
+                const int Kc = cv.K, slot = eslot[i];
+                float* u = cv.u + (int64_t)(m0 + m) * cv.conv_n + n;
+                if (slot < 0 || slot >= cv.S) {
+                    atomicOr(cv.status, SSM_STATUS_BAD_SLOT);
+                    *u = 0.0f;
+                    continue;
+                }
+                float acc = ebv[i];
+#pragma unroll
+                for (int j = 0; j < kMaxConv - 1; ++j)
+                    if (j < Kc - 1) acc += ewv[i][j] * ehv[i][j];
+                float wl = 0.0f;
+#pragma unroll
+                for (int j = 0; j < kMaxConv; ++j)
+                    if (j == Kc - 1) wl = ewv[i][j];
+                acc += wl * v;
+                *u = silu_f(acc);
+                float* hist = cv.conv_pool + ((int64_t)slot * cv.conv_n + n) * (Kc - 1);
+#pragma unroll
+                for (int j = 0; j < kMaxConv - 2; ++j)
+                    if (j < Kc - 2) hist[j] = ehv[i][j + 1];
+                hist[Kc - 2] = v;
+                continue;
+            }
+        }
         C[(int64_t)m * ldc + n] = v;
     }
 }
 
-template <int ROLE, int NW>
+template <int ROLE, int NW, bool CONV = false>
 hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
-                                float* C, int64_t ldc, hipStream_t s) {
+                                float* C, int64_t ldc, hipStream_t s, const F32ConvEpi& cv = {}) {
     const dim3 grid((unsigned)((N + 15) / 16)), block(NW * 64);
     // 33..64 rows over wide outputs: two 16-column tiles per workgroup, so each staged block
     // of activation rows serves 32 columns (half the activation re-reads; the hybrid shard's
@@ -952,13 +1023,13 @@ hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda
     if constexpr (NW == 8) {
         if (M > 32 && M <= 64 && (N + 31) / 32 >= 128) {
             const dim3 g2((unsigned)((N + 31) / 32));
-            if (M <= 48) SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 6, 2>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
-            else SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 8, 2>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
+            if (M <= 48) SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 6, 2, CONV>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv);
+            else SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, 2, 8, 2, CONV>), g2, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv);
             return hipGetLastError();
         }
     }
 #define SSM_F32S(XB, NST) \
-    SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, NST, XB>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc)
+    SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, NW, NST, XB, 1, CONV>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv)
     if (M <= 8) SSM_F32S(1, 3);
     else if (M <= 16) SSM_F32S(2, 3);
     else if (M <= 32) SSM_F32S(4, 3);
@@ -971,21 +1042,21 @@ hipError_t launch_f32_stream_nw(int M, int N, int K, const float* A, int64_t lda
     return hipGetLastError();
 }
 
-template <int ROLE>
+template <int ROLE, bool CONV = false>
 hipError_t launch_f32_stream_role(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
-                                  float* C, int64_t ldc, hipStream_t s) {
+                                  float* C, int64_t ldc, hipStream_t s, const F32ConvEpi& cv = {}) {
     // few column tiles (x_proj: 16): 16 waves, so that each wave's run of K stays short; more
     // than 16 rows are cut into 16-row tiles along the grid's second dimension, so that more
     // CUs share the stream and each reads 16 activation rows instead of all of them (the
     // hybrid shard's x_proj of 64 rows: 16 workgroups each reading 64 activation rows of
     // 14 KB took 14 us)
     if ((N + 15) / 16 < 128) {
-        if (M <= 16) return launch_f32_stream_nw<ROLE, 16>(M, N, K, A, lda, B, ldb, C, ldc, s);
+        if (M <= 16) return launch_f32_stream_nw<ROLE, 16, CONV>(M, N, K, A, lda, B, ldb, C, ldc, s, cv);
         const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 15) / 16)), block(16 * 64);
-        SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, 16, 3, 2>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc);
+        SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, 16, 3, 2, 1, CONV>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv);
         return hipGetLastError();
     }
-    return launch_f32_stream_nw<ROLE, 8>(M, N, K, A, lda, B, ldb, C, ldc, s);
+    return launch_f32_stream_nw<ROLE, 8, CONV>(M, N, K, A, lda, B, ldb, C, ldc, s, cv);
 }
 
 }  // namespace
@@ -1045,13 +1116,30 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& p, SkinnyEpi epi, hipStream_t s)
 
 namespace ssm {
 
+namespace {
+bool f32_stream_fits(int64_t M, int64_t K, const float* A, int64_t lda, const float* B, int64_t ldb) {
+    auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+    return M <= 64 && K % kF32Stage == 0 && lda % 4 == 0 && ldb % 4 == 0 && al16(A) && al16(B) &&
+           M * lda * 4 < ((int64_t)1 << 31) && 16 * ldb * 4 < ((int64_t)1 << 31);
+}
+}  // namespace
+
+bool gemv_f32_conv_fits(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B, int64_t ldb,
+                        const F32ConvEpi& cv) {
+    return f32_stream_fits(M, K, A, lda, B, ldb) && cv.K >= 2 && cv.K <= kMaxConv && cv.conv_n <= N;
+}
+
+hipError_t launch_gemv_f32_conv(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                                int64_t ldb, float* C, int64_t ldc, const F32ConvEpi& cv, hipStream_t s) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    if (!gemv_f32_conv_fits(M, N, K, A, lda, B, ldb, cv)) return hipErrorNotSupported;
+    return launch_f32_stream_role<kGemmInProj, true>((int)M, (int)N, (int)K, A, lda, B, ldb, C, ldc, s, cv);
+}
+
 hipError_t launch_gemv_f32_stream(int role, int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                                   const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t s) {
-    auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
     if (M <= 0 || N <= 0) return hipSuccess;
-    if (M > 64 || K % kF32Stage != 0 || lda % 4 != 0 || ldb % 4 != 0 || !al16(A) || !al16(B) ||
-        M * lda * 4 >= ((int64_t)1 << 31) || 16 * ldb * 4 >= ((int64_t)1 << 31))
-        return hipErrorNotSupported;
+    if (!f32_stream_fits(M, K, A, lda, B, ldb)) return hipErrorNotSupported;
     const int m = (int)M, n = (int)N, k = (int)K;
     switch (role) {
         case kGemmInProj: return launch_f32_stream_role<kGemmInProj>(m, n, k, A, lda, B, ldb, C, ldc, s);
