@@ -126,20 +126,26 @@ def _decode_batch_case(shape, batch, init, seed, state_tol=None):
 
 # 3 sequences of a small layer (16-row kernels, the state step in dt_proj's epilogue) and
 # 70 of the 2.8B quarter shard (streamed tile kernel with the conv window in its epilogue,
-# the state-step kernel)
-@pytest.mark.parametrize("case", ["few_rows", "tiles"])
+# the state-step kernel); at float32, 3 sequences of the small layer and 40 of the quarter
+# shard (the float32 streamed in_proj with the conv window in its epilogue: its 16-wave and
+# 8-wave forms)
+@pytest.mark.parametrize("case", ["few_rows", "tiles", "f32_few_rows", "f32_rows40"])
 def test_decode_bad_slot_is_flagged(case):
     """A slot outside the pool is flagged; the valid sequences advance exactly as alone."""
     from paper_2602_21144_amd import binding as B
     if case == "few_rows":
         shape, batch, bad = synth.LayerShape(64, 128, 16, 16, 4, 1, "bf16"), 3, 1
-    else:
+    elif case == "tiles":
         shape, batch, bad = synth.LayerShape(2560, 1280, 16, 160, 4, 1, "bf16"), 70, 37
+    elif case == "f32_few_rows":
+        shape, batch, bad = synth.LayerShape(64, 128, 16, 16, 4, 1, "f32"), 3, 1
+    else:
+        shape, batch, bad = synth.LayerShape(2560, 1280, 16, 160, 4, 1, "f32"), 40, 17
     full = synth.make_layer(shape, 5)
     g = GpuLayer(shape, full)
     S = batch + 3
     rng = np.random.default_rng(1)
-    xt = synth.make_tokens(rng, batch, shape.d_model, "bf16")
+    xt = synth.make_tokens(rng, batch, shape.d_model, shape.act)
     conv, ssm = g.new_pools(S, poison=False)
     conv2, ssm2 = g.new_pools(S, poison=False)
     slots = rng.permutation(S)[:batch].astype(np.int32)
