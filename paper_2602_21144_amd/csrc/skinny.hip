@@ -1046,14 +1046,14 @@ template <int ROLE, bool CONV = false>
 hipError_t launch_f32_stream_role(int M, int N, int K, const float* A, int64_t lda, const float* B, int64_t ldb,
                                   float* C, int64_t ldc, hipStream_t s, const F32ConvEpi& cv = {}) {
     // few column tiles (x_proj: 16): 16 waves, so that each wave's run of K stays short; more
-    // than 16 rows are cut into 16-row tiles along the grid's second dimension, so that more
-    // CUs share the stream and each reads 16 activation rows instead of all of them (the
-    // hybrid shard's x_proj of 64 rows: 16 workgroups each reading 64 activation rows of
-    // 14 KB took 14 us)
+    // than 8 rows are cut into 8-row tiles along the grid's second dimension, so that more
+    // CUs share the stream and each reads 8 activation rows instead of all of them (the
+    // hybrid shard's x_proj of 64 rows: 16 workgroups each reading all 64 rows took 14 us,
+    // 64 of 16-row tiles 9.1 us, 128 of 8-row tiles 8.1 us)
     if ((N + 15) / 16 < 128) {
-        if (M <= 16) return launch_f32_stream_nw<ROLE, 16, CONV>(M, N, K, A, lda, B, ldb, C, ldc, s, cv);
-        const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 15) / 16)), block(16 * 64);
-        SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, 16, 3, 2, 1, CONV>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv);
+        if (M <= 8) return launch_f32_stream_nw<ROLE, 16, CONV>(M, N, K, A, lda, B, ldb, C, ldc, s, cv);
+        const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 7) / 8)), block(16 * 64);
+        SSM_LAUNCH((gemv_f32_stream_kernel<ROLE, 16, 3, 1, 1, CONV>), grid, block, 0, s, M, N, K, A, lda, B, ldb, C, ldc, cv);
         return hipGetLastError();
     }
     return launch_f32_stream_nw<ROLE, 8, CONV>(M, N, K, A, lda, B, ldb, C, ldc, s, cv);
