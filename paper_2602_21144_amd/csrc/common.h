@@ -247,6 +247,7 @@ struct ScanArgs {
     const void* w_dt;
     // scan scratch (prefill only)
     float* h_local; float* sum_delta; float* h_in; float* h0_seq;
+    float* delta;                                                  // [T][E]: Delta of every token
     int64_t T; int E, nseq, S, win;                                // win: tokens per window
 };
 int scan_window_len(int64_t T, int E);

@@ -7,13 +7,16 @@
 //                             y_t = sum_n C_t[n] h_t[n] + D u_t ;  g_t = y_t * SiLU(z_t)
 //
 // Layout on gfx950: one lane per channel, its 16 fp32 states in VGPRs; B_t and C_t are
-// the same for every channel of a token, so a wave reads them with scalar loads. The
+// the same for every channel of a token, so a workgroup stages them once per block of
+// tokens in LDS and every lane reads them as broadcasts. The
 // packed token range is cut into windows of `win` tokens so that there are enough
 // waves for the 1024 SIMDs: pass A computes, for each window whose last sequence runs
 // on into the next window, that piece's end state from a zero start (and its sum of
 // Delta); pass B links windows in order per (channel, state) -- the state entering
 // window j+1 is exp(A * sum Delta_j) * (state entering j) + local end state of j; pass C
 // runs the full recurrence from the linked state and writes g and the final states.
+// Pass A also stores Delta of every token of its window (it needs Delta for most of
+// them anyway), so pass C reads it and runs no softplus.
 // Initial states of continuing sequences are copied out of the pool in pass A, so pass
 // C (which writes final states into the pool) never reads a slot another pass writes.
 #include "common.h"
@@ -45,17 +48,23 @@ int64_t target_windows(int E) { return std::max<int64_t>(1, (int64_t)kTargetWave
 
 constexpr int kTB = 8;  // tokens per block: loads for block i+1 are in flight while block i computes
 
-// Per-lane activations of one block of tokens, prefetched a block ahead.
-template <typename T, bool WITH_Z>
+// Per-lane activations of one block of tokens, prefetched a block ahead: u and dt for
+// pass A; u, the stored Delta and z for pass C.
+template <typename T, bool MAIN>
 struct TokBlock {
-    T u[kTB], dt[kTB], z[WITH_Z ? kTB : 1];
+    T u[kTB], dt[MAIN ? 1 : kTB], z[MAIN ? kTB : 1];
+    float delta[MAIN ? kTB : 1];
     __device__ __forceinline__ void load(const ScanArgs& a, int64_t b0, int64_t w1, int c) {
 #pragma unroll
         for (int i = 0; i < kTB; ++i) {
             const int64_t t = b0 + i < w1 ? b0 + i : w1 - 1;  // clamp: tail entries are never used
             u[i] = ((const T*)a.u)[t * a.E + c];
-            dt[i] = ((const T*)a.dt)[t * a.E + c];
-            if constexpr (WITH_Z) z[i] = ((const T*)a.z)[t * a.ld_z + c];
+            if constexpr (MAIN) {
+                delta[i] = a.delta[t * a.E + c];
+                z[i] = ((const T*)a.z)[t * a.ld_z + c];
+            } else {
+                dt[i] = ((const T*)a.dt)[t * a.E + c];
+            }
         }
     }
 };
@@ -120,6 +129,22 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
         load_h(h, a.pool + ((int64_t)slot * a.E + c) * kN);
         store_h(a.h0_seq + ((int64_t)s * a.E + c) * kN, h);
     }
+
+    // Delta of the tokens before the piece whose recurrence runs here (all of them when
+    // no piece carries out of the window)
+    const float bdt = a.b_dt[c];
+    const int64_t t0 = !carry_out ? w1 : last_cont ? w0 : b_last;
+    for (int64_t b0 = w0; b0 < t0; b0 += kTB) {
+        T dtv[kTB];
+#pragma unroll
+        for (int i = 0; i < kTB; ++i) {
+            const int64_t t = b0 + i < t0 ? b0 + i : t0 - 1;
+            dtv[i] = ((const T*)a.dt)[t * a.E + c];
+        }
+#pragma unroll
+        for (int i = 0; i < kTB; ++i)
+            if (b0 + i < t0) a.delta[(b0 + i) * a.E + c] = softplus_f(to_f32(dtv[i]) + bdt);
+    }
     if (!carry_out) return;
 
     // local end state of the last piece: from zero if it continues an earlier window,
@@ -127,8 +152,6 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
     float A2[kN], h[kN];
 #pragma unroll
     for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
-    const float bdt = a.b_dt[c];
-    const int64_t t0 = last_cont ? w0 : b_last;
     if (!last_cont && a.has_init[s_last]) {
         const int slot = uni(a.slot[s_last]);
         if (slot >= 0 && slot < a.S) load_h(h, a.pool + ((int64_t)slot * a.E + c) * kN);
@@ -157,6 +180,7 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
         const int nt = rows_upto(w1 - b0, kTB);
         auto step = [&](int i) {
             const float delta = softplus_f(to_f32(cur.dt[i]) + bdt);
+            a.delta[(b0 + i) * a.E + c] = delta;
             const float du = delta * to_f32(cur.u[i]);
             sum_delta += delta;
 #pragma unroll
@@ -179,37 +203,84 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
 }
 
 // ---------------------------------------------------------------- pass B
-// One lane per (channel, state): walk the windows in order carrying the state across
-// window boundaries of continuing sequences. Also clears the state of empty sequences
-// that start fresh (their final state is the zero initial state).
-__global__ __launch_bounds__(256) void scan_link_kernel(ScanArgs a, int nwin, const int32_t* wflags) {
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= (int64_t)a.E * kN) return;
-    const int c = (int)(gid / kN), n = (int)(gid % kN);
+// Window j maps the state carried across its start to the one carried across its end by
+// x -> m x + l: (exp(A * sum Delta_j), local end state) when its last piece continues from
+// its start, (0, local end state) when that piece starts inside it, (1, 0) when nothing
+// carries out. The windows of a (channel, state) are cut into kLinkSeg ranges, one lane
+// each: a lane composes its range's maps, takes its entry state from the composites of
+// the ranges before it (through LDS), then walks its range again from that entry, writing
+// the linked entry state of every window whose first token continues a sequence. The
+// serial chain is thus one range long instead of all windows. Also clears the state of
+// empty sequences that start fresh (their final state is the zero initial state).
+constexpr int kLinkSeg = 8;     // ranges per (channel, state): one wave each
+constexpr int kLinkPairs = 64;  // (channel, state) pairs per workgroup: one per lane
+constexpr int kLB = 16;         // windows fetched at a time, so that only the chain itself is serial
+
+__global__ __launch_bounds__(kLinkSeg * kLinkPairs) void scan_link_kernel(ScanArgs a, int nwin,
+                                                                          const int32_t* wflags) {
+    __shared__ float cm[kLinkSeg][kLinkPairs], cl[kLinkSeg][kLinkPairs];
+    const int p = threadIdx.x % kLinkPairs, r = uni(threadIdx.x / kLinkPairs);
+    const int64_t pair = (int64_t)blockIdx.x * kLinkPairs + p;
+    const bool live = pair < (int64_t)a.E * kN;
+    const int c = live ? (int)(pair / kN) : 0, n = live ? (int)(pair % kN) : 0;
     const float A2 = -__expf(a.A_log[c * kN + n]) * kLog2e;
-    // the windows' local values are fetched kLB at a time, so that only the carry chain
-    // itself is serial (entries of windows without a carry are never written by pass A
-    // and are read but not used)
-    constexpr int kLB = 16;
-    float carry = 0.0f;
-    for (int j0 = 0; j0 < nwin; j0 += kLB) {
-        float hl[kLB], sd[kLB];
+    const int per = (nwin + kLinkSeg - 1) / kLinkSeg;
+    const int j_beg = min(r * per, nwin), j_end = min(j_beg + per, nwin);
+
+    // one batch of the range's windows: flags, decay exp(A * sum Delta) and local end
+    // state (entries of windows without a carry are never written by pass A and are read
+    // but not used)
+    int fl[kLB];
+    float dd[kLB], hl[kLB];
+    auto fetch = [&](int j0) {
 #pragma unroll
         for (int q = 0; q < kLB; ++q) {
-            const int64_t j = min(j0 + q, nwin - 1);
+            if (j0 + q >= j_end) break;
+            const int64_t j = j0 + q;
+            fl[q] = wflags[j];
             hl[q] = a.h_local[(j * a.E + c) * kN + n];
-            sd[q] = a.sum_delta[j * a.E + c];
+            dd[q] = a.sum_delta[j * a.E + c];
         }
 #pragma unroll
         for (int q = 0; q < kLB; ++q) {
-            const int j = j0 + q;
-            if (j >= nwin) break;
-            const int f = wflags[j];
-            if (f & kFlagContIn) a.h_in[((int64_t)j * a.E + c) * kN + n] = carry;
-            if (f & kFlagCarryOut) carry = (f & kFlagLastCont) ? fast_exp2(sd[q] * A2) * carry + hl[q] : hl[q];
+            if (j0 + q >= j_end) break;
+            dd[q] = fast_exp2(dd[q] * A2);
+        }
+    };
+
+    // this range's composite map
+    float m = 1.0f, l = 0.0f;
+    for (int j0 = j_beg; j0 < j_end; j0 += kLB) {
+        fetch(j0);
+#pragma unroll
+        for (int q = 0; q < kLB; ++q) {
+            if (j0 + q >= j_end) break;
+            if (fl[q] & kFlagCarryOut) {
+                if (fl[q] & kFlagLastCont) { m *= dd[q]; l = dd[q] * l + hl[q]; }
+                else { m = 0.0f; l = hl[q]; }
+            }
         }
     }
-    for (int s = 0; s < a.nseq; ++s) {
+    cm[r][p] = m;
+    cl[r][p] = l;
+    __syncthreads();
+    float carry = 0.0f;
+    for (int q = 0; q < r; ++q) carry = cm[q][p] * carry + cl[q][p];
+
+    // walk the range again from its entry (a range of one batch still holds it)
+    const bool refetch = j_end - j_beg > kLB;
+    for (int j0 = j_beg; j0 < j_end; j0 += kLB) {
+        if (refetch) fetch(j0);
+#pragma unroll
+        for (int q = 0; q < kLB; ++q) {
+            if (j0 + q >= j_end) break;
+            if ((fl[q] & kFlagContIn) && live) a.h_in[((int64_t)(j0 + q) * a.E + c) * kN + n] = carry;
+            if (fl[q] & kFlagCarryOut) carry = (fl[q] & kFlagLastCont) ? dd[q] * carry + hl[q] : hl[q];
+        }
+    }
+
+    if (!live) return;
+    for (int s = r; s < a.nseq; s += kLinkSeg) {  // the ranges' waves share the sequences
         if (a.cu[s + 1] != a.cu[s] || a.has_init[s]) continue;
         const int slot = a.slot[s];
         if (slot < 0 || slot >= a.S) continue;
@@ -219,9 +290,8 @@ __global__ __launch_bounds__(256) void scan_link_kernel(ScanArgs a, int nwin, co
 
 // ---------------------------------------------------------------- pass C
 // One token of the full recurrence for this lane's channel; returns g.
-__device__ __forceinline__ float token_step(float* h, const float* A2, float u, float dt, float z, float bdt, float Dc,
+__device__ __forceinline__ float token_step(float* h, const float* A2, float u, float delta, float z, float Dc,
                                             const float* bcrow) {
-    const float delta = softplus_f(dt + bdt);
     const float du = delta * u;
     float y = 0.0f;
 #pragma unroll
@@ -244,7 +314,7 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
     float A2[kN], h[kN];
 #pragma unroll
     for (int n = 0; n < kN; ++n) A2[n] = -__expf(a.A_log[c * kN + n]) * kLog2e;
-    const float bdt = a.b_dt[c], Dc = a.D[c];
+    const float Dc = a.D[c];
     T* g = (T*)a.g;
 
     // the sequence holding the first token, and the state entering the window
@@ -279,8 +349,8 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
             // no sequence ends inside this block: straight-line recurrence from registers
             // (a whole block without per-token guards, so the states stay in place)
             auto step = [&](int i) {
-                g[(b0 + i) * a.E + c] = from_f32<T>(token_step(h, A2, to_f32(cur.u[i]), to_f32(cur.dt[i]),
-                                                               to_f32(cur.z[i]), bdt, Dc, bc[buf][i]));
+                g[(b0 + i) * a.E + c] = from_f32<T>(token_step(h, A2, to_f32(cur.u[i]), cur.delta[i],
+                                                               to_f32(cur.z[i]), Dc, bc[buf][i]));
             };
             if (nt == kTB) {
 #pragma unroll
@@ -319,9 +389,9 @@ __global__ __launch_bounds__(kWave * CW) void scan_main_kernel(ScanArgs a) {
                 }
                 if (!ok) break;
                 const float u = to_f32(((const T*)a.u)[t * a.E + c]);
-                const float dt = to_f32(((const T*)a.dt)[t * a.E + c]);
+                const float delta = a.delta[t * a.E + c];
                 const float z = to_f32(((const T*)a.z)[t * a.ld_z + c]);
-                g[t * a.E + c] = from_f32<T>(token_step(h, A2, u, dt, z, bdt, Dc, bc[buf][i]));
+                g[t * a.E + c] = from_f32<T>(token_step(h, A2, u, delta, z, Dc, bc[buf][i]));
             }
         }
         if (more) st.store(bc[buf ^ 1], tid);
@@ -646,7 +716,7 @@ static int64_t max_windows(int64_t max_T, int E) {
 
 // Scratch regions of the windowed scan, in order: local end states [nwin][E][N],
 // sums of Delta [nwin][E], linked entry states [nwin][E][N], copied initial states
-// [nseq][E][N], window flags [nwin].
+// [nseq][E][N], window flags [nwin], Delta [T][E].
 static size_t scan_layout(char* base, int64_t T, int E, int nseq, int nwin, ScanArgs* a, int32_t** wflags) {
     size_t off = 0;
     auto take = [&](size_t bytes) { char* p = base ? base + off : nullptr; off += align256(bytes); return p; };
@@ -655,11 +725,12 @@ static size_t scan_layout(char* base, int64_t T, int E, int nseq, int nwin, Scan
     char* hi = take((size_t)nwin * E * kN * 4);
     char* h0 = take((size_t)std::max(nseq, 1) * E * kN * 4);
     char* wf = take((size_t)std::max(nwin, 1) * 4);
+    char* dl = take((size_t)std::max<int64_t>(T, 1) * E * 4);
     if (a) {
         a->h_local = (float*)hl; a->sum_delta = (float*)sd; a->h_in = (float*)hi; a->h0_seq = (float*)h0;
+        a->delta = (float*)dl;
     }
     if (wflags) *wflags = (int32_t*)wf;
-    (void)T;
     return off;
 }
 
@@ -688,8 +759,9 @@ hipError_t launch_scan_prefill(const ScanArgs& a0, bool bf, hipStream_t s) {
     }
     {
         KernelTimer kt("prefill.scan_link", s);
-        const int64_t lanes = (int64_t)a.E * kN;
-        SSM_LAUNCH(scan_link_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, nwin,
+        const int64_t pairs = (int64_t)a.E * kN;
+        SSM_LAUNCH(scan_link_kernel, dim3((unsigned)((pairs + kLinkPairs - 1) / kLinkPairs)),
+                   dim3(kLinkSeg * kLinkPairs), 0, s, a, nwin,
                            (const int32_t*)wflags);
     }
     if (nwin > 0) {

@@ -327,12 +327,13 @@ def test_selective_scan(B, act, E, lens):
 
 
 @pytest.mark.parametrize("act", ["f32", "bf16"])
-def test_selective_scan_long_sequence_many_windows(B, act):
-    """One long sequence crossing ~100 windows: exercises the window-to-window state links."""
-    rng = np.random.default_rng(99)
+@pytest.mark.parametrize("T", [3333, 9001])
+def test_selective_scan_long_sequence_many_windows(B, act, T):
+    """One long sequence crossing ~100 (~280) windows: exercises the window-to-window state
+    links, with each of the link pass's ranges one (several, the last ragged) fetch batches long."""
+    rng = np.random.default_rng(99 + T)
     shape = synth.LayerShape(64, 64, 16, 16, 4, 1, act)
     E, N, R = 64, 16, 16
-    T = 3333
     u, dt, xz, xdbl = _scan_inputs(rng, T, E, R, act)
     dt = (dt - 2.0).astype(np.float32)        # small steps: long memory across windows
     if act == "bf16":
