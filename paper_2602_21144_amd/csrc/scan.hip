@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kWave * CW) void scan_local_kernel(ScanArgs a, int 
 // empty sequences that start fresh (their final state is the zero initial state).
 constexpr int kLinkSeg = 8;     // ranges per (channel, state): one wave each
 constexpr int kLinkPairs = 64;  // (channel, state) pairs per workgroup: one per lane
-constexpr int kLB = 16;         // windows fetched at a time, so that only the chain itself is serial
+constexpr int kLB = 8;          // windows fetched at a time, so that only the chain itself is serial
 
 __global__ __launch_bounds__(kLinkSeg * kLinkPairs) void scan_link_kernel(ScanArgs a, int nwin,
                                                                           const int32_t* wflags) {
